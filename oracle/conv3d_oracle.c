@@ -1,0 +1,409 @@
+/*
+ * Reference oracle for the cached causal Conv3D -- TEST INFRASTRUCTURE ONLY.
+ *
+ * Only the test suite, the smoke check and the benchmark's CPU-baseline leg
+ * may load this library.  It shares no code, header, table or helper with the
+ * HIP library; it is written from the paper ("Cache-Aware Conv3D Lowering
+ * Across Embedded World-Model Decoders", Sec. 4) and from the plain
+ * definition of a zero-padded cross-correlation.
+ *
+ * What it computes (all in fp64, inputs widened exactly):
+ *
+ *   Z      = [C ; X]_T              cache frames first, then the new chunk
+ *                                   (Sec. 4.2, Z = [C;X]_T)
+ *   p_l    = p_base - |C|_T         effective left temporal pad (Sec. 4.2)
+ *   T_o    = floor((|Z| + p_l + p_r - d_t (K_t - 1) - 1) / s_t) + 1   (Eq. 3)
+ *   H_o, W_o: the same formula with the spatial stride / pad / dilation
+ *   y[n,co,t,h,w] = sum_{ci in group(co)} sum_{k,i,j}
+ *                     W[co, ci - g0, k, i, j] *
+ *                     Zhat[n, ci, t s_t + k d_t - p_l,
+ *                                 h s_h + i d_h - p_h,
+ *                                 w s_w + j d_w - p_w]
+ *                   + b[co]                       (bias added once, last)
+ *   where Zhat is Z inside its range and 0 outside, in all three dims
+ *   (Eq. 1 gives the temporal source index, Eq. 2 the tap sum).
+ *
+ *   cache' = the last L = min(p_base, |Z|) frames of Z (a byte copy).  The
+ *   paper leaves the cache rule to the decoder; this is the reading that
+ *   makes chunked streaming equal one whole-sequence causal convolution.
+ *
+ * The per-tap valid interval of Eq. 4 and the output length of Eq. 3 are
+ * also exported, written from the formulas, so that tests can compare them
+ * with brute-force enumeration.
+ *
+ * The route rule (which calls the lowered fast route accepts) is the written
+ * guard of Alg. 1 plus two clauses of this library's fast-kernel contract
+ * (K_t >= 2, and a 3x3 / stride 1 / pad 1 / dilation 1 spatial kernel).
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+typedef struct {
+  int64_t N, Ci, Co, T, Tc, H, W, Kt, Kh, Kw;
+  int64_t s_t, s_h, s_w; /* stride */
+  int64_t d_t, d_h, d_w; /* dilation */
+  int64_t p_base;        /* p_l^base: temporal left pad before the cache */
+  int64_t p_r;           /* temporal right pad */
+  int64_t p_h, p_w;      /* spatial pad (both sides) */
+  int64_t groups;
+  int64_t has_bias;
+} ora_desc;
+
+/* element types the oracle can read; they are widened exactly to fp64 */
+enum { ORA_F64 = 0, ORA_F32 = 1, ORA_BF16 = 2, ORA_F16 = 3 };
+
+/* route reasons, in the order the clauses are tested */
+enum {
+  ORA_OK = 0,
+  ORA_FORCED = 1,
+  ORA_DTYPE = 2,
+  ORA_GROUPS = 3,
+  ORA_STRIDE_T = 4,
+  ORA_PAD_RIGHT = 5,
+  ORA_NO_OUTPUT = 6,
+  ORA_NO_TAP = 7,
+  ORA_KT1 = 8,
+  ORA_SPATIAL = 9
+};
+
+static int64_t floordiv(int64_t a, int64_t b) {
+  int64_t q = a / b;
+  if ((a % b != 0) && ((a < 0) != (b < 0))) q -= 1;
+  return q;
+}
+
+/* Eq. 3 for time, and the same closed form for one spatial axis. */
+static int64_t out_len(int64_t in, int64_t pad_lo, int64_t pad_hi, int64_t dil,
+                       int64_t k, int64_t stride) {
+  return floordiv(in + pad_lo + pad_hi - dil * (k - 1) - 1, stride) + 1;
+}
+
+static int valid_desc(const ora_desc* d) {
+  if (!d) return 0;
+  if (d->N < 1 || d->Ci < 1 || d->Co < 1 || d->H < 1 || d->W < 1) return 0;
+  if (d->Kt < 1 || d->Kh < 1 || d->Kw < 1) return 0;
+  if (d->T < 0 || d->Tc < 0 || d->p_base < 0 || d->p_h < 0 || d->p_w < 0) return 0;
+  if (d->s_t < 1 || d->s_h < 1 || d->s_w < 1) return 0;
+  if (d->d_t < 1 || d->d_h < 1 || d->d_w < 1) return 0;
+  if (d->groups < 1 || d->Ci % d->groups || d->Co % d->groups) return 0;
+  if (out_len(d->H, d->p_h, d->p_h, d->d_h, d->Kh, d->s_h) < 1) return 0;
+  if (out_len(d->W, d->p_w, d->p_w, d->d_w, d->Kw, d->s_w) < 1) return 0;
+  return 1;
+}
+
+int ora_output_dims(const ora_desc* d, int64_t* To, int64_t* Ho, int64_t* Wo,
+                    int64_t* L) {
+  if (!valid_desc(d)) return -1;
+  int64_t Z = d->Tc + d->T;
+  int64_t p_l = d->p_base - d->Tc;
+  int64_t to = out_len(Z, p_l, d->p_r, d->d_t, d->Kt, d->s_t);
+  if (To) *To = to < 0 ? 0 : to;
+  if (Ho) *Ho = out_len(d->H, d->p_h, d->p_h, d->d_h, d->Kh, d->s_h);
+  if (Wo) *Wo = out_len(d->W, d->p_w, d->p_w, d->d_w, d->Kw, d->s_w);
+  if (L) *L = d->p_base < Z ? d->p_base : Z;
+  return 0;
+}
+
+/* Eq. 4: for tap k, output frames o in [o_l, o_h) read source frame
+ * o + delta_k with delta_k = k d_t - p_l (unit temporal stride). */
+int ora_tap_interval(const ora_desc* d, int64_t k, int64_t* o_l, int64_t* o_h) {
+  int64_t To;
+  if (ora_output_dims(d, &To, NULL, NULL, NULL)) return -1;
+  if (k < 0 || k >= d->Kt) return -1;
+  int64_t Z = d->Tc + d->T;
+  int64_t p_l = d->p_base - d->Tc;
+  int64_t delta = k * d->d_t - p_l;
+  int64_t lo = -delta > 0 ? -delta : 0;
+  int64_t hi = Z - delta < To ? Z - delta : To;
+  *o_l = lo;
+  *o_h = hi;
+  return 0;
+}
+
+/* Fast-route predicate: 0 = fast, 1 = fallback; *reason = first failing
+ * clause.  dtype_ok says whether the element type has a fast kernel
+ * (bf16 and fp32 do). */
+int ora_route(const ora_desc* d, int dtype_ok, int force_fallback, int* route,
+              int* reason) {
+  int64_t To;
+  if (ora_output_dims(d, &To, NULL, NULL, NULL)) return -1;
+  int r = ORA_OK;
+  if (force_fallback)
+    r = ORA_FORCED;
+  else if (!dtype_ok)
+    r = ORA_DTYPE;
+  else if (d->groups != 1)
+    r = ORA_GROUPS;
+  else if (d->s_t != 1)
+    r = ORA_STRIDE_T;
+  else if (d->p_r < 0)
+    r = ORA_PAD_RIGHT;
+  else if (To < 1)
+    r = ORA_NO_OUTPUT;
+  else {
+    int any = 0;
+    for (int64_t k = 0; k < d->Kt; ++k) {
+      int64_t lo, hi;
+      ora_tap_interval(d, k, &lo, &hi);
+      if (lo < hi) any = 1;
+    }
+    if (!any)
+      r = ORA_NO_TAP;
+    else if (d->Kt < 2)
+      r = ORA_KT1;
+    else if (!(d->Kh == 3 && d->Kw == 3 && d->s_h == 1 && d->s_w == 1 &&
+               d->p_h == 1 && d->p_w == 1 && d->d_h == 1 && d->d_w == 1))
+      r = ORA_SPATIAL;
+  }
+  *route = (r == ORA_OK) ? 0 : 1;
+  *reason = r;
+  return 0;
+}
+
+/* exact widening of one element */
+static double widen(const void* p, int dtype, int64_t i) {
+  switch (dtype) {
+    case ORA_F64:
+      return ((const double*)p)[i];
+    case ORA_F32:
+      return (double)((const float*)p)[i];
+    case ORA_BF16: {
+      uint32_t u = (uint32_t)((const uint16_t*)p)[i] << 16;
+      float f;
+      memcpy(&f, &u, sizeof f);
+      return (double)f;
+    }
+    default: { /* IEEE binary16 */
+      uint16_t h = ((const uint16_t*)p)[i];
+      int sign = (h >> 15) & 1, ex = (h >> 10) & 0x1f, man = h & 0x3ff;
+      double v;
+      if (ex == 0)
+        v = ldexp((double)man, -24);
+      else if (ex == 31)
+        v = man ? NAN : INFINITY;
+      else
+        v = ldexp((double)(man | 0x400), ex - 25);
+      return sign ? -v : v;
+    }
+  }
+}
+
+static size_t elem_size(int dtype) {
+  return dtype == ORA_F64 ? 8 : dtype == ORA_F32 ? 4 : 2;
+}
+
+/* Frame f of Z: cache frame f when f < |C|, else chunk frame f - |C|.
+ * Returns the base pointer and the element offset of Z[n, c, f, 0, 0]. */
+static const void* z_frame(const ora_desc* d, const void* x, const void* cache,
+                           int64_t n, int64_t c, int64_t f, int64_t* off) {
+  int64_t hw = d->H * d->W;
+  if (f < d->Tc) {
+    *off = ((n * d->Ci + c) * d->Tc + f) * hw;
+    return cache;
+  }
+  *off = ((n * d->Ci + c) * d->T + (f - d->Tc)) * hw;
+  return x;
+}
+
+/* One output row y[n, co, t, h, 0:W_o], accumulated in fp64.
+ * zrow is scratch of W doubles, acc of W_o doubles. */
+static void one_row(const ora_desc* d, int dtype, const void* x,
+                    const void* cache, const double* wd, const double* bd,
+                    int64_t To, int64_t Ho, int64_t Wo, int64_t n, int64_t co,
+                    int64_t t, int64_t h, double* zrow, double* acc) {
+  int64_t Z = d->Tc + d->T;
+  int64_t p_l = d->p_base - d->Tc;
+  int64_t cig = d->Ci / d->groups, cog = d->Co / d->groups;
+  int64_t g0 = (co / cog) * cig;
+  (void)To;
+  (void)Ho;
+  for (int64_t w = 0; w < Wo; ++w) acc[w] = 0.0;
+  for (int64_t c = 0; c < cig; ++c) {
+    for (int64_t k = 0; k < d->Kt; ++k) {
+      int64_t tz = t * d->s_t + k * d->d_t - p_l; /* Eq. 1 */
+      if (tz < 0 || tz >= Z) continue;
+      for (int64_t i = 0; i < d->Kh; ++i) {
+        int64_t hz = h * d->s_h + i * d->d_h - d->p_h;
+        if (hz < 0 || hz >= d->H) continue;
+        int64_t off;
+        const void* base = z_frame(d, x, cache, n, g0 + c, tz, &off);
+        off += hz * d->W;
+        for (int64_t q = 0; q < d->W; ++q) zrow[q] = widen(base, dtype, off + q);
+        for (int64_t j = 0; j < d->Kw; ++j) {
+          double wv = wd[(((co * cig + c) * d->Kt + k) * d->Kh + i) * d->Kw + j];
+          int64_t shift = j * d->d_w - d->p_w;
+          /* output columns w whose source column w s_w + shift is in range */
+          for (int64_t w = 0; w < Wo; ++w) {
+            int64_t wz = w * d->s_w + shift;
+            if (wz >= 0 && wz < d->W) acc[w] += wv * zrow[wz];
+          }
+        }
+      }
+    }
+  }
+  if (d->has_bias)
+    for (int64_t w = 0; w < Wo; ++w) acc[w] += bd[co];
+}
+
+static double* widen_all(const void* p, int dtype, int64_t n) {
+  double* out = (double*)malloc((size_t)(n > 0 ? n : 1) * sizeof(double));
+  if (!out) return NULL;
+  for (int64_t i = 0; i < n; ++i) out[i] = widen(p, dtype, i);
+  return out;
+}
+
+/* Output rows [row0, row1) of the flattened (n, co, t, h) row space, which is
+ * the NCTHW output order; y receives (row1 - row0) * W_o doubles. */
+int ora_conv3d_rows(const ora_desc* d, int dtype, const void* x,
+                    const void* cache, const void* w, const void* b,
+                    int64_t row0, int64_t row1, double* y) {
+  int64_t To, Ho, Wo;
+  if (ora_output_dims(d, &To, &Ho, &Wo, NULL)) return -1;
+  int64_t nrows = d->N * d->Co * To * Ho;
+  if (row0 < 0 || row1 < row0 || row1 > nrows) return -1;
+  if (row1 == row0) return 0;
+  if (!y || !w || (d->T > 0 && !x) || (d->Tc > 0 && !cache)) return -1;
+  if (d->has_bias && !b) return -1;
+  int64_t nw = d->Co * (d->Ci / d->groups) * d->Kt * d->Kh * d->Kw;
+  double* wd = widen_all(w, dtype, nw);
+  double* bd = widen_all(b, dtype, d->has_bias ? d->Co : 0);
+  if (!wd || !bd) {
+    free(wd);
+    free(bd);
+    return -2;
+  }
+  int err = 0;
+#pragma omp parallel
+  {
+    double* zrow = (double*)malloc((size_t)d->W * sizeof(double));
+    double* acc = (double*)malloc((size_t)Wo * sizeof(double));
+    if (!zrow || !acc) {
+#pragma omp atomic write
+      err = -2;
+    } else {
+#pragma omp for schedule(dynamic, 4)
+      for (int64_t r = row0; r < row1; ++r) {
+        int64_t h = r % Ho, rest = r / Ho;
+        int64_t t = rest % To;
+        rest /= To;
+        int64_t co = rest % d->Co, n = rest / d->Co;
+        one_row(d, dtype, x, cache, wd, bd, To, Ho, Wo, n, co, t, h, zrow, acc);
+        memcpy(y + (r - row0) * Wo, acc, (size_t)Wo * sizeof(double));
+      }
+    }
+    free(zrow);
+    free(acc);
+  }
+  free(wd);
+  free(bd);
+  return err;
+}
+
+/* The whole output y [N][Co][T_o][H_o][W_o] in fp64. */
+int ora_conv3d(const ora_desc* d, int dtype, const void* x, const void* cache,
+               const void* w, const void* b, double* y) {
+  int64_t To, Ho;
+  if (ora_output_dims(d, &To, &Ho, NULL, NULL)) return -1;
+  return ora_conv3d_rows(d, dtype, x, cache, w, b, 0, d->N * d->Co * To * Ho, y);
+}
+
+/* Selected output elements, by flat NCTHW index, each summed on its own. */
+int ora_conv3d_points(const ora_desc* d, int dtype, const void* x,
+                      const void* cache, const void* w, const void* b,
+                      int64_t npts, const int64_t* idx, double* out) {
+  int64_t To, Ho, Wo;
+  if (ora_output_dims(d, &To, &Ho, &Wo, NULL)) return -1;
+  int64_t total = d->N * d->Co * To * Ho * Wo;
+  if (npts < 0 || (npts > 0 && (!idx || !out || !w))) return -1;
+  if (d->has_bias && !b) return -1;
+  for (int64_t p = 0; p < npts; ++p)
+    if (idx[p] < 0 || idx[p] >= total) return -1;
+  int64_t Z = d->Tc + d->T;
+  int64_t p_l = d->p_base - d->Tc;
+  int64_t cig = d->Ci / d->groups, cog = d->Co / d->groups;
+#pragma omp parallel for schedule(dynamic, 16)
+  for (int64_t p = 0; p < npts; ++p) {
+    int64_t r = idx[p];
+    int64_t wo = r % Wo;
+    r /= Wo;
+    int64_t h = r % Ho;
+    r /= Ho;
+    int64_t t = r % To;
+    r /= To;
+    int64_t co = r % d->Co, n = r / d->Co;
+    int64_t g0 = (co / cog) * cig;
+    double acc = 0.0;
+    for (int64_t c = 0; c < cig; ++c)
+      for (int64_t k = 0; k < d->Kt; ++k) {
+        int64_t tz = t * d->s_t + k * d->d_t - p_l;
+        if (tz < 0 || tz >= Z) continue;
+        for (int64_t i = 0; i < d->Kh; ++i) {
+          int64_t hz = h * d->s_h + i * d->d_h - d->p_h;
+          if (hz < 0 || hz >= d->H) continue;
+          for (int64_t j = 0; j < d->Kw; ++j) {
+            int64_t wz = wo * d->s_w + j * d->d_w - d->p_w;
+            if (wz < 0 || wz >= d->W) continue;
+            int64_t off;
+            const void* base = z_frame(d, x, cache, n, g0 + c, tz, &off);
+            double zv = widen(base, dtype, off + hz * d->W + wz);
+            double wv =
+                widen(w, dtype, (((co * cig + c) * d->Kt + k) * d->Kh + i) * d->Kw + j);
+            acc += wv * zv;
+          }
+        }
+      }
+    if (d->has_bias) acc += widen(b, dtype, co);
+    out[p] = acc;
+  }
+  return 0;
+}
+
+/* cache' = last L frames of Z, copied byte for byte into [N][Ci][L][H][W]. */
+int ora_cache_update(const ora_desc* d, int dtype, const void* x,
+                     const void* cache, void* cache_out) {
+  int64_t L;
+  if (ora_output_dims(d, NULL, NULL, NULL, &L)) return -1;
+  if (L == 0) return 0;
+  if (!cache_out || (d->T > 0 && !x) || (d->Tc > 0 && !cache)) return -1;
+  size_t es = elem_size(dtype);
+  int64_t Z = d->Tc + d->T, hw = d->H * d->W;
+  for (int64_t n = 0; n < d->N; ++n)
+    for (int64_t c = 0; c < d->Ci; ++c)
+      for (int64_t j = 0; j < L; ++j) {
+        int64_t off;
+        const void* base = z_frame(d, x, cache, n, c, Z - L + j, &off);
+        memcpy((char*)cache_out + (size_t)(((n * d->Ci + c) * L + j) * hw) * es,
+               (const char*)base + (size_t)off * es, (size_t)hw * es);
+      }
+  return 0;
+}
+
+/* Algorithmic FLOP of one call: 2 * N * Co * (Ci/g) * Kh * Kw * H_o * W_o
+ * times the number of valid (output frame, tap) pairs, counted by brute
+ * force over the output frames (not through Eq. 4). */
+double ora_flops(const ora_desc* d) {
+  int64_t To, Ho, Wo;
+  if (ora_output_dims(d, &To, &Ho, &Wo, NULL)) return -1.0;
+  int64_t Z = d->Tc + d->T, p_l = d->p_base - d->Tc, pairs = 0;
+  for (int64_t t = 0; t < To; ++t)
+    for (int64_t k = 0; k < d->Kt; ++k) {
+      int64_t tz = t * d->s_t + k * d->d_t - p_l;
+      if (tz >= 0 && tz < Z) ++pairs;
+    }
+  return 2.0 * (double)d->N * (double)d->Co * (double)(d->Ci / d->groups) *
+         (double)d->Kh * (double)d->Kw * (double)Ho * (double)Wo * (double)pairs;
+}
+
+int ora_num_threads(void) {
+#ifdef _OPENMP
+  return omp_get_max_threads();
+#else
+  return 1;
+#endif
+}

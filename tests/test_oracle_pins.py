@@ -1,0 +1,471 @@
+"""Pins for the CPU oracle: each check compares it with something other than
+itself -- an independent library routine (torch's conv3d in fp64), brute
+force on tiny inputs, closed forms, special cases that reduce to textbook
+routines (a matmul, a 1-D FIR), and invariants of the method (bias once,
+linearity, chunked streaming with a carried cache == one whole-sequence
+causal convolution, the interval algebra of Eq. 3 and Eq. 4).
+
+A plausible slip in the oracle -- a dropped tap, a wrong sign in the source
+frame index, the cache frames in the wrong order, the bias added per tap, a
+transposed weight index -- makes at least one of these fail.
+"""
+import itertools
+import math
+
+import numpy as np
+import pytest
+import torch
+import torch.nn.functional as F
+
+import oracle
+from paper_2609_31938_amd.inputs import spec
+
+RNG = np.random.default_rng(20260912)
+
+
+# --------------------------------------------------------------------------
+# helpers (test-side, independent of the oracle)
+# --------------------------------------------------------------------------
+
+def _rand(shape, rng=RNG):
+    return rng.standard_normal(shape)
+
+
+def _arrays(sp, rng=RNG):
+    x = _rand((sp["N"], sp["Ci"], sp["T"], sp["H"], sp["W"]), rng)
+    c = _rand((sp["N"], sp["Ci"], sp["Tc"], sp["H"], sp["W"]), rng)
+    w = _rand((sp["Co"], sp["Ci"] // sp["groups"], sp["Kt"], sp["Kh"], sp["Kw"]), rng)
+    b = _rand((sp["Co"],), rng)
+    return x, c, w, b
+
+
+def _pad_time(Z, lo, hi):
+    """Prepend lo zero frames (crop -lo frames when lo < 0), then append hi
+    zero frames (crop -hi frames when hi < 0)."""
+    zeros = lambda n: np.zeros(Z.shape[:2] + (n,) + Z.shape[3:])
+    Z = np.concatenate([zeros(lo), Z], axis=2) if lo >= 0 else Z[:, :, -lo:]
+    Z = np.concatenate([Z, zeros(hi)], axis=2) if hi >= 0 else Z[:, :, :max(Z.shape[2] + hi, 0)]
+    return Z
+
+
+def torch_conv3d_ref(sp, x, c, w, b):
+    """Library reference: torch's own conv3d (fp64, CPU) applied to the
+    concatenation [C; X] padded p_l frames on the left (cropped when p_l < 0)
+    and p_r on the right.  torch pads space itself."""
+    Z = np.concatenate([c, x], axis=2)
+    p_l = sp["p_base"] - sp["Tc"]
+    ext = sp["d_t"] * (sp["Kt"] - 1) + 1
+    if Z.shape[2] + p_l + sp["p_r"] < ext:
+        return None  # no output frame
+    Zp = torch.from_numpy(_pad_time(Z, p_l, sp["p_r"]))
+    y = F.conv3d(Zp, torch.from_numpy(w),
+                 torch.from_numpy(b) if sp["has_bias"] else None,
+                 stride=(sp["s_t"], sp["s_h"], sp["s_w"]),
+                 padding=(0, sp["p_h"], sp["p_w"]),
+                 dilation=(sp["d_t"], sp["d_h"], sp["d_w"]), groups=sp["groups"])
+    return y.numpy()
+
+
+def brute_force(sp, x, c, w, b):
+    """Materialise the zero-padded Z and sum with explicit loops, no bounds
+    logic in the inner sum (tiny inputs only)."""
+    N, Ci, Co, Kt, Kh, Kw = (sp[k] for k in ("N", "Ci", "Co", "Kt", "Kh", "Kw"))
+    # pad (or crop) time, pad space
+    Z = _pad_time(np.concatenate([c, x], axis=2), sp["p_base"] - sp["Tc"], sp["p_r"])
+    Z = np.pad(Z, ((0, 0), (0, 0), (0, 0), (sp["p_h"],) * 2, (sp["p_w"],) * 2))
+    Tp, Hp, Wp = Z.shape[2:]
+    To = (Tp - sp["d_t"] * (Kt - 1) - 1) // sp["s_t"] + 1
+    Ho = (Hp - sp["d_h"] * (Kh - 1) - 1) // sp["s_h"] + 1
+    Wo = (Wp - sp["d_w"] * (Kw - 1) - 1) // sp["s_w"] + 1
+    To = max(To, 0)
+    g = sp["groups"]
+    cig, cog = Ci // g, Co // g
+    y = np.zeros((N, Co, To, Ho, Wo))
+    for n, co, t, h, ww in itertools.product(range(N), range(Co), range(To), range(Ho), range(Wo)):
+        s = 0.0
+        for ci, k, i, j in itertools.product(range(cig), range(Kt), range(Kh), range(Kw)):
+            s += w[co, ci, k, i, j] * Z[n, (co // cog) * cig + ci,
+                                        t * sp["s_t"] + k * sp["d_t"],
+                                        h * sp["s_h"] + i * sp["d_h"],
+                                        ww * sp["s_w"] + j * sp["d_w"]]
+        y[n, co, t, h, ww] = s + (b[co] if sp["has_bias"] else 0.0)
+    return y
+
+
+def _rel(a, b):
+    m = np.max(np.abs(b)) if b.size else 0.0
+    return np.max(np.abs(a - b)) / (m if m > 0 else 1.0) if b.size else 0.0
+
+
+def _random_spec(rng):
+    while True:
+        g = int(rng.choice([1, 1, 1, 2]))
+        Kt, Kh, Kw = (int(v) for v in rng.integers(1, 4, 3))
+        d_t, d_h, d_w = (int(v) for v in rng.integers(1, 3, 3))
+        sp = spec(N=int(rng.integers(1, 3)), Ci=g * int(rng.integers(1, 3)),
+                  Co=g * int(rng.integers(1, 3)), T=int(rng.integers(0, 5)),
+                  Tc=int(rng.integers(0, 4)), H=int(rng.integers(1, 7)),
+                  W=int(rng.integers(1, 7)), Kt=Kt, Kh=Kh, Kw=Kw,
+                  s_t=int(rng.integers(1, 3)), s_h=int(rng.integers(1, 3)),
+                  s_w=int(rng.integers(1, 3)), d_t=d_t, d_h=d_h, d_w=d_w,
+                  p_base=int(rng.integers(0, 5)), p_r=int(rng.integers(-1, 3)),
+                  p_h=int(rng.integers(0, 3)), p_w=int(rng.integers(0, 3)),
+                  groups=g, has_bias=int(rng.integers(0, 2)))
+        Ho = (sp["H"] + 2 * sp["p_h"] - d_h * (Kh - 1) - 1) // sp["s_h"] + 1
+        Wo = (sp["W"] + 2 * sp["p_w"] - d_w * (Kw - 1) - 1) // sp["s_w"] + 1
+        if Ho >= 1 and Wo >= 1:
+            return sp
+
+
+# --------------------------------------------------------------------------
+# the definition against independent implementations
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("case", range(300))
+def test_matches_torch_conv3d_fp64(case):
+    rng = np.random.default_rng(1000 + case)
+    sp = _random_spec(rng)
+    x, c, w, b = _arrays(sp, rng)
+    y = oracle.conv3d(sp, "f64", x, c, w, b)
+    ref = torch_conv3d_ref(sp, x, c, w, b)
+    if ref is None:
+        assert y.shape[2] == 0
+        return
+    assert y.shape == ref.shape
+    assert _rel(y, ref) < 1e-12
+
+
+@pytest.mark.parametrize("case", range(60))
+def test_matches_brute_force(case):
+    rng = np.random.default_rng(5000 + case)
+    sp = _random_spec(rng)
+    sp.update(N=1, H=min(sp["H"], 4), W=min(sp["W"], 4))
+    # keep the spatial output nonempty after shrinking
+    for ax, k, s, d, p in (("H", "Kh", "s_h", "d_h", "p_h"), ("W", "Kw", "s_w", "d_w", "p_w")):
+        while (sp[ax] + 2 * sp[p] - sp[d] * (sp[k] - 1) - 1) // sp[s] + 1 < 1:
+            sp[p] += 1
+    x, c, w, b = _arrays(sp, rng)
+    y = oracle.conv3d(sp, "f64", x, c, w, b)
+    ref = brute_force(sp, x, c, w, b)
+    assert y.shape == ref.shape
+    assert _rel(y, ref) < 1e-12
+
+
+def test_points_and_rows_agree_with_full():
+    rng = np.random.default_rng(7)
+    sp = spec(N=2, Ci=5, Co=3, T=3, Tc=2, H=9, W=11)
+    x, c, w, b = _arrays(sp, rng)
+    y = oracle.conv3d(sp, "f64", x, c, w, b)
+    idx = rng.integers(0, y.size, 300)
+    pts = oracle.conv3d_points(sp, "f64", x, c, w, b, idx)
+    assert np.array_equal(pts, y.reshape(-1)[idx])
+    rows = oracle.conv3d_rows(sp, "f64", x, c, w, b, 7, 40)
+    assert np.array_equal(rows, y.reshape(-1, y.shape[-1])[7:40])
+
+
+# --------------------------------------------------------------------------
+# closed forms and delta kernels
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("Tc,T,P,d_t,Kt", [(2, 4, 2, 1, 3), (0, 3, 2, 1, 3), (1, 1, 2, 1, 3),
+                                           (3, 2, 2, 1, 3), (2, 5, 4, 2, 3), (0, 1, 1, 1, 2)])
+def test_ones_closed_form(Tc, T, P, d_t, Kt):
+    sp = spec(N=1, Ci=3, Co=2, T=T, Tc=Tc, H=5, W=7, Kt=Kt, d_t=d_t, p_base=P)
+    x = np.ones((1, 3, T, 5, 7))
+    c = np.ones((1, 3, Tc, 5, 7))
+    w = np.ones((2, 3, Kt, 3, 3))
+    b = np.zeros(2)
+    y = oracle.conv3d(sp, "f64", x, c, w, b)
+    Zlen, p_l = Tc + T, P - Tc
+    To = y.shape[2]
+    for t in range(To):
+        taps = sum(1 for k in range(Kt) if 0 <= t + k * d_t - p_l < Zlen)
+        rows = np.array([sum(1 for i in range(3) if 0 <= h + i - 1 < 5) for h in range(5)])
+        cols = np.array([sum(1 for j in range(3) if 0 <= v + j - 1 < 7) for v in range(7)])
+        expect = 3 * taps * rows[:, None] * cols[None, :]
+        assert np.array_equal(y[0, 0, t], expect)
+        assert np.array_equal(y[0, 1, t], expect)
+
+
+def test_identity_kernel_gives_x_plus_b_exactly():
+    rng = np.random.default_rng(11)
+    Ci = 4
+    sp = spec(N=2, Ci=Ci, Co=Ci, T=3, Tc=2, H=6, W=5)
+    x, c, _, b = _arrays(sp, rng)
+    w = np.zeros((Ci, Ci, 3, 3, 3))
+    for ci in range(Ci):
+        w[ci, ci, 2, 1, 1] = 1.0
+    y = oracle.conv3d(sp, "f64", x, c, w, b)
+    assert np.array_equal(y, x + b[None, :, None, None, None])
+
+
+@pytest.mark.parametrize("k0", [0, 1, 2])
+@pytest.mark.parametrize("Tc", [0, 1, 2])
+def test_tap_delta_is_a_causal_time_shift(k0, Tc):
+    rng = np.random.default_rng(13 + k0 + 3 * Tc)
+    sp = spec(N=1, Ci=2, Co=2, T=4, Tc=Tc, H=3, W=4, has_bias=0)
+    x, c, _, b = _arrays(sp, rng)
+    w = np.zeros((2, 2, 3, 3, 3))
+    w[0, 0, k0, 1, 1] = 1.0
+    w[1, 1, k0, 1, 1] = 1.0
+    y = oracle.conv3d(sp, "f64", x, c, w, b)
+    # output frame t reads Z frame t + k0 - (2 - Tc); frames before Z are zero
+    Z = np.concatenate([c, x], axis=2)
+    for t in range(y.shape[2]):
+        src = t + k0 - (2 - Tc)
+        expect = Z[:, :, src] if 0 <= src < Z.shape[2] else np.zeros_like(Z[:, :, 0])
+        assert np.array_equal(y[:, :, t], expect)
+
+
+def test_off_centre_spatial_delta_shifts_with_zero_border():
+    rng = np.random.default_rng(17)
+    sp = spec(N=1, Ci=1, Co=1, T=2, Tc=2, H=5, W=6, has_bias=0)
+    x, c, _, b = _arrays(sp, rng)
+    w = np.zeros((1, 1, 3, 3, 3))
+    w[0, 0, 2, 0, 2] = 1.0  # row above, column to the right
+    y = oracle.conv3d(sp, "f64", x, c, w, b)
+    expect = np.zeros_like(x)
+    expect[:, :, :, 1:, :-1] = x[:, :, :, :-1, 1:]
+    assert np.array_equal(y, expect)
+
+
+def test_zero_weights_give_bias_bit_exact():
+    rng = np.random.default_rng(19)
+    sp = spec(N=1, Ci=3, Co=4, T=3, Tc=2, H=4, W=4)
+    x, c, _, b = _arrays(sp, rng)
+    w = np.zeros((4, 3, 3, 3, 3))
+    y = oracle.conv3d(sp, "f64", x, c, w, b)
+    assert np.array_equal(y, np.broadcast_to(b[None, :, None, None, None], y.shape))
+
+
+def test_linearity():
+    rng = np.random.default_rng(23)
+    sp = spec(N=1, Ci=3, Co=2, T=3, Tc=2, H=5, W=5, has_bias=0)
+    x1, c1, w, b = _arrays(sp, rng)
+    x2, c2, _, _ = _arrays(sp, rng)
+    a, bb = 0.75, -1.25
+    y1 = oracle.conv3d(sp, "f64", x1, c1, w, b)
+    y2 = oracle.conv3d(sp, "f64", x2, c2, w, b)
+    y = oracle.conv3d(sp, "f64", a * x1 + bb * x2, a * c1 + bb * c2, w, b)
+    assert _rel(y, a * y1 + bb * y2) < 1e-13
+
+
+# --------------------------------------------------------------------------
+# cache semantics: chunked streaming == one whole-sequence causal conv
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("chunks,d_t,zero_cache", [([2, 1, 3, 1], 1, False),
+                                                   ([2, 1, 3, 1], 1, True),
+                                                   ([1, 1, 1, 1, 1], 1, True),
+                                                   ([3, 2, 1, 4], 2, False),
+                                                   ([4, 4, 4], 1, True)])
+def test_streaming_equals_whole_sequence(chunks, d_t, zero_cache):
+    rng = np.random.default_rng(29 + sum(chunks) + d_t)
+    Ci, Co, H, W = 3, 2, 4, 5
+    P = 2 * d_t
+    whole = spec(N=1, Ci=Ci, Co=Co, T=sum(chunks), Tc=0, H=H, W=W, d_t=d_t)
+    X = _rand((1, Ci, sum(chunks), H, W), rng)
+    w = _rand((Co, Ci, 3, 3, 3), rng)
+    b = _rand((Co,), rng)
+    y_whole = oracle.conv3d(whole, "f64", X, None, w, b)
+
+    cache = np.zeros((1, Ci, P, H, W)) if zero_cache else np.zeros((1, Ci, 0, H, W))
+    outs, t0 = [], 0
+    for T in chunks:
+        sp = spec(N=1, Ci=Ci, Co=Co, T=T, Tc=cache.shape[2], H=H, W=W, d_t=d_t)
+        x = X[:, :, t0:t0 + T]
+        outs.append(oracle.conv3d(sp, "f64", x, cache, w, b))
+        cache = oracle.cache_update(sp, "f64", x, cache)
+        assert cache.shape[2] == min(P, sp["Tc"] + T)
+        t0 += T
+    assert np.array_equal(np.concatenate(outs, axis=2), y_whole)
+
+
+def test_resume_from_serialized_cache_is_bit_exact():
+    rng = np.random.default_rng(31)
+    Ci, Co, H, W = 2, 3, 4, 4
+    w = _rand((Co, Ci, 3, 3, 3), rng)
+    b = _rand((Co,), rng)
+    xs = [_rand((1, Ci, 2, H, W), rng) for _ in range(4)]
+
+    def run(cache, seq):
+        out = []
+        for x in seq:
+            sp = spec(N=1, Ci=Ci, Co=Co, T=2, Tc=cache.shape[2], H=H, W=W)
+            out.append(oracle.conv3d(sp, "f64", x, cache, w, b))
+            cache = oracle.cache_update(sp, "f64", x, cache)
+        return out, cache
+
+    c0 = np.zeros((1, Ci, 2, H, W))
+    full, _ = run(c0, xs)
+    first, mid = run(c0, xs[:2])
+    blob = mid.tobytes()
+    restored = np.frombuffer(bytearray(blob), dtype=np.float64).reshape(mid.shape)
+    second, _ = run(restored, xs[2:])
+    for a, b_ in zip(first + second, full):
+        assert np.array_equal(a, b_)
+
+
+def test_cache_update_is_last_frames_of_concat():
+    rng = np.random.default_rng(37)
+    for Tc, T, P in [(2, 4, 2), (2, 1, 2), (0, 1, 2), (3, 2, 2), (1, 0, 2), (0, 3, 0)]:
+        sp = spec(N=2, Ci=3, Co=1, T=T, Tc=Tc, H=2, W=3, p_base=P)
+        x = rng.standard_normal((2, 3, T, 2, 3)).astype(np.float32)
+        c = rng.standard_normal((2, 3, Tc, 2, 3)).astype(np.float32)
+        out = oracle.cache_update(sp, "f32", x, c)
+        Z = np.concatenate([c, x], axis=2)
+        L = min(P, Tc + T)
+        assert np.array_equal(out, Z[:, :, Z.shape[2] - L:])
+
+
+# --------------------------------------------------------------------------
+# Eq. 3 and Eq. 4 against enumeration
+# --------------------------------------------------------------------------
+
+def test_output_length_matches_window_count():
+    rng = np.random.default_rng(41)
+    for _ in range(400):
+        sp = _random_spec(rng)
+        To, Ho, Wo, L = oracle.output_dims(sp)
+        padded = sp["Tc"] + sp["T"] + (sp["p_base"] - sp["Tc"]) + sp["p_r"]
+        ext = sp["d_t"] * (sp["Kt"] - 1)
+        count = sum(1 for t in range(0, 64) if t * sp["s_t"] + ext <= padded - 1)
+        assert To == count
+        assert L == min(sp["p_base"], sp["Tc"] + sp["T"])
+
+
+def test_tap_intervals_match_enumeration():
+    rng = np.random.default_rng(43)
+    for _ in range(400):
+        sp = _random_spec(rng)
+        sp["s_t"] = 1
+        To, _, _, _ = oracle.output_dims(sp)
+        Z = sp["Tc"] + sp["T"]
+        for k in range(sp["Kt"]):
+            lo, hi = oracle.tap_interval(sp, k)
+            # outputs whose k-th tap lands inside Z, straight from the window
+            # definition: window of output t starts at padded frame t, and
+            # padded frame q is Z frame q - p_l
+            valid = [t for t in range(To)
+                     if 0 <= t + k * sp["d_t"] - (sp["p_base"] - sp["Tc"]) < Z]
+            if valid:
+                assert (lo, hi) == (valid[0], valid[-1] + 1)
+                assert valid == list(range(lo, hi))  # contiguous
+            else:
+                assert lo >= hi
+
+
+# --------------------------------------------------------------------------
+# special cases that reduce to textbook routines
+# --------------------------------------------------------------------------
+
+def test_1x1x1_is_a_per_frame_matmul():
+    rng = np.random.default_rng(47)
+    sp = spec(N=2, Ci=5, Co=3, T=3, Tc=0, H=4, W=6, Kt=1, Kh=1, Kw=1)
+    x, c, w, b = _arrays(sp, rng)
+    y = oracle.conv3d(sp, "f64", x, c, w, b)
+    ref = np.einsum("oc,nczyx->nozyx", w[:, :, 0, 0, 0], x) + b[None, :, None, None, None]
+    assert _rel(y, ref) < 1e-13
+
+
+@pytest.mark.parametrize("Kt", [1, 2, 3, 5])
+def test_point_spatial_is_a_causal_fir(Kt):
+    rng = np.random.default_rng(53 + Kt)
+    T = 17
+    sp = spec(N=1, Ci=1, Co=1, T=T, Tc=0, H=1, W=1, Kt=Kt, Kh=1, Kw=1, has_bias=0)
+    z = rng.standard_normal(T)
+    w = rng.standard_normal(Kt)
+    y = oracle.conv3d(sp, "f64", z.reshape(1, 1, T, 1, 1), None,
+                      w.reshape(1, 1, Kt, 1, 1), np.zeros(1))
+    ref = np.convolve(z, w[::-1])[:T]
+    assert np.max(np.abs(y.reshape(-1) - ref)) < 1e-12
+
+
+# --------------------------------------------------------------------------
+# element types: exact widening
+# --------------------------------------------------------------------------
+
+def test_bf16_and_f16_inputs_are_widened_exactly():
+    rng = np.random.default_rng(59)
+    sp = spec(N=1, Ci=3, Co=2, T=2, Tc=2, H=4, W=5)
+    x, c, w, b = (torch.from_numpy(a) for a in _arrays(sp, rng))
+    for dt, tdt in (("bf16", torch.bfloat16), ("f16", torch.float16)):
+        xs, cs, ws, bs = (t.to(tdt) for t in (x, c, w, b))
+        y = oracle.conv3d(sp, dt, xs, cs, ws, bs)
+        y64 = oracle.conv3d(sp, "f64", *(t.double().numpy() for t in (xs, cs, ws, bs)))
+        assert np.array_equal(y, y64)
+
+
+# --------------------------------------------------------------------------
+# algorithmic FLOP count: closed forms for the benchmarked layer shapes
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("Ci,Co,T,Tc,H,W,Kt,pairs", [
+    (384, 384, 1, 2, 60, 104, 3, 3),      # one new frame, 2 cached: 3 taps
+    (192, 192, 4, 2, 240, 416, 3, 12),    # 4 new frames, 2 cached: 4 x 3
+    (192, 192, 4, 0, 240, 416, 3, 9),     # first chunk without cache: 3+2+2+... = 9
+    (320, 160, 4, 0, 352, 640, 1, 4),     # 1x1x1 shortcut
+])
+def test_flops_closed_form(Ci, Co, T, Tc, H, W, Kt, pairs):
+    kk = 3 if Kt == 3 else 1
+    sp = spec(N=1, Ci=Ci, Co=Co, T=T, Tc=Tc, H=H, W=W, Kt=Kt, Kh=kk, Kw=kk)
+    assert oracle.flops(sp) == 2.0 * Co * Ci * kk * kk * H * W * pairs
+
+
+# --------------------------------------------------------------------------
+# the route rule, clause by clause
+# --------------------------------------------------------------------------
+
+ROUTE_TABLE = [
+    # (spec overrides, dtype, forced, expected reason)
+    (dict(), "bf16", False, "none"),
+    (dict(), "f32", False, "none"),
+    (dict(), "bf16", True, "forced"),
+    (dict(), "f16", False, "dtype"),
+    (dict(Ci=4, Co=4, groups=2), "bf16", False, "groups"),
+    (dict(s_t=2), "bf16", False, "stride_t"),
+    (dict(p_r=-1), "bf16", False, "pad_right"),
+    (dict(T=0, Tc=2), "bf16", False, "no_output"),
+    (dict(Kt=1, Kh=1, Kw=1, p_base=0, Tc=0), "bf16", False, "kt1"),
+    (dict(Kt=1, p_base=0, Tc=0), "bf16", False, "kt1"),
+    (dict(Kh=1, Kw=1), "bf16", False, "spatial"),
+    (dict(p_h=0, H=5), "bf16", False, "spatial"),
+    (dict(d_h=2, p_h=2), "bf16", False, "spatial"),
+    (dict(s_w=2), "bf16", False, "spatial"),
+    (dict(Tc=0), "bf16", False, "none"),
+    (dict(Tc=3), "bf16", False, "none"),       # p_l < 0 is allowed
+    (dict(d_t=2, p_base=4, Tc=4), "bf16", False, "none"),
+    (dict(Kt=2, p_base=1, Tc=1), "bf16", False, "none"),
+    (dict(T=0, Tc=0, Kt=1, Kh=3, p_base=2), "bf16", False, "no_tap"),  # |Z| = 0
+    (dict(T=1, Tc=0, Kt=2, d_t=2, p_base=1, p_r=1), "bf16", False, "no_tap"),  # straddle
+]
+
+
+@pytest.mark.parametrize("over,dtype,forced,reason", ROUTE_TABLE)
+def test_route_rule_table(over, dtype, forced, reason):
+    sp = spec(N=1, Ci=2, Co=2, T=2, Tc=2, H=4, W=4)
+    sp.update(over)
+    r, why = oracle.route(sp, dtype, forced)
+    assert why == reason
+    assert r == ("fast" if reason == "none" else "fallback")
+
+
+def test_no_tap_clause_matches_enumeration():
+    # the "no active tap" clause fires exactly when no (output frame, tap)
+    # pair reads a frame of Z -- possible with temporal dilation and a right
+    # pad, where a window can straddle Z -- checked by enumeration
+    rng = np.random.default_rng(61)
+    seen = 0
+    for _ in range(3000):
+        sp = _random_spec(rng)
+        sp["s_t"] = 1
+        To, _, _, _ = oracle.output_dims(sp)
+        _, why = oracle.route(sp, "bf16")
+        if sp["groups"] != 1 or sp["p_r"] < 0 or To < 1:
+            continue
+        p_l = sp["p_base"] - sp["Tc"]
+        hit = any(0 <= t + k * sp["d_t"] - p_l < sp["Tc"] + sp["T"]
+                  for t in range(To) for k in range(sp["Kt"]))
+        assert (why == "no_tap") == (not hit)
+        seen += not hit
+    assert seen > 0
