@@ -1,0 +1,217 @@
+#!/usr/bin/env python3
+"""Benchmark of the cached causal Conv3D on one MI355X.
+
+Workload (default): the 720p wide-channel decode stack -- causal Conv3D
+layers Ci=Co=640 at 44x80, Ci=Co=320 at 176x320, Ci=320->Co=160 at 352x640,
+Ci=Co=160 at 704x1280 (3x3x3, stride 1, spatial pad 1, 4 new frames + a
+2-frame cache that starts at zeros), then a 1x1x1 shortcut conv
+Ci=320->Co=160 at 352x640 that takes the fallback route; bf16 storage, fp32
+accumulation.  One STEP is one chunk through all five layers: route
+decisions, the fast implicit-GEMM kernel with its fused bias and cache update,
+and the fallback kernel.  Caches are carried between steps.  Weights are
+repacked once per layer before timing (the paper caches the derived weight
+slices across calls).  Inputs are seeded synthetic tensors already resident
+in device memory.
+
+Prints ONE JSON line: whole-chunk TFLOP/s (algorithmic FLOP: only valid
+temporal taps, padded spatial positions counted), chunk latency, per-layer
+TFLOP/s and fraction of the 2.5 PFLOP/s bf16 matrix peak, the dominant
+kernel's roofline, and the oracle's CPU rate on a bounded sample.
+"""
+import argparse
+import json
+import math
+import os
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = ("causal Conv3D TFLOP/s and % of bf16 MFMA peak per layer shape; "
+          "chunk latency (ms)")
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 matrix peak (published)
+PEAK_F32_TFLOPS = 157.3     # MI355X fp32 matrix peak (published)
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="stack_720p")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(run with --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2609_31938_amd import c3c, inputs
+
+    wl = inputs.WORKLOADS[args.workload]
+    dtype = wl["dtype"]
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    ctx = c3c.Context()
+    chunks = wl["chunks"]
+
+    # ---------------------------------------------------------------- setup
+    layers = []
+    for lid, (lname, sp) in enumerate(wl["layers"]):
+        w, b = inputs.layer_tensors(sp, dtype, wl["id"], lid, dev)
+        route, why = c3c.route_query(None, sp, dtype)
+        t0 = time.perf_counter()
+        wpack = c3c.weight_repack(ctx, sp, w) if route == "fast" else None
+        torch.cuda.synchronize()
+        repack_ms = (time.perf_counter() - t0) * 1e3
+        To, Ho, Wo, L = c3c.output_dims(sp, dtype)
+        xs = [inputs.chunk_input(sp, dtype, wl["id"], lid, c, dev) for c in range(chunks)]
+        y = torch.empty((sp["N"], sp["Co"], To, Ho, Wo), dtype=w.dtype, device=dev)
+        cbuf = [torch.zeros((sp["N"], sp["Ci"], sp["Tc"], sp["H"], sp["W"]), dtype=w.dtype,
+                            device=dev) for _ in range(2)]
+        layers.append(dict(name=lname, sp=sp, w=w, b=b, wpack=wpack, xs=xs, y=y, cbuf=cbuf,
+                           route=route, reason=why, flops=c3c.flops(sp, dtype),
+                           repack_ms=repack_ms))
+    torch.cuda.synchronize()
+
+    def reset_caches():
+        for L_ in layers:
+            for cb in L_["cbuf"]:
+                cb.zero_()
+            L_["cur"] = 0
+
+    def step(s, evs=None):
+        c = s % chunks
+        for i, L_ in enumerate(layers):
+            sp = L_["sp"]
+            cin = L_["cbuf"][L_["cur"]] if sp["Tc"] else None
+            cout = L_["cbuf"][1 - L_["cur"]] if sp["Tc"] else None
+            if evs is not None:
+                evs[i][0].record()
+            c3c.conv3d_causal_cached(ctx, sp, L_["xs"][c], cin, L_["w"], L_["wpack"], L_["b"],
+                                     L_["y"], cout)
+            if evs is not None:
+                evs[i][1].record()
+            if sp["Tc"]:
+                L_["cur"] = 1 - L_["cur"]
+
+    # ---------------------------------------------------------------- warmup
+    reset_caches()
+    for s in range(args.warmup):
+        step(s)
+    torch.cuda.synchronize()
+    ctx.reset()
+    reset_caches()
+    torch.cuda.synchronize()
+
+    # ---------------------------------------------------------------- timed
+    ev = [[[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in layers]
+          for _ in range(args.steps)]
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter()
+    start.record()
+    for s in range(args.steps):
+        step(s, ev[s])
+    stop.record()
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter() - t_wall
+    total_ms = start.elapsed_time(stop)
+
+    counters = ctx.counters()
+    per_layer = []
+    total_flops = 0.0
+    for i, L_ in enumerate(layers):
+        times = [ev[s][i][0].elapsed_time(ev[s][i][1]) for s in range(args.steps)]
+        fl = L_["flops"]
+        total_flops += fl * args.steps
+        med = statistics.median(times)
+        tf = fl / (med * 1e-3) / 1e12
+        peak = PEAK_BF16_TFLOPS if dtype == "bf16" else PEAK_F32_TFLOPS
+        per_layer.append(dict(layer=L_["name"], route=L_["route"], reason=L_["reason"],
+                              gflop=round(fl / 1e9, 3), ms_median=round(med, 4),
+                              ms_mean=round(sum(times) / len(times), 4),
+                              tflops=round(tf, 2), frac_peak=round(tf / peak, 4),
+                              repack_ms=round(L_["repack_ms"], 3)))
+    value = total_flops / (total_ms * 1e-3) / 1e12
+
+    # dominant kernel: the fast conv on the largest layer
+    fast_layers = [p for p in per_layer if p["route"] == "fast"]
+    dom = max(fast_layers, key=lambda p: p["gflop"])
+    dom_i = [p["layer"] for p in per_layer].index(dom["layer"])
+    dom_mean_ms = dom["ms_mean"]
+    achieved = dom["gflop"] * 1e9 / (dom_mean_ms * 1e-3) / 1e12
+    peak = PEAK_BF16_TFLOPS if dtype == "bf16" else PEAK_F32_TFLOPS
+    roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak,
+                "unit": "TFLOP/s", "frac": round(achieved / peak, 4), "traffic": None,
+                "kernel": f"fast conv, layer {dom['layer']}"}
+
+    out = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(total_ms / args.steps, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": dtype,
+        "data": "synthetic",
+        "config": {"workload": f"{args.workload}: " + ", ".join(
+            f"{L_['name']}" for L_ in layers) + f"; N=1, T=4 new + 2 cached frames, "
+            f"{chunks}-chunk cache carry; step = one chunk through every layer",
+            "global_batch": 1, "chunks_per_stream": chunks},
+        "chunk_latency_ms": round(total_ms / args.steps, 4),
+        "layers": per_layer,
+        "roofline": roofline,
+        "counters": counters,
+        "wall_s": round(t_wall, 4),
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(layers[dom_i], dtype, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+def cpu_baseline(L_, dtype, budget_s):
+    """The oracle, as it stands, on host cores: output rows of the dominant
+    layer for an output frame whose three taps are all valid, sampled until
+    about `budget_s` seconds of CPU work; scaled to TFLOP/s."""
+    import torch
+    import oracle
+    sp = dict(L_["sp"])
+    x = L_["xs"][1].cpu()
+    cache = L_["xs"][0][:, :, -sp["Tc"]:].contiguous().cpu() if sp["Tc"] else None
+    w, b = L_["w"].cpu(), L_["b"].cpu()
+    To, Ho, Wo, _ = oracle.output_dims(sp)
+    t_frame = To - 1  # last output frame: every tap reads a real frame
+    per_row = 2.0 * sp["Ci"] * sp["Kt"] * sp["Kh"] * sp["Kw"] * Wo
+    rows_done, t_used, co = 0, 0.0, 0
+    batch = 8
+    while t_used < budget_s and co < sp["Co"]:
+        r0 = (co * To + t_frame) * Ho + 1  # interior rows: all 3 kernel rows valid
+        n = min(batch, Ho - 2)
+        t0 = time.perf_counter()
+        oracle.conv3d_rows(sp, dtype, x, cache, w, b, r0, r0 + n)
+        dt = time.perf_counter() - t0
+        t_used += dt
+        rows_done += n
+        co += 1
+        if dt < 1.0:
+            batch = min(batch * 2, Ho - 2)
+    flops = per_row * rows_done
+    return {"value": round(flops / t_used / 1e12, 6), "unit": "TFLOP/s",
+            "cores": oracle.num_threads(), "kind": "oracle",
+            "sample": f"layer {L_['name']}: {rows_done} interior output rows of "
+                      f"{Wo} pixels in output frame {t_frame} (all taps valid), "
+                      f"{flops / 1e9:.1f} GFLOP fp64 in {t_used:.1f} s"}
+
+
+if __name__ == "__main__":
+    main()

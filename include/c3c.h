@@ -1,0 +1,233 @@
+/*
+ * c3c.h -- cached causal Conv3D for AMD Instinct MI355X (gfx950).
+ *
+ * The library evaluates a cached causal Conv3D call the way the paper's
+ * cache-aware lowering defines it (Sec. 4, Eq. 1-4, Alg. 1): every temporal
+ * tap k of the kernel is a batched spatial Conv2D over the valid frames of
+ * the cache-augmented input Z = [C; X]_T, the taps are summed, the bias is
+ * added exactly once, the output is NCTHW, and the cache is replaced by the
+ * last frames of Z.  On the fast route all active taps of one call are one
+ * implicit-GEMM kernel on bf16 (or fp32) matrix cores with fp32 accumulation;
+ * calls the fast route does not support go to a generic direct-Conv3D
+ * fallback kernel, and route counters account for every call (Alg. 1 keeps
+ * call / fast counters; Sec. 1 and Sec. 6 speak of fallbacks and unsupported
+ * cases).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Every call returns a status code (enum c3c_status); nothing throws.
+ *  - Tensor pointers are DEVICE pointers (HIP device memory) unless stated.
+ *    The caller allocates and owns every buffer; the library never allocates
+ *    device memory in a compute call.
+ *  - `stream` is a hipStream_t passed as void* (NULL = the default stream).
+ *    Work is enqueued asynchronously on it; the caller synchronises before
+ *    reading outputs.  A device fault after enqueue is reported by the HIP
+ *    runtime at the next synchronisation, not by the call that enqueued it.
+ *  - A c3c_ctx holds the mode bits, the route counters and the histogram of
+ *    shapes that went to the fallback.  It is not thread-safe: use one
+ *    context per host thread (and, mirroring the paper's attribution of calls
+ *    to the active encode or decode scope, one per scope).
+ *  - All tensors are contiguous, element type `dtype` throughout:
+ *      x         [N][Ci][T][H][W]          the new chunk (X)
+ *      cache     [N][Ci][Tc][H][W]         cached prior frames (C); NULL iff Tc == 0
+ *      w         [Co][Ci/groups][Kt][Kh][Kw]   the unchanged Conv3D weights
+ *      bias      [Co]                      NULL iff has_bias == 0
+ *      y         [N][Co][To][Ho][Wo]       output, NCTHW; may be NULL iff To*Ho*Wo*N*Co == 0
+ *      cache_out [N][Ci][L][H][W]          the new cache; NULL allowed iff L == 0
+ *    where To is Eq. 3 with p_l = pad_t_base - Tc, Ho/Wo the spatial
+ *    analogue, and L = min(pad_t_base, Tc + T).
+ */
+#ifndef C3C_H
+#define C3C_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---------------------------------------------------------------- status */
+typedef enum c3c_status {
+  C3C_OK = 0,
+  C3C_E_INVAL = 1,       /* null / negative / inconsistent arguments, aliasing */
+  C3C_E_UNSUPPORTED = 2, /* strict mode and the call does not route fast      */
+  C3C_E_DEVICE = 3,      /* a HIP launch or runtime call failed               */
+  C3C_E_INJECTED = 4     /* strict mode and an injected fast-route failure    */
+} c3c_status;
+
+/* ---------------------------------------------------------------- dtypes */
+typedef enum c3c_dtype {
+  C3C_DTYPE_BF16 = 1, /* fast route: bf16 matrix cores, fp32 accumulation   */
+  C3C_DTYPE_F32 = 2,  /* fast route: fp32 matrix cores, fp32 accumulation   */
+  C3C_DTYPE_F16 = 3   /* fallback route only                               */
+} c3c_dtype;
+
+/* ---------------------------------------------------------------- modes */
+enum {
+  /* an unsupported call or a fast-route failure returns an error instead of
+   * falling back (the paper's strict validation mode, Sec. 4.3) */
+  C3C_MODE_STRICT = 1u,
+  /* every call takes the fallback route: the baseline that must record zero
+   * fast hits (acceptance rule, Sec. 5.3) */
+  C3C_MODE_FORCE_FALLBACK = 2u,
+  /* the fast route fails before launching anything, as a test of the failure
+   * path: counted in fast_error, then fallback (or C3C_E_INJECTED if strict) */
+  C3C_MODE_INJECT_FAST_FAILURE = 4u
+};
+
+/* ---------------------------------------------------------------- routes */
+typedef enum c3c_route { C3C_ROUTE_FAST = 0, C3C_ROUTE_FALLBACK = 1 } c3c_route;
+
+/* Why a call does not route fast: the first failing clause, tested in this
+ * order.  Clauses 2-7 are the paper's guard (Alg. 1); 8-9 state what the
+ * fast kernel is specialised for. */
+typedef enum c3c_reason {
+  C3C_REASON_NONE = 0,      /* routes fast                                   */
+  C3C_REASON_FORCED = 1,    /* C3C_MODE_FORCE_FALLBACK                       */
+  C3C_REASON_DTYPE = 2,     /* dtype has no fast kernel (f16)                */
+  C3C_REASON_GROUPS = 3,    /* groups != 1                                   */
+  C3C_REASON_STRIDE_T = 4,  /* temporal stride != 1                          */
+  C3C_REASON_PAD_RIGHT = 5, /* pad_t_right < 0                               */
+  C3C_REASON_NO_OUTPUT = 6, /* To < 1                                        */
+  C3C_REASON_NO_TAP = 7,    /* no temporal tap has a nonempty Eq. 4 interval */
+  C3C_REASON_KT1 = 8,       /* Kt < 2 (e.g. a 1x1x1 shortcut conv)           */
+  C3C_REASON_SPATIAL = 9,   /* spatial kernel is not 3x3, stride 1, pad 1, dil 1 */
+  /* not a predicate clause: the call routed fast, the fast route failed and
+   * the call fell back (appears only in the fallback-shape histogram) */
+  C3C_REASON_FAST_ERROR = 10
+} c3c_reason;
+
+/* ---------------------------------------------------------------- descriptor */
+/* One Conv3D call (Sec. 4.1 notation).  pad_t_base is p_l^base, the temporal
+ * left pad the layer would apply with no cache; the effective left pad is
+ * p_l = pad_t_base - Tc (Sec. 4.2) and may be negative, in which case the
+ * oldest cache frames are not read.  A causal 3-tap layer has
+ * pad_t_base = 2 * dil_t, pad_t_right = 0. */
+typedef struct c3c_conv_desc {
+  int64_t N, Ci, Co;       /* batch, input / output channels (>= 1)          */
+  int64_t T, Tc;           /* new frames, cached frames (>= 0)               */
+  int64_t H, W;            /* spatial size (>= 1)                            */
+  int64_t Kt, Kh, Kw;      /* kernel size (>= 1)                             */
+  int64_t stride_t, stride_h, stride_w; /* >= 1                              */
+  int64_t dil_t, dil_h, dil_w;          /* >= 1                              */
+  int64_t pad_t_base;      /* p_l^base >= 0                                  */
+  int64_t pad_t_right;     /* p_r (any sign; < 0 routes to the fallback)     */
+  int64_t pad_h, pad_w;    /* symmetric spatial zero padding (>= 0)          */
+  int64_t groups;          /* divides Ci and Co                              */
+  int32_t dtype;           /* enum c3c_dtype                                 */
+  int32_t has_bias;        /* 0 or 1                                         */
+} c3c_conv_desc;
+
+typedef struct c3c_counters {
+  /* Invariants: calls = fast + fallback + strict_rejects
+   *             fallback = unsupported + forced + fast_error */
+  uint64_t calls;          /* valid calls (EINVAL calls are not counted)     */
+  uint64_t fast;           /* completed on the fast route                    */
+  uint64_t fallback;       /* completed on the fallback route                */
+  uint64_t unsupported;    /* fell back because a guard clause failed        */
+  uint64_t forced;         /* fell back because of C3C_MODE_FORCE_FALLBACK   */
+  uint64_t fast_error;     /* fell back because the fast route failed        */
+  uint64_t strict_rejects; /* refused in strict mode                         */
+  uint64_t repacks;        /* weight repacks enqueued                        */
+} c3c_counters;
+
+/* One entry of the fallback-shape histogram: the reason and the full call
+ * signature (the paper keys runtime signatures by channels, frames, spatial
+ * size and cache length, Table 1). */
+typedef struct c3c_sig_count {
+  int32_t reason;          /* enum c3c_reason */
+  int32_t reserved;
+  c3c_conv_desc desc;
+  uint64_t count;
+} c3c_sig_count;
+
+typedef struct c3c_ctx c3c_ctx;
+
+/* ---------------------------------------------------------------- context */
+/* Create a context with the given mode bits.  *out receives a host object
+ * owned by the caller; free it with c3c_ctx_destroy.  EINVAL if out is NULL
+ * or mode has unknown bits. */
+int c3c_ctx_create(uint32_t mode, c3c_ctx** out);
+/* Free a context (NULL is accepted). */
+int c3c_ctx_destroy(c3c_ctx* ctx);
+/* Replace / read the mode bits.  EINVAL on NULL or unknown bits. */
+int c3c_set_mode(c3c_ctx* ctx, uint32_t mode);
+int c3c_get_mode(const c3c_ctx* ctx, uint32_t* mode);
+
+/* ---------------------------------------------------------------- host maths */
+/* Output sizes (Eq. 3 and its spatial analogue) and the new cache length
+ * L = min(pad_t_base, Tc + T).  Pure host code.  Any output pointer may be
+ * NULL.  EINVAL for an invalid descriptor (including Ho < 1 or Wo < 1). */
+int c3c_output_dims(const c3c_conv_desc* d, int64_t* To, int64_t* Ho,
+                    int64_t* Wo, int64_t* L);
+/* Eq. 4: output frames [o_l, o_h) that temporal tap k contributes to
+ * (source frames o + delta_k, delta_k = k dil_t - p_l).  Unit temporal stride
+ * only (EINVAL otherwise); o_l >= o_h means the tap is inactive. */
+int c3c_tap_interval(const c3c_conv_desc* d, int64_t k, int64_t* o_l,
+                     int64_t* o_h);
+/* Algorithmic FLOP of one call: 2 N Co (Ci/groups) Kh Kw Ho Wo times the
+ * number of (output frame, temporal tap) pairs whose source frame lies in Z.
+ * Pure host code.  EINVAL for an invalid descriptor. */
+int c3c_flops(const c3c_conv_desc* d, double* flops);
+/* The route the call would take under ctx's mode, with the reason.  Pure
+ * host code: no device access, counters untouched.  ctx may be NULL (mode 0). */
+int c3c_route_query(const c3c_ctx* ctx, const c3c_conv_desc* d, int* route,
+                    int* reason);
+
+/* ---------------------------------------------------------------- weights */
+/* Size in bytes of the packed fast-route weights for this layer (the paper's
+ * derived per-tap weight slices, Alg. 1, kept as one matrix-core-ready copy).
+ * 0 when the call does not route fast under mode 0. */
+int c3c_weight_pack_bytes(const c3c_conv_desc* d, size_t* bytes);
+/* Repack w (device, [Co][Ci][Kt][Kh][Kw]) into wpack (device, caller
+ * allocated, c3c_weight_pack_bytes bytes): a bit-exact permutation into
+ * K-major matrix-core fragments, zero padded to whole fragments.  Enqueued on
+ * `stream`.  Re-run it whenever w changes.  EINVAL if the layer has no fast
+ * layout (bytes == 0), on NULL pointers or if wpack aliases w. */
+int c3c_weight_repack(c3c_ctx* ctx, const c3c_conv_desc* d, const void* w,
+                      void* wpack, void* stream);
+/* Inverse permutation, for tests: wpack -> w_out ([Co][Ci][Kt][Kh][Kw]). */
+int c3c_weight_unpack(const c3c_conv_desc* d, const void* wpack, void* w_out,
+                      void* stream);
+
+/* ---------------------------------------------------------------- the call */
+/* y = CausalConv3D([cache; x], w) + bias, cache_out = last L frames of
+ * [cache; x]  (Eq. 2 with the intervals of Eq. 4; Alg. 1).
+ *
+ * Fast route: one kernel launch evaluates every active tap into fp32
+ * registers, adds the bias once, rounds to `dtype` (nearest even), stores
+ * NCTHW, and writes cache_out.  It reads wpack (required, from
+ * c3c_weight_repack on the same w); w itself is not read.
+ * Fallback route: the direct-Conv3D kernel reads w (wpack may be NULL), then a
+ * copy kernel writes cache_out.
+ *
+ * Counters: calls++ first; then fast++, or fallback++ with unsupported /
+ * forced / fast_error, or strict_rejects++ (with C3C_E_UNSUPPORTED or
+ * C3C_E_INJECTED).  A call returning EINVAL is not counted.
+ * EINVAL: NULL ctx/desc, invalid descriptor, a required pointer NULL,
+ * cache_out overlapping cache or x, y overlapping any input, or wpack NULL
+ * on a call that routes fast. */
+int c3c_conv3d_causal_cached(c3c_ctx* ctx, const c3c_conv_desc* d,
+                             const void* x, const void* cache, const void* w,
+                             const void* wpack, const void* bias, void* y,
+                             void* cache_out, void* stream);
+
+/* ---------------------------------------------------------------- counters */
+int c3c_counters_get(const c3c_ctx* ctx, c3c_counters* out);
+int c3c_counters_reset(c3c_ctx* ctx); /* also clears the shape histogram */
+/* Copy up to `cap` histogram entries (first-seen order) into out (host
+ * memory); *n receives the total number of distinct entries. */
+int c3c_fallback_shapes(const c3c_ctx* ctx, c3c_sig_count* out, int cap,
+                        int* n);
+
+/* ---------------------------------------------------------------- messages */
+const char* c3c_strerror(int status);
+/* Message of the last failed call on ctx ("" if none); valid until the next
+ * call on ctx. */
+const char* c3c_last_error(const c3c_ctx* ctx);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* C3C_H */

@@ -1,0 +1,289 @@
+"""Python binding of libc3c (ctypes): argument marshalling only.
+
+Every step of the cached causal Conv3D runs in the HIP library; this module
+turns torch device tensors into pointers, passes torch's current HIP stream,
+and maps status codes to exceptions.  It imports nothing else from this
+repository.  Importing it raises if ``libc3c.so`` has not been built (run
+``python -m paper_2609_31938_amd.build``): there is no CPU fallback.
+
+Call shapes are described by the same plain ``spec`` dict the input module
+builds (keys ``N Ci Co T Tc H W Kt Kh Kw s_t s_h s_w d_t d_h d_w p_base p_r
+p_h p_w groups has_bias``); element types are ``"bf16" "f32" "f16"``.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+import re
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libc3c.so")
+HEADER = os.path.join(os.path.dirname(_HERE), "include", "c3c.h")
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(f"{LIB_PATH} is missing: build it with "
+                      "`python -m paper_2609_31938_amd.build` (no CPU fallback exists)")
+
+OK, E_INVAL, E_UNSUPPORTED, E_DEVICE, E_INJECTED = 0, 1, 2, 3, 4
+DTYPES = {"bf16": 1, "f32": 2, "f16": 3}
+MODE_STRICT, MODE_FORCE_FALLBACK, MODE_INJECT_FAST_FAILURE = 1, 2, 4
+ROUTES = ["fast", "fallback"]
+REASONS = ["none", "forced", "dtype", "groups", "stride_t", "pad_right", "no_output",
+           "no_tap", "kt1", "spatial", "fast_error"]
+
+
+class C3CError(RuntimeError):
+    def __init__(self, status, msg):
+        super().__init__(f"c3c status {status}: {msg}")
+        self.status = status
+
+
+class Desc(C.Structure):
+    _fields_ = [(n, C.c_int64) for n in
+                ("N", "Ci", "Co", "T", "Tc", "H", "W", "Kt", "Kh", "Kw",
+                 "stride_t", "stride_h", "stride_w", "dil_t", "dil_h", "dil_w",
+                 "pad_t_base", "pad_t_right", "pad_h", "pad_w", "groups")] + \
+               [("dtype", C.c_int32), ("has_bias", C.c_int32)]
+
+
+class Counters(C.Structure):
+    _fields_ = [(n, C.c_uint64) for n in ("calls", "fast", "fallback", "unsupported", "forced",
+                                          "fast_error", "strict_rejects", "repacks")]
+
+
+class SigCount(C.Structure):
+    _fields_ = [("reason", C.c_int32), ("reserved", C.c_int32), ("desc", Desc),
+                ("count", C.c_uint64)]
+
+
+lib = C.CDLL(LIB_PATH)
+_P, _vp, _i64 = C.POINTER, C.c_void_p, C.c_int64
+lib.c3c_ctx_create.argtypes = [C.c_uint32, _P(_vp)]
+lib.c3c_ctx_destroy.argtypes = [_vp]
+lib.c3c_set_mode.argtypes = [_vp, C.c_uint32]
+lib.c3c_get_mode.argtypes = [_vp, _P(C.c_uint32)]
+lib.c3c_output_dims.argtypes = [_P(Desc), _P(_i64), _P(_i64), _P(_i64), _P(_i64)]
+lib.c3c_tap_interval.argtypes = [_P(Desc), _i64, _P(_i64), _P(_i64)]
+lib.c3c_flops.argtypes = [_P(Desc), _P(C.c_double)]
+lib.c3c_route_query.argtypes = [_vp, _P(Desc), _P(C.c_int), _P(C.c_int)]
+lib.c3c_weight_pack_bytes.argtypes = [_P(Desc), _P(C.c_size_t)]
+lib.c3c_weight_repack.argtypes = [_vp, _P(Desc), _vp, _vp, _vp]
+lib.c3c_weight_unpack.argtypes = [_P(Desc), _vp, _vp, _vp]
+lib.c3c_conv3d_causal_cached.argtypes = [_vp, _P(Desc), _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp]
+lib.c3c_counters_get.argtypes = [_vp, _P(Counters)]
+lib.c3c_counters_reset.argtypes = [_vp]
+lib.c3c_fallback_shapes.argtypes = [_vp, _P(SigCount), C.c_int, _P(C.c_int)]
+lib.c3c_strerror.argtypes = [C.c_int]
+lib.c3c_strerror.restype = C.c_char_p
+lib.c3c_last_error.argtypes = [_vp]
+lib.c3c_last_error.restype = C.c_char_p
+
+
+def declared_symbols():
+    """Function names declared in include/c3c.h."""
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:int|const char\*)\s+(c3c_\w+)\s*\(", text, re.M)))
+
+
+def make_desc(spec: dict, dtype: str) -> Desc:
+    d = Desc()
+    d.N, d.Ci, d.Co, d.T, d.Tc = spec["N"], spec["Ci"], spec["Co"], spec["T"], spec["Tc"]
+    d.H, d.W, d.Kt, d.Kh, d.Kw = spec["H"], spec["W"], spec["Kt"], spec["Kh"], spec["Kw"]
+    d.stride_t, d.stride_h, d.stride_w = spec["s_t"], spec["s_h"], spec["s_w"]
+    d.dil_t, d.dil_h, d.dil_w = spec["d_t"], spec["d_h"], spec["d_w"]
+    d.pad_t_base, d.pad_t_right = spec["p_base"], spec["p_r"]
+    d.pad_h, d.pad_w, d.groups = spec["p_h"], spec["p_w"], spec["groups"]
+    d.dtype = DTYPES[dtype]
+    d.has_bias = int(spec["has_bias"])
+    return d
+
+
+def _raise(status, ctx=None, what=""):
+    if status != OK:
+        msg = lib.c3c_strerror(status).decode()
+        if ctx is not None:
+            extra = lib.c3c_last_error(ctx._h).decode()
+            if extra:
+                msg += f" ({extra})"
+        raise C3CError(status, f"{what}: {msg}")
+
+
+class Context:
+    """A c3c_ctx: mode bits, route counters and the fallback-shape histogram."""
+
+    def __init__(self, mode: int = 0):
+        h = _vp()
+        _raise(lib.c3c_ctx_create(mode, C.byref(h)), what="c3c_ctx_create")
+        self._h = h
+
+    def close(self):
+        if self._h:
+            lib.c3c_ctx_destroy(self._h)
+            self._h = _vp()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    @property
+    def mode(self) -> int:
+        m = C.c_uint32()
+        _raise(lib.c3c_get_mode(self._h, C.byref(m)), self, "c3c_get_mode")
+        return m.value
+
+    @mode.setter
+    def mode(self, m: int):
+        _raise(lib.c3c_set_mode(self._h, m), self, "c3c_set_mode")
+
+    def counters(self) -> dict:
+        c = Counters()
+        _raise(lib.c3c_counters_get(self._h, C.byref(c)), self, "c3c_counters_get")
+        return {n: int(getattr(c, n)) for n, _ in Counters._fields_}
+
+    def reset(self):
+        _raise(lib.c3c_counters_reset(self._h), self, "c3c_counters_reset")
+
+    def fallback_shapes(self):
+        """[(reason, desc fields dict, count)] in first-seen order."""
+        n = C.c_int()
+        _raise(lib.c3c_fallback_shapes(self._h, None, 0, C.byref(n)), self, "c3c_fallback_shapes")
+        arr = (SigCount * max(n.value, 1))()
+        _raise(lib.c3c_fallback_shapes(self._h, arr, n.value, C.byref(n)), self,
+               "c3c_fallback_shapes")
+        out = []
+        for i in range(n.value):
+            e = arr[i]
+            out.append((REASONS[e.reason], {f: getattr(e.desc, f) for f, _ in Desc._fields_},
+                        int(e.count)))
+        return out
+
+    @property
+    def last_error(self) -> str:
+        return lib.c3c_last_error(self._h).decode()
+
+
+# ---------------------------------------------------------------- host maths
+
+def output_dims(spec: dict, dtype: str = "bf16"):
+    v = [_i64() for _ in range(4)]
+    _raise(lib.c3c_output_dims(C.byref(make_desc(spec, dtype)), *[C.byref(x) for x in v]),
+           what="c3c_output_dims")
+    return tuple(int(x.value) for x in v)
+
+
+def tap_interval(spec: dict, k: int, dtype: str = "bf16"):
+    lo, hi = _i64(), _i64()
+    _raise(lib.c3c_tap_interval(C.byref(make_desc(spec, dtype)), k, C.byref(lo), C.byref(hi)),
+           what="c3c_tap_interval")
+    return int(lo.value), int(hi.value)
+
+
+def flops(spec: dict, dtype: str = "bf16") -> float:
+    f = C.c_double()
+    _raise(lib.c3c_flops(C.byref(make_desc(spec, dtype)), C.byref(f)), what="c3c_flops")
+    return f.value
+
+
+def route_query(ctx, spec: dict, dtype: str):
+    r, why = C.c_int(), C.c_int()
+    _raise(lib.c3c_route_query(ctx._h if ctx is not None else None,
+                               C.byref(make_desc(spec, dtype)), C.byref(r), C.byref(why)),
+           ctx, "c3c_route_query")
+    return ROUTES[r.value], REASONS[why.value]
+
+
+def weight_pack_bytes(spec: dict, dtype: str) -> int:
+    n = C.c_size_t()
+    _raise(lib.c3c_weight_pack_bytes(C.byref(make_desc(spec, dtype)), C.byref(n)),
+           what="c3c_weight_pack_bytes")
+    return int(n.value)
+
+
+# ---------------------------------------------------------------- device calls
+
+_TORCH = {}
+
+
+def _torch_dtype(dtype):
+    import torch
+    return {"bf16": torch.bfloat16, "f32": torch.float32, "f16": torch.float16}[dtype]
+
+
+def dtype_of(t) -> str:
+    import torch
+    return {torch.bfloat16: "bf16", torch.float32: "f32", torch.float16: "f16"}[t.dtype]
+
+
+def _ptr(t, name, dtype, numel=None):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if t.dtype != _torch_dtype(dtype):
+        raise ValueError(f"{name} has dtype {t.dtype}, expected {dtype}")
+    if numel is not None and t.numel() != numel:
+        raise ValueError(f"{name} has {t.numel()} elements, expected {numel}")
+    return t.data_ptr() or None
+
+
+def _stream(stream):
+    import torch
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    return getattr(stream, "cuda_stream", stream)
+
+
+def weight_repack(ctx, spec: dict, w, wpack=None, stream=None):
+    """Pack w into the fast route's matrix-core layout (a new device buffer
+    unless ``wpack`` is given).  Returns the packed buffer."""
+    import torch
+    dtype = dtype_of(w)
+    nbytes = weight_pack_bytes(spec, dtype)
+    if wpack is None:
+        wpack = torch.empty(nbytes // w.element_size(), dtype=w.dtype, device=w.device)
+    _raise(lib.c3c_weight_repack(ctx._h if ctx is not None else None,
+                                 C.byref(make_desc(spec, dtype)), _ptr(w, "w", dtype),
+                                 _ptr(wpack, "wpack", dtype, nbytes // w.element_size()),
+                                 _stream(stream)), ctx, "c3c_weight_repack")
+    return wpack
+
+
+def weight_unpack(spec: dict, wpack, out=None, stream=None):
+    import torch
+    dtype = dtype_of(wpack)
+    if out is None:
+        out = torch.empty((spec["Co"], spec["Ci"] // spec["groups"], spec["Kt"], spec["Kh"],
+                           spec["Kw"]), dtype=wpack.dtype, device=wpack.device)
+    _raise(lib.c3c_weight_unpack(C.byref(make_desc(spec, dtype)), _ptr(wpack, "wpack", dtype),
+                                 _ptr(out, "w_out", dtype), _stream(stream)),
+           what="c3c_weight_unpack")
+    return out
+
+
+def conv3d_causal_cached(ctx, spec: dict, x, cache, w, wpack, bias, y=None, cache_out=None,
+                         stream=None):
+    """One cached causal Conv3D call.  Returns (y, cache_out); allocates the
+    outputs with torch when they are not given."""
+    import torch
+    dtype = dtype_of(w)
+    To, Ho, Wo, L = output_dims(spec, dtype)
+    dev = w.device
+    if y is None:
+        y = torch.empty((spec["N"], spec["Co"], To, Ho, Wo), dtype=w.dtype, device=dev)
+    if cache_out is None:
+        cache_out = torch.empty((spec["N"], spec["Ci"], L, spec["H"], spec["W"]),
+                                dtype=w.dtype, device=dev)
+    hw = spec["H"] * spec["W"]
+    st = lib.c3c_conv3d_causal_cached(
+        ctx._h, C.byref(make_desc(spec, dtype)),
+        _ptr(x, "x", dtype, spec["N"] * spec["Ci"] * spec["T"] * hw),
+        _ptr(cache, "cache", dtype, spec["N"] * spec["Ci"] * spec["Tc"] * hw) if spec["Tc"] else None,
+        _ptr(w, "w", dtype), _ptr(wpack, "wpack", dtype),
+        _ptr(bias, "bias", dtype, spec["Co"]) if spec["has_bias"] else None,
+        _ptr(y, "y", dtype), _ptr(cache_out, "cache_out", dtype), _stream(stream))
+    _raise(st, ctx, "c3c_conv3d_causal_cached")
+    return y, cache_out

@@ -1,0 +1,326 @@
+// Fast route: the cache-aware lowering of a causal Conv3D (paper Sec. 4,
+// Eq. 2 and Eq. 4, Alg. 1) as ONE implicit-GEMM kernel on gfx950 matrix cores.
+//
+// The paper evaluates each active temporal tap k as a batched Conv2D over the
+// frames [z_l, z_h) of Z = [C; X]_T, folded into the batch, and sums the taps
+// into an accumulator before adding the bias once.  Here the fold is only an
+// index map: a workgroup owns an output tile (one frame o, a BH x BW block of
+// pixels, a block of output channels) and, for every tap whose Eq. 4 interval
+// contains o, reads source frame o + delta_k straight from the cache or from
+// the new chunk (no concatenated copy of Z), so all taps accumulate in fp32
+// registers.  The bias is added once in the epilogue.
+//
+// GEMM view per output frame: D[co][px] = sum_K A[co][K] * B[K][px] with
+// K = (tap kt, kh, kw, input channel).  A (weights) comes pre-packed in
+// matrix-core fragment order; B (activations) is staged through LDS as a halo
+// tile [BH+2][BW+2][channels], channel-innermost, so that each lane reads its
+// K-contiguous operand with one LDS load and the nine spatial offsets of a
+// 3x3 kernel are nine address shifts into the same tile.
+#include "c3c_internal.h"
+
+namespace c3c {
+
+PackDims pack_dims(const c3c_conv_desc& d) {
+  PackDims p;
+  p.kpl = d.dtype == C3C_DTYPE_F32 ? 1 : 8;
+  p.kstep = 2 * p.kpl;
+  p.taps = d.Kt * d.Kh * d.Kw;
+  p.chunks = (d.Ci + p.kstep - 1) / p.kstep;
+  p.cofrags = (d.Co + 31) / 32;
+  return p;
+}
+
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// ---------------------------------------------------------------- repack
+// packed index (tap, chunk, cofrag, lane, e) <-> w[co][ci][tap]
+template <typename T>
+__global__ __launch_bounds__(256) void repack_kernel(const T* __restrict__ w, T* __restrict__ wp,
+                                                     int64_t total, int64_t Ci, int64_t Co,
+                                                     int64_t taps, int64_t chunks,
+                                                     int64_t cofrags, int kpl) {
+  for (int64_t idx = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x; idx < total;
+       idx += static_cast<int64_t>(gridDim.x) * 256) {
+    int64_t r = idx;
+    const int e = static_cast<int>(r % kpl);
+    r /= kpl;
+    const int lane = static_cast<int>(r % 64);
+    r /= 64;
+    const int64_t cf = r % cofrags;
+    r /= cofrags;
+    const int64_t ch = r % chunks;
+    const int64_t tap = r / chunks;
+    const int64_t co = cf * 32 + (lane & 31);
+    const int64_t ci = ch * 2 * kpl + (lane >> 5) * kpl + e;
+    T v = T(0);
+    if (co < Co && ci < Ci) v = w[(co * Ci + ci) * taps + tap];
+    wp[idx] = v;
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void unpack_kernel(const T* __restrict__ wp, T* __restrict__ w,
+                                                     int64_t total, int64_t Ci, int64_t taps,
+                                                     int64_t chunks, int64_t cofrags, int kpl) {
+  for (int64_t idx = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x; idx < total;
+       idx += static_cast<int64_t>(gridDim.x) * 256) {
+    const int64_t tap = idx % taps;
+    const int64_t ci = (idx / taps) % Ci;
+    const int64_t co = idx / (taps * Ci);
+    const int64_t kstep = 2 * kpl;
+    const int64_t ch = ci / kstep, rem = ci % kstep;
+    const int64_t lane = (co & 31) + 32 * (rem / kpl);
+    const int64_t e = rem % kpl;
+    const int64_t cf = co / 32;
+    w[idx] = wp[((((tap * chunks + ch) * cofrags + cf) * 64 + lane) * kpl) + e];
+  }
+}
+
+// ---------------------------------------------------------------- conversions
+__device__ inline uint16_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return static_cast<uint16_t>((u >> 16) | 0x40u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return static_cast<uint16_t>(u >> 16);
+}
+
+// ---------------------------------------------------------------- matrix-core policy
+// bf16: v_mfma_f32_32x32x16_bf16, each lane supplies 8 consecutive K values.
+// fp32: v_mfma_f32_32x32x2_f32, each lane supplies 1 K value.
+// Output fragment (both): lane l holds D[row][col = l % 32] for the 16 rows
+// row = 8 * (r / 4) + 4 * (l / 32) + (r % 4), r = 0..15.
+template <typename T>
+struct Mma;
+
+template <>
+struct Mma<uint16_t> {
+  static constexpr int KPL = 8, KSTEP = 16, BKC = 32, PIXS = 40;  // PIXS: LDS elems per pixel
+  typedef u32x4 frag;
+  static __device__ inline frag zero() { return frag{0u, 0u, 0u, 0u}; }
+  static __device__ inline frag load(const uint16_t* p) { return *reinterpret_cast<const frag*>(p); }
+  static __device__ inline f32x16 mma(frag a, frag b, f32x16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
+                                                   __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+  }
+  static __device__ inline float to_f(uint16_t v) { return __uint_as_float(static_cast<uint32_t>(v) << 16); }
+  static __device__ inline uint16_t from_f(float v) { return f32_to_bf16(v); }
+};
+
+template <>
+struct Mma<float> {
+  static constexpr int KPL = 1, KSTEP = 2, BKC = 16, PIXS = 17;
+  typedef float frag;
+  static __device__ inline frag zero() { return 0.f; }
+  static __device__ inline frag load(const float* p) { return *p; }
+  static __device__ inline f32x16 mma(frag a, frag b, f32x16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
+  }
+  static __device__ inline float to_f(float v) { return v; }
+  static __device__ inline float from_f(float v) { return v; }
+};
+
+struct FastArgs {
+  const void* x;
+  const void* cache;
+  const void* wpack;
+  const void* bias;
+  void* y;
+  int64_t Ci, Co, T, Tc, H, W;
+  int64_t Kt, dt, p_l, Z, To;
+  int64_t chunks, cofrags;
+  int tiles_co, tiles_w, tiles_h;
+  int has_bias;
+};
+
+// Workgroup tile: BCO = 32 * CO_FRAGS * WAVES_CO output channels by
+// BH rows x (32 * BWF) columns of one output frame.  Wave (wco, wpx) owns
+// CO_FRAGS x PX_FRAGS 32x32 accumulator fragments.
+template <typename T, int CO_FRAGS, int PX_FRAGS, int WAVES_CO, int WAVES_PX, int BH, int BWF>
+__global__ __launch_bounds__(64 * WAVES_CO * WAVES_PX) void fast_conv3d(FastArgs a) {
+  using M = Mma<T>;
+  static_assert(WAVES_PX * PX_FRAGS == BH * BWF, "pixel fragments must tile the block");
+  constexpr int NT = 64 * WAVES_CO * WAVES_PX;
+  constexpr int BW = 32 * BWF;
+  constexpr int TW = BW + 2, TH = BH + 2;  // halo tile for a 3x3 kernel, pad 1
+  constexpr int BKC = M::BKC, PIXS = M::PIXS, KSTEP = M::KSTEP, KPL = M::KPL;
+  __shared__ __align__(16) T tile[TH * TW * PIXS];
+
+  const T* __restrict__ x = static_cast<const T*>(a.x);
+  const T* __restrict__ cache = static_cast<const T*>(a.cache);
+  const typename M::frag* __restrict__ wp = static_cast<const typename M::frag*>(a.wpack);
+  const T* __restrict__ bias = static_cast<const T*>(a.bias);
+  T* __restrict__ y = static_cast<T*>(a.y);
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wco = wave % WAVES_CO, wpx = wave / WAVES_CO;
+
+  int64_t id = blockIdx.x;
+  const int ct = static_cast<int>(id % a.tiles_co);
+  id /= a.tiles_co;
+  const int tw = static_cast<int>(id % a.tiles_w);
+  id /= a.tiles_w;
+  const int th = static_cast<int>(id % a.tiles_h);
+  id /= a.tiles_h;
+  const int64_t o = id % a.To, n = id / a.To;
+  const int h0 = th * BH, w0 = tw * BW;
+  const int64_t hw = a.H * a.W;
+  const int cofrag0 = (ct * WAVES_CO + wco) * CO_FRAGS;
+
+  f32x16 acc[CO_FRAGS][PX_FRAGS];
+#pragma unroll
+  for (int i = 0; i < CO_FRAGS; ++i)
+#pragma unroll
+    for (int j = 0; j < PX_FRAGS; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+  for (int64_t k = 0; k < a.Kt; ++k) {
+    // Eq. 4: tap k is active for this frame iff its source frame lies in Z.
+    const int64_t f = o + k * a.dt - a.p_l;
+    if (f < 0 || f >= a.Z) continue;
+    const T* src;
+    int64_t cstride;
+    if (f < a.Tc) {
+      src = cache + (n * a.Ci * a.Tc + f) * hw;
+      cstride = a.Tc * hw;
+    } else {
+      src = x + (n * a.Ci * a.T + (f - a.Tc)) * hw;
+      cstride = a.T * hw;
+    }
+    for (int64_t c0 = 0; c0 < a.Ci; c0 += BKC) {
+      __syncthreads();
+      // stage the halo tile: rows h0-1 .. h0+BH, cols w0-1 .. w0+BW, BKC channels
+      for (int e = tid; e < BKC * TH * TW; e += NT) {
+        const int cc = e % TW, rr = (e / TW) % TH, ch = e / (TW * TH);
+        const int gh = h0 - 1 + rr, gw = w0 - 1 + cc;
+        T v = T(0);
+        if (c0 + ch < a.Ci && gh >= 0 && gh < a.H && gw >= 0 && gw < a.W)
+          v = src[(c0 + ch) * cstride + static_cast<int64_t>(gh) * a.W + gw];
+        tile[(rr * TW + cc) * PIXS + ch] = v;
+      }
+      __syncthreads();
+#pragma unroll 1
+      for (int ij = 0; ij < 9; ++ij) {
+        const int ki = ij / 3, kj = ij % 3;
+        const int64_t tap = k * 9 + ij;
+#pragma unroll
+        for (int ks = 0; ks < BKC / KSTEP; ++ks) {
+          const int64_t chunk = c0 / KSTEP + ks;
+          if (chunk >= a.chunks) break;
+          typename M::frag af[CO_FRAGS], bf[PX_FRAGS];
+#pragma unroll
+          for (int cf = 0; cf < CO_FRAGS; ++cf) {
+            const int cofrag = cofrag0 + cf;
+            af[cf] = cofrag < a.cofrags ? wp[((tap * a.chunks + chunk) * a.cofrags + cofrag) * 64 + lane]
+                                        : M::zero();
+          }
+#pragma unroll
+          for (int pf = 0; pf < PX_FRAGS; ++pf) {
+            const int q = wpx * PX_FRAGS + pf;
+            const int r = q / BWF, cb = (q % BWF) * 32;
+            bf[pf] = M::load(&tile[((r + ki) * TW + cb + (lane & 31) + kj) * PIXS + ks * KSTEP +
+                                   (lane >> 5) * KPL]);
+          }
+#pragma unroll
+          for (int cf = 0; cf < CO_FRAGS; ++cf)
+#pragma unroll
+            for (int pf = 0; pf < PX_FRAGS; ++pf) acc[cf][pf] = M::mma(af[cf], bf[pf], acc[cf][pf]);
+        }
+      }
+    }
+  }
+
+  // epilogue: bias once, round to the storage type, NCTHW store
+  const int64_t Ho = a.H, Wo = a.W;
+#pragma unroll
+  for (int cf = 0; cf < CO_FRAGS; ++cf) {
+    const int cofrag = cofrag0 + cf;
+#pragma unroll
+    for (int pf = 0; pf < PX_FRAGS; ++pf) {
+      const int q = wpx * PX_FRAGS + pf;
+      const int h = h0 + q / BWF, wc = w0 + (q % BWF) * 32 + (lane & 31);
+      if (h >= Ho || wc >= Wo) continue;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int64_t co = static_cast<int64_t>(cofrag) * 32 + 8 * (r / 4) + 4 * (lane >> 5) + (r & 3);
+        if (co >= a.Co) continue;
+        float v = acc[cf][pf][r];
+        if (a.has_bias) v += M::to_f(bias[co]);
+        y[((n * a.Co + co) * a.To + o) * Ho * Wo + static_cast<int64_t>(h) * Wo + wc] = M::from_f(v);
+      }
+    }
+  }
+}
+
+template <typename T, int CO_FRAGS, int PX_FRAGS, int WAVES_CO, int WAVES_PX, int BH, int BWF>
+hipError_t run_fast(const Geo& g, FastArgs a, hipStream_t s) {
+  constexpr int BCO = 32 * CO_FRAGS * WAVES_CO, BW = 32 * BWF;
+  a.tiles_co = static_cast<int>((g.d.Co + BCO - 1) / BCO);
+  a.tiles_w = static_cast<int>((g.Wo + BW - 1) / BW);
+  a.tiles_h = static_cast<int>((g.Ho + BH - 1) / BH);
+  const int64_t blocks = static_cast<int64_t>(a.tiles_co) * a.tiles_w * a.tiles_h * g.To * g.d.N;
+  if (blocks == 0) return hipSuccess;
+  if (blocks > 0x7fffffff) return hipErrorInvalidConfiguration;
+  hipLaunchKernelGGL((fast_conv3d<T, CO_FRAGS, PX_FRAGS, WAVES_CO, WAVES_PX, BH, BWF>),
+                     dim3(static_cast<unsigned>(blocks)), dim3(64 * WAVES_CO * WAVES_PX), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_repack(const Geo& g, const void* w, void* wpack, hipStream_t s) {
+  const PackDims p = pack_dims(g.d);
+  const int64_t total = p.elems();
+  int64_t blocks = (total + 255) / 256;
+  if (blocks > 65536) blocks = 65536;
+  if (g.d.dtype == C3C_DTYPE_F32)
+    hipLaunchKernelGGL(repack_kernel<float>, dim3(blocks), dim3(256), 0, s,
+                       static_cast<const float*>(w), static_cast<float*>(wpack), total, g.d.Ci,
+                       g.d.Co, p.taps, p.chunks, p.cofrags, p.kpl);
+  else
+    hipLaunchKernelGGL(repack_kernel<uint16_t>, dim3(blocks), dim3(256), 0, s,
+                       static_cast<const uint16_t*>(w), static_cast<uint16_t*>(wpack), total,
+                       g.d.Ci, g.d.Co, p.taps, p.chunks, p.cofrags, p.kpl);
+  return hipGetLastError();
+}
+
+hipError_t launch_unpack(const Geo& g, const void* wpack, void* w, hipStream_t s) {
+  const PackDims p = pack_dims(g.d);
+  const int64_t total = g.d.Co * g.d.Ci * p.taps;
+  int64_t blocks = (total + 255) / 256;
+  if (blocks > 65536) blocks = 65536;
+  if (g.d.dtype == C3C_DTYPE_F32)
+    hipLaunchKernelGGL(unpack_kernel<float>, dim3(blocks), dim3(256), 0, s,
+                       static_cast<const float*>(wpack), static_cast<float*>(w), total, g.d.Ci,
+                       p.taps, p.chunks, p.cofrags, p.kpl);
+  else
+    hipLaunchKernelGGL(unpack_kernel<uint16_t>, dim3(blocks), dim3(256), 0, s,
+                       static_cast<const uint16_t*>(wpack), static_cast<uint16_t*>(w), total,
+                       g.d.Ci, p.taps, p.chunks, p.cofrags, p.kpl);
+  return hipGetLastError();
+}
+
+hipError_t launch_fast(const Geo& g, const void* x, const void* cache, const void* wpack,
+                       const void* bias, void* y, void* cache_out, hipStream_t s) {
+  const PackDims p = pack_dims(g.d);
+  FastArgs a;
+  a.x = x; a.cache = cache; a.wpack = wpack; a.bias = bias; a.y = y;
+  a.Ci = g.d.Ci; a.Co = g.d.Co; a.T = g.d.T; a.Tc = g.d.Tc; a.H = g.d.H; a.W = g.d.W;
+  a.Kt = g.d.Kt; a.dt = g.d.dil_t; a.p_l = g.p_l; a.Z = g.Z; a.To = g.To;
+  a.chunks = p.chunks; a.cofrags = p.cofrags;
+  a.has_bias = g.d.has_bias ? 1 : 0;
+  a.tiles_co = a.tiles_w = a.tiles_h = 0;
+  hipError_t e;
+  if (g.d.dtype == C3C_DTYPE_F32)
+    e = run_fast<float, 1, 2, 1, 4, 4, 2>(g, a, s);
+  else
+    e = run_fast<uint16_t, 2, 2, 2, 2, 2, 2>(g, a, s);
+  if (e != hipSuccess) return e;
+  return launch_cache_copy(g, x, cache, cache_out, s);
+}
+
+}  // namespace c3c

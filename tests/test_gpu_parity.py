@@ -1,0 +1,205 @@
+"""GPU parity: the HIP library (called through its C ABI) against the CPU
+oracle, element by element on the same seeded inputs.
+
+Bar: max|err| / max|ref| <= 1e-5 (fp32) and <= 2e-2 (bf16) per output tensor
+per call; cache contents, route counters and output shapes bit-exact; no
+NaN/Inf; every output element written (poisoned buffers).
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2609_31938_amd import c3c, inputs
+from paper_2609_31938_amd.inputs import spec
+
+from gpu_util import (TOL, as_f64, check, chunk, host, layer, metrics, oracle_args, run,
+                      sample_indices, say)
+
+pytestmark = pytest.mark.gpu
+
+
+def _case(sp, dtype, mode=0, seed=0, poison=True):
+    """One call on fresh inputs, compared in full with the oracle."""
+    say(f"case {dtype} {sp} mode={mode}")
+    ctx = c3c.Context(mode)
+    w, b = layer(sp, dtype, 901, seed)
+    x = chunk(sp, dtype, 901, seed, 0)
+    cache = chunk(dict(sp, T=sp["Tc"]), dtype, 901, seed, 1)
+    wpack = None
+    if c3c.route_query(None, sp, dtype)[0] == "fast":
+        wpack = c3c.weight_repack(ctx, sp, w)
+    To, Ho, Wo, L = c3c.output_dims(sp, dtype)
+    y = torch.empty((sp["N"], sp["Co"], To, Ho, Wo), dtype=w.dtype, device="cuda")
+    co = torch.empty((sp["N"], sp["Ci"], L, sp["H"], sp["W"]), dtype=w.dtype, device="cuda")
+    if poison:
+        y.fill_(float("nan"))
+        co.fill_(float("nan"))
+    y, co = c3c.conv3d_causal_cached(ctx, sp, x, cache, w, wpack, b, y, co)
+    torch.cuda.synchronize()
+    args = oracle_args(sp, x, cache, w, b)
+    ref = oracle.conv3d(sp, dtype, *args)
+    assert tuple(y.shape) == ref.shape
+    m = check(as_f64(y), ref, dtype, str(sp))
+    ref_cache = oracle.cache_update(sp, dtype, args[0], args[1])
+    got_cache = host(co)
+    if dtype == "bf16":
+        got_cache = got_cache.view(torch.int16).numpy().view(np.uint16)
+    else:
+        got_cache = got_cache.numpy()
+    assert np.array_equal(got_cache, ref_cache)
+    return ctx, y, m
+
+
+# ---------------------------------------------------------------- repack
+
+@pytest.mark.parametrize("Ci,Co,dtype", [(48, 80, "bf16"), (384, 384, "bf16"), (3, 5, "bf16"),
+                                         (32, 32, "f32"), (7, 45, "f32")])
+def test_repack_round_trip(Ci, Co, dtype):
+    sp = spec(N=1, Ci=Ci, Co=Co, T=2, Tc=2, H=4, W=4)
+    say(f"repack {Ci}->{Co} {dtype}")
+    ctx = c3c.Context()
+    w, _ = layer(sp, dtype)
+    wp = c3c.weight_repack(ctx, sp, w)
+    back = c3c.weight_unpack(sp, wp)
+    torch.cuda.synchronize()
+    assert torch.equal(back.view(torch.int16) if dtype == "bf16" else back,
+                       w.view(torch.int16) if dtype == "bf16" else w)
+    assert ctx.counters()["repacks"] == 1
+    # the padding of partial fragments is zero: total |wpack| == total |w|
+    assert torch.equal(wp.float().abs().sum(), w.float().abs().sum())
+
+
+# ---------------------------------------------------------------- fast route
+
+FAST_CASES = [
+    ("bf16", dict(N=1, Ci=48, Co=80, T=3, Tc=2, H=37, W=70)),
+    ("bf16", dict(N=2, Ci=32, Co=64, T=2, Tc=1, H=9, W=33)),
+    ("bf16", dict(N=1, Ci=160, Co=96, T=4, Tc=2, H=20, W=100)),
+    ("bf16", dict(N=1, Ci=16, Co=32, T=1, Tc=0, H=5, W=5)),
+    ("bf16", dict(N=1, Ci=24, Co=40, T=2, Tc=3, H=11, W=65)),          # p_l < 0
+    ("bf16", dict(N=1, Ci=64, Co=192, T=4, Tc=2, H=16, W=64)),
+    ("bf16", dict(N=1, Ci=8, Co=8, T=5, Tc=4, H=6, W=40, d_t=2, p_base=4)),  # temporal dilation
+    ("bf16", dict(N=1, Ci=20, Co=36, T=2, Tc=2, H=7, W=9, Kt=5, p_base=4)),  # Kt = 5
+    ("bf16", dict(N=1, Ci=12, Co=20, T=3, Tc=2, H=6, W=35, p_r=1)),          # right pad
+    ("f32", dict(N=1, Ci=32, Co=32, T=2, Tc=2, H=32, W=32)),
+    ("f32", dict(N=2, Ci=7, Co=45, T=3, Tc=1, H=13, W=34)),
+    ("f32", dict(N=1, Ci=33, Co=70, T=1, Tc=2, H=10, W=66)),
+]
+
+
+@pytest.mark.parametrize("dtype,over", FAST_CASES)
+def test_fast_route_matches_oracle(dtype, over):
+    sp = spec(**over)
+    ctx, _, m = _case(sp, dtype)
+    c = ctx.counters()
+    assert (c["calls"], c["fast"], c["fallback"]) == (1, 1, 0)
+    say(f"  rel={m['rel']:.3e} cos={m['cos']:.8f}")
+
+
+# ---------------------------------------------------------------- fallback route
+
+FALLBACK_CASES = FAST_CASES + [
+    ("bf16", dict(N=1, Ci=32, Co=16, T=4, Tc=0, H=12, W=20, Kt=1, Kh=1, Kw=1)),  # 1x1x1
+    ("bf16", dict(N=2, Ci=6, Co=4, T=5, Tc=2, H=9, W=7, s_t=2)),                # stride_t 2
+    ("bf16", dict(N=1, Ci=8, Co=12, T=3, Tc=2, H=10, W=11, groups=4)),
+    ("f32", dict(N=1, Ci=5, Co=6, T=3, Tc=1, H=9, W=13, Kh=5, Kw=3, s_h=2, d_w=2, p_w=2)),
+    ("f32", dict(N=1, Ci=4, Co=4, T=2, Tc=2, H=6, W=6, p_r=2)),
+    ("f32", dict(N=1, Ci=4, Co=4, T=4, Tc=2, H=6, W=6, p_r=-1)),
+    ("f16", dict(N=1, Ci=16, Co=24, T=3, Tc=2, H=10, W=18)),
+]
+
+
+@pytest.mark.parametrize("dtype,over", FALLBACK_CASES)
+def test_fallback_route_matches_oracle(dtype, over):
+    sp = spec(**over)
+    forced = oracle.route(sp, dtype)[0] == "fast"
+    mode = c3c.MODE_FORCE_FALLBACK if forced else 0
+    ctx, _, m = _case(sp, dtype, mode)
+    c = ctx.counters()
+    assert (c["calls"], c["fast"], c["fallback"]) == (1, 0, 1)
+    assert c["forced"] == int(forced) and c["unsupported"] == int(not forced)
+    shapes = ctx.fallback_shapes()
+    assert len(shapes) == 1 and shapes[0][2] == 1
+    assert shapes[0][0] == oracle.route(sp, dtype, forced)[1]
+
+
+def test_injected_fast_failure_falls_back():
+    sp = spec(N=1, Ci=16, Co=32, T=2, Tc=2, H=8, W=40)
+    ctx, _, _ = _case(sp, "bf16", c3c.MODE_INJECT_FAST_FAILURE)
+    c = ctx.counters()
+    assert (c["calls"], c["fast"], c["fallback"], c["fast_error"]) == (1, 0, 1, 1)
+    assert ctx.fallback_shapes()[0][0] == "fast_error"
+
+
+# ---------------------------------------------------------------- edge cases
+
+def test_empty_chunk_keeps_the_cache():
+    # T = 0: no output frame (fallback, reason no_output), cache' == cache
+    sp = spec(N=1, Ci=8, Co=8, T=0, Tc=2, H=5, W=7)
+    ctx, y, _ = _case(sp, "bf16")
+    assert y.numel() == 0
+    assert ctx.fallback_shapes()[0][0] == "no_output"
+
+
+def test_first_chunk_without_cache_equals_zero_cache():
+    sp0 = spec(N=1, Ci=32, Co=48, T=3, Tc=0, H=10, W=40)
+    sp2 = dict(sp0, Tc=2)
+    ctx = c3c.Context()
+    w, b = layer(sp0, "bf16")
+    x = chunk(sp0, "bf16")
+    wp = c3c.weight_repack(ctx, sp0, w)
+    y0, c0 = run(ctx, sp0, x, None, w, wp, b)
+    zero = torch.zeros((1, 32, 2, 10, 40), dtype=torch.bfloat16, device="cuda")
+    y2, c2 = run(ctx, sp2, x, zero, w, wp, b)
+    assert torch.equal(y0.view(torch.int16), y2.view(torch.int16))
+    assert torch.equal(c0.view(torch.int16), c2.view(torch.int16))
+
+
+def test_deterministic_bitwise():
+    sp = spec(N=1, Ci=96, Co=160, T=4, Tc=2, H=24, W=72)
+    ctx = c3c.Context()
+    w, b = layer(sp, "bf16")
+    x = chunk(sp, "bf16")
+    cache = chunk(dict(sp, T=2), "bf16", ci=1)
+    wp = c3c.weight_repack(ctx, sp, w)
+    y1, _ = run(ctx, sp, x, cache, w, wp, b)
+    y2, _ = run(ctx, sp, x, cache, w, wp, b)
+    assert torch.equal(y1.view(torch.int16), y2.view(torch.int16))
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_streaming_equals_whole_sequence_on_gpu(dtype):
+    Ci, Co, H, W = 24, 40, 9, 45
+    sizes = [2, 1, 3, 2]
+    whole = spec(N=1, Ci=Ci, Co=Co, T=sum(sizes), Tc=0, H=H, W=W)
+    ctx = c3c.Context()
+    w, b = layer(whole, dtype)
+    X = chunk(whole, dtype)
+    wp = c3c.weight_repack(ctx, whole, w)
+    ref = oracle.conv3d(whole, dtype, host(X), None, host(w), host(b))
+    yw, _ = run(ctx, whole, X, None, w, wp, b)
+    check(as_f64(yw), ref, dtype, "whole")
+    cache, outs, t0 = None, [], 0
+    for T in sizes:
+        sp = spec(N=1, Ci=Ci, Co=Co, T=T, Tc=0 if cache is None else cache.shape[2], H=H, W=W)
+        y, cache = run(ctx, sp, X[:, :, t0:t0 + T].contiguous(), cache, w, wp, b)
+        outs.append(y)
+        t0 += T
+    ys = torch.cat(outs, dim=2)
+    check(as_f64(ys), ref, dtype, "streamed")
+    assert ctx.counters()["fast"] == 1 + len(sizes)
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_fuzz_off_grid_shapes(seed):
+    rng = np.random.default_rng(4242 + seed)
+    dtype = "bf16" if seed % 4 else "f32"
+    d_t = int(rng.choice([1, 1, 2]))
+    sp = spec(N=int(rng.integers(1, 3)), Ci=int(rng.integers(1, 70)), Co=int(rng.integers(1, 100)),
+              T=int(rng.integers(1, 5)), Tc=int(rng.integers(0, 4)), H=int(rng.integers(1, 23)),
+              W=int(rng.integers(1, 90)), d_t=d_t, Kt=int(rng.choice([2, 3, 3])))
+    if sp["Tc"] > sp["p_base"] + 1:
+        sp["Tc"] = sp["p_base"] + 1
+    ctx, _, m = _case(sp, dtype, seed=seed)
+    assert ctx.counters()["fast"] == 1

@@ -1,0 +1,180 @@
+"""Host-side checks of libc3c that need no GPU: the library loads and exports
+every symbol its header declares; its host maths (Eq. 3 output sizes, Eq. 4
+intervals, the FLOP count) and its route rule agree with the oracle's
+independent implementation; argument errors, strict-mode rejections and the
+counters behave as documented.
+
+The calls below that pass fake device addresses are all rejected before any
+device access (argument validation or strict mode); they are skipped where a
+GPU is present so that a validation bug could never turn into a launch on a
+bogus pointer.
+"""
+import ctypes as C
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2609_31938_amd import c3c
+from paper_2609_31938_amd.inputs import spec
+
+from test_oracle_pins import ROUTE_TABLE, _random_spec
+
+no_gpu = pytest.mark.skipif(torch.cuda.is_available(),
+                            reason="fake-pointer argument tests run on CPU-only hosts")
+
+
+def test_every_declared_symbol_is_exported():
+    names = c3c.declared_symbols()
+    assert names == sorted([
+        "c3c_ctx_create", "c3c_ctx_destroy", "c3c_set_mode", "c3c_get_mode",
+        "c3c_output_dims", "c3c_tap_interval", "c3c_flops", "c3c_route_query",
+        "c3c_weight_pack_bytes", "c3c_weight_repack", "c3c_weight_unpack",
+        "c3c_conv3d_causal_cached", "c3c_counters_get", "c3c_counters_reset",
+        "c3c_fallback_shapes", "c3c_strerror", "c3c_last_error"])
+    for n in names:
+        assert hasattr(c3c.lib, n), n
+
+
+def test_descriptor_layout_matches_header():
+    # 21 int64 fields + 2 int32 = 176 bytes, no padding surprises
+    assert C.sizeof(c3c.Desc) == 21 * 8 + 2 * 4
+    assert C.sizeof(c3c.Counters) == 8 * 8
+
+
+@pytest.mark.parametrize("case", range(300))
+def test_host_maths_match_oracle(case):
+    rng = np.random.default_rng(90000 + case)
+    sp = _random_spec(rng)
+    assert c3c.output_dims(sp) == oracle.output_dims(sp)
+    assert c3c.flops(sp) == oracle.flops(sp)
+    for dt in ("bf16", "f32", "f16"):
+        assert c3c.route_query(None, sp, dt) == oracle.route(sp, dt)
+    if sp["s_t"] == 1:
+        for k in range(sp["Kt"]):
+            assert c3c.tap_interval(sp, k) == oracle.tap_interval(sp, k)
+
+
+@pytest.mark.parametrize("over,dtype,forced,reason", ROUTE_TABLE)
+def test_route_table(over, dtype, forced, reason):
+    sp = spec(N=1, Ci=2, Co=2, T=2, Tc=2, H=4, W=4)
+    sp.update(over)
+    ctx = c3c.Context(c3c.MODE_FORCE_FALLBACK if forced else 0)
+    r, why = c3c.route_query(ctx, sp, dtype)
+    assert why == reason
+    assert r == ("fast" if reason == "none" else "fallback")
+    assert ctx.counters()["calls"] == 0  # a query counts nothing
+
+
+def test_workload_routes():
+    from paper_2609_31938_amd.inputs import WORKLOADS
+    for name, wl in WORKLOADS.items():
+        for lname, sp in wl["layers"]:
+            r, why = c3c.route_query(None, sp, wl["dtype"])
+            if sp["Kt"] == 1:
+                assert (r, why) == ("fallback", "kt1")
+            else:
+                assert (r, why) == ("fast", "none"), (name, lname)
+
+
+def test_pack_bytes_closed_form():
+    for Ci, Co in [(384, 384), (192, 192), (96, 96), (320, 160), (640, 640), (48, 80), (3, 5)]:
+        sp = spec(Ci=Ci, Co=Co, T=4, Tc=2, H=8, W=8)
+        chunks, frags = -(-Ci // 16), -(-Co // 32)
+        assert c3c.weight_pack_bytes(sp, "bf16") == 27 * chunks * frags * 64 * 8 * 2
+        chunks2 = -(-Ci // 2)
+        assert c3c.weight_pack_bytes(sp, "f32") == 27 * chunks2 * frags * 64 * 4
+    # no fast layout for a call that does not route fast
+    assert c3c.weight_pack_bytes(spec(Ci=4, Co=4, Kt=1, Kh=1, Kw=1, T=2), "bf16") == 0
+
+
+def test_invalid_descriptors_are_rejected():
+    bad = [dict(N=0), dict(Ci=0), dict(H=0), dict(T=-1), dict(Tc=-1), dict(Kt=0),
+           dict(s_h=0), dict(d_t=0), dict(p_base=-1), dict(p_h=-1), dict(groups=3),
+           dict(H=1, p_h=0)]  # Ho < 1
+    for over in bad:
+        sp = spec(N=1, Ci=4, Co=4, T=2, Tc=2, H=4, W=4)
+        sp.update(over)
+        with pytest.raises(c3c.C3CError) as e:
+            c3c.output_dims(sp)
+        assert e.value.status == c3c.E_INVAL
+    d = c3c.make_desc(spec(Ci=4, Co=4, T=2, H=4, W=4), "bf16")
+    d.dtype = 9
+    assert c3c.lib.c3c_output_dims(C.byref(d), None, None, None, None) == c3c.E_INVAL
+    d.dtype = 1
+    d.has_bias = 2
+    assert c3c.lib.c3c_output_dims(C.byref(d), None, None, None, None) == c3c.E_INVAL
+
+
+def test_context_modes():
+    ctx = c3c.Context()
+    assert ctx.mode == 0
+    ctx.mode = c3c.MODE_STRICT | c3c.MODE_FORCE_FALLBACK
+    assert ctx.mode == 3
+    with pytest.raises(c3c.C3CError):
+        ctx.mode = 8
+    h = C.c_void_p()
+    assert c3c.lib.c3c_ctx_create(16, C.byref(h)) == c3c.E_INVAL
+    assert c3c.lib.c3c_ctx_create(0, None) == c3c.E_INVAL
+    assert c3c.lib.c3c_ctx_destroy(None) == c3c.OK
+    assert c3c.lib.c3c_strerror(2).decode().startswith("unsupported")
+
+
+# ---------------------------------------------------------------------------
+# calls rejected before any device access (fake, never-dereferenced addresses)
+# ---------------------------------------------------------------------------
+
+FAKE = {"x": 0x10000000, "cache": 0x20000000, "w": 0x30000000, "wpack": 0x40000000,
+        "b": 0x50000000, "y": 0x60000000, "co": 0x70000000}
+
+
+def _call(ctx, sp, dtype="bf16", **over):
+    p = dict(FAKE)
+    p.update(over)
+    return c3c.lib.c3c_conv3d_causal_cached(ctx._h if ctx else None,
+                                            C.byref(c3c.make_desc(sp, dtype)), p["x"],
+                                            p["cache"], p["w"], p["wpack"], p["b"], p["y"],
+                                            p["co"], None)
+
+
+@no_gpu
+def test_argument_errors_are_not_counted():
+    sp = spec(N=1, Ci=4, Co=4, T=2, Tc=2, H=8, W=8)
+    ctx = c3c.Context()
+    assert _call(None, sp) == c3c.E_INVAL
+    assert _call(ctx, sp, x=None) == c3c.E_INVAL
+    assert _call(ctx, sp, cache=None) == c3c.E_INVAL
+    assert _call(ctx, sp, w=None) == c3c.E_INVAL
+    assert _call(ctx, sp, b=None) == c3c.E_INVAL
+    assert _call(ctx, sp, y=None) == c3c.E_INVAL
+    assert _call(ctx, sp, co=None) == c3c.E_INVAL
+    assert _call(ctx, sp, wpack=None) == c3c.E_INVAL        # routes fast without wpack
+    assert "wpack" in ctx.last_error
+    # cache_out aliasing the cache (in-place cache update is refused)
+    assert _call(ctx, sp, co=FAKE["cache"]) == c3c.E_INVAL
+    assert _call(ctx, sp, co=FAKE["x"] + 64) == c3c.E_INVAL
+    assert _call(ctx, sp, y=FAKE["x"]) == c3c.E_INVAL
+    assert _call(ctx, sp, y=FAKE["wpack"] + 2) == c3c.E_INVAL
+    bad = dict(sp, Ci=0)
+    assert _call(ctx, bad) == c3c.E_INVAL
+    assert ctx.counters() == dict(calls=0, fast=0, fallback=0, unsupported=0, forced=0,
+                                  fast_error=0, strict_rejects=0, repacks=0)
+
+
+@no_gpu
+def test_strict_mode_rejects_without_device_work():
+    ctx = c3c.Context(c3c.MODE_STRICT)
+    shortcut = spec(N=1, Ci=4, Co=4, T=2, Tc=0, H=8, W=8, Kt=1, Kh=1, Kw=1)
+    assert _call(ctx, shortcut, cache=None, co=None, wpack=None) == c3c.E_UNSUPPORTED
+    ctx.mode = c3c.MODE_STRICT | c3c.MODE_FORCE_FALLBACK
+    assert _call(ctx, spec(N=1, Ci=4, Co=4, T=2, Tc=2, H=8, W=8)) == c3c.E_UNSUPPORTED
+    ctx.mode = c3c.MODE_STRICT | c3c.MODE_INJECT_FAST_FAILURE
+    assert _call(ctx, spec(N=1, Ci=4, Co=4, T=2, Tc=2, H=8, W=8)) == c3c.E_INJECTED
+    assert "injected" in ctx.last_error
+    c = ctx.counters()
+    assert c["calls"] == 3 and c["strict_rejects"] == 3
+    assert c["fast"] == c["fallback"] == 0
+    assert ctx.fallback_shapes() == []
+    ctx.reset()
+    assert ctx.counters()["calls"] == 0
