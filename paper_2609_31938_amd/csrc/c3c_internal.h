@@ -19,18 +19,22 @@ struct Geo {
   int elem;     // bytes per element
 };
 
-// Fast-route packed-weight layout.  The K index of one tap (kt, kh, kw) is the
-// input channel; it is cut into chunks of KSTEP channels (16 for bf16, 2 for
-// fp32: the K extent of one matrix-core instruction) and the output channels
-// into fragments of 32.  Element (tap, chunk, cofrag, lane, e) holds
-// w[co = cofrag*32 + lane%32][ci = chunk*KSTEP + (lane/32)*KPL + e][tap],
+// Fast-route packed-weight layout, in matrix-core fragment order.  One
+// fragment covers ROWS output channels and KSTEP input channels of one kernel
+// tap (kt, kh, kw); lane l of the wave holds KPL consecutive input channels of
+// output channel row l % ROWS:
+//   bf16: v_mfma_f32_16x16x32_bf16  ROWS = 16, KSTEP = 32, KPL = 8
+//   fp32: v_mfma_f32_32x32x2_f32    ROWS = 32, KSTEP = 2,  KPL = 1
+// Element (tap, chunk, cofrag, lane, e) holds
+//   w[co = cofrag*ROWS + lane%ROWS][ci = chunk*KSTEP + (lane/ROWS)*KPL + e][tap],
 // zero outside [0, Co) x [0, Ci).
 struct PackDims {
-  int kpl;        // elements per lane (8 for bf16, 1 for fp32)
-  int kstep;      // channels per matrix-core step (2 * kpl)
+  int rows;       // output channels per fragment
+  int kpl;        // consecutive input channels per lane
+  int kstep;      // input channels per fragment = (64 / rows) * kpl
   int64_t taps;   // Kt * Kh * Kw
   int64_t chunks; // ceil(Ci / kstep)
-  int64_t cofrags;// ceil(Co / 32)
+  int64_t cofrags;// ceil(Co / rows)
   int64_t elems() const { return taps * chunks * cofrags * 64 * kpl; }
 };
 PackDims pack_dims(const c3c_conv_desc& d);
@@ -39,6 +43,11 @@ hipError_t launch_repack(const Geo& g, const void* w, void* wpack, hipStream_t s
 hipError_t launch_unpack(const Geo& g, const void* wpack, void* w, hipStream_t s);
 hipError_t launch_fast(const Geo& g, const void* x, const void* cache, const void* wpack,
                        const void* bias, void* y, void* cache_out, hipStream_t s);
+// bf16 fast kernel (conv_bf16.hip); writes cache_out itself when it can
+// (returns *cache_written = true), else the caller copies the cache.
+hipError_t launch_fast_bf16(const Geo& g, const void* x, const void* cache, const void* wpack,
+                            const void* bias, void* y, void* cache_out, bool* cache_written,
+                            hipStream_t s);
 hipError_t launch_fallback(const Geo& g, const void* x, const void* cache, const void* w,
                            const void* bias, void* y, hipStream_t s);
 hipError_t launch_cache_copy(const Geo& g, const void* x, const void* cache, void* cache_out,

@@ -1,5 +1,11 @@
-// Fast route: the cache-aware lowering of a causal Conv3D (paper Sec. 4,
-// Eq. 2 and Eq. 4, Alg. 1) as ONE implicit-GEMM kernel on gfx950 matrix cores.
+// Fast route, shared parts: the packed-weight layout and its repack / unpack
+// kernels, the dispatch of one fast call, and the fp32 kernel.  The bf16
+// kernel lives in conv_bf16.hip.
+//
+// The fp32 kernel is the same cache-aware lowering of a causal Conv3D (paper
+// Sec. 4, Eq. 2 and Eq. 4, Alg. 1) as one implicit-GEMM kernel on gfx950 fp32
+// matrix cores, in a simpler form (single-buffered LDS, no prefetch): fp32
+// calls are small validation workloads.
 //
 // The paper evaluates each active temporal tap k as a batched Conv2D over the
 // frames [z_l, z_h) of Z = [C; X]_T, folded into the batch, and sums the taps
@@ -22,11 +28,13 @@ namespace c3c {
 
 PackDims pack_dims(const c3c_conv_desc& d) {
   PackDims p;
-  p.kpl = d.dtype == C3C_DTYPE_F32 ? 1 : 8;
-  p.kstep = 2 * p.kpl;
+  const bool f32 = d.dtype == C3C_DTYPE_F32;
+  p.rows = f32 ? 32 : 16;
+  p.kpl = f32 ? 1 : 8;
+  p.kstep = (64 / p.rows) * p.kpl;
   p.taps = d.Kt * d.Kh * d.Kw;
   p.chunks = (d.Ci + p.kstep - 1) / p.kstep;
-  p.cofrags = (d.Co + 31) / 32;
+  p.cofrags = (d.Co + p.rows - 1) / p.rows;
   return p;
 }
 
@@ -42,7 +50,8 @@ template <typename T>
 __global__ __launch_bounds__(256) void repack_kernel(const T* __restrict__ w, T* __restrict__ wp,
                                                      int64_t total, int64_t Ci, int64_t Co,
                                                      int64_t taps, int64_t chunks,
-                                                     int64_t cofrags, int kpl) {
+                                                     int64_t cofrags, int rows, int kpl) {
+  const int kstep = (64 / rows) * kpl;
   for (int64_t idx = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x; idx < total;
        idx += static_cast<int64_t>(gridDim.x) * 256) {
     int64_t r = idx;
@@ -54,8 +63,8 @@ __global__ __launch_bounds__(256) void repack_kernel(const T* __restrict__ w, T*
     r /= cofrags;
     const int64_t ch = r % chunks;
     const int64_t tap = r / chunks;
-    const int64_t co = cf * 32 + (lane & 31);
-    const int64_t ci = ch * 2 * kpl + (lane >> 5) * kpl + e;
+    const int64_t co = cf * rows + lane % rows;
+    const int64_t ci = ch * kstep + (lane / rows) * kpl + e;
     T v = T(0);
     if (co < Co && ci < Ci) v = w[(co * Ci + ci) * taps + tap];
     wp[idx] = v;
@@ -65,17 +74,18 @@ __global__ __launch_bounds__(256) void repack_kernel(const T* __restrict__ w, T*
 template <typename T>
 __global__ __launch_bounds__(256) void unpack_kernel(const T* __restrict__ wp, T* __restrict__ w,
                                                      int64_t total, int64_t Ci, int64_t taps,
-                                                     int64_t chunks, int64_t cofrags, int kpl) {
+                                                     int64_t chunks, int64_t cofrags, int rows,
+                                                     int kpl) {
+  const int64_t kstep = (64 / rows) * kpl;
   for (int64_t idx = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x; idx < total;
        idx += static_cast<int64_t>(gridDim.x) * 256) {
     const int64_t tap = idx % taps;
     const int64_t ci = (idx / taps) % Ci;
     const int64_t co = idx / (taps * Ci);
-    const int64_t kstep = 2 * kpl;
     const int64_t ch = ci / kstep, rem = ci % kstep;
-    const int64_t lane = (co & 31) + 32 * (rem / kpl);
+    const int64_t lane = co % rows + rows * (rem / kpl);
     const int64_t e = rem % kpl;
-    const int64_t cf = co / 32;
+    const int64_t cf = co / rows;
     w[idx] = wp[((((tap * chunks + ch) * cofrags + cf) * 64 + lane) * kpl) + e];
   }
 }
@@ -89,26 +99,11 @@ __device__ inline uint16_t f32_to_bf16(float f) {
 }
 
 // ---------------------------------------------------------------- matrix-core policy
-// bf16: v_mfma_f32_32x32x16_bf16, each lane supplies 8 consecutive K values.
 // fp32: v_mfma_f32_32x32x2_f32, each lane supplies 1 K value.
-// Output fragment (both): lane l holds D[row][col = l % 32] for the 16 rows
+// Output fragment: lane l holds D[row][col = l % 32] for the 16 rows
 // row = 8 * (r / 4) + 4 * (l / 32) + (r % 4), r = 0..15.
 template <typename T>
 struct Mma;
-
-template <>
-struct Mma<uint16_t> {
-  static constexpr int KPL = 8, KSTEP = 16, BKC = 32, PIXS = 40;  // PIXS: LDS elems per pixel
-  typedef u32x4 frag;
-  static __device__ inline frag zero() { return frag{0u, 0u, 0u, 0u}; }
-  static __device__ inline frag load(const uint16_t* p) { return *reinterpret_cast<const frag*>(p); }
-  static __device__ inline f32x16 mma(frag a, frag b, f32x16 c) {
-    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
-                                                   __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
-  }
-  static __device__ inline float to_f(uint16_t v) { return __uint_as_float(static_cast<uint32_t>(v) << 16); }
-  static __device__ inline uint16_t from_f(float v) { return f32_to_bf16(v); }
-};
 
 template <>
 struct Mma<float> {
@@ -280,11 +275,11 @@ hipError_t launch_repack(const Geo& g, const void* w, void* wpack, hipStream_t s
   if (g.d.dtype == C3C_DTYPE_F32)
     hipLaunchKernelGGL(repack_kernel<float>, dim3(blocks), dim3(256), 0, s,
                        static_cast<const float*>(w), static_cast<float*>(wpack), total, g.d.Ci,
-                       g.d.Co, p.taps, p.chunks, p.cofrags, p.kpl);
+                       g.d.Co, p.taps, p.chunks, p.cofrags, p.rows, p.kpl);
   else
     hipLaunchKernelGGL(repack_kernel<uint16_t>, dim3(blocks), dim3(256), 0, s,
                        static_cast<const uint16_t*>(w), static_cast<uint16_t*>(wpack), total,
-                       g.d.Ci, g.d.Co, p.taps, p.chunks, p.cofrags, p.kpl);
+                       g.d.Ci, g.d.Co, p.taps, p.chunks, p.cofrags, p.rows, p.kpl);
   return hipGetLastError();
 }
 
@@ -296,11 +291,11 @@ hipError_t launch_unpack(const Geo& g, const void* wpack, void* w, hipStream_t s
   if (g.d.dtype == C3C_DTYPE_F32)
     hipLaunchKernelGGL(unpack_kernel<float>, dim3(blocks), dim3(256), 0, s,
                        static_cast<const float*>(wpack), static_cast<float*>(w), total, g.d.Ci,
-                       p.taps, p.chunks, p.cofrags, p.kpl);
+                       p.taps, p.chunks, p.cofrags, p.rows, p.kpl);
   else
     hipLaunchKernelGGL(unpack_kernel<uint16_t>, dim3(blocks), dim3(256), 0, s,
                        static_cast<const uint16_t*>(wpack), static_cast<uint16_t*>(w), total,
-                       g.d.Ci, p.taps, p.chunks, p.cofrags, p.kpl);
+                       g.d.Ci, p.taps, p.chunks, p.cofrags, p.rows, p.kpl);
   return hipGetLastError();
 }
 
@@ -314,11 +309,13 @@ hipError_t launch_fast(const Geo& g, const void* x, const void* cache, const voi
   a.chunks = p.chunks; a.cofrags = p.cofrags;
   a.has_bias = g.d.has_bias ? 1 : 0;
   a.tiles_co = a.tiles_w = a.tiles_h = 0;
-  hipError_t e;
-  if (g.d.dtype == C3C_DTYPE_F32)
-    e = run_fast<float, 1, 2, 1, 4, 4, 2>(g, a, s);
-  else
-    e = run_fast<uint16_t, 2, 2, 2, 2, 2, 2>(g, a, s);
+  if (g.d.dtype == C3C_DTYPE_BF16) {
+    bool written = false;
+    const hipError_t e = launch_fast_bf16(g, x, cache, wpack, bias, y, cache_out, &written, s);
+    if (e != hipSuccess || written) return e;
+    return launch_cache_copy(g, x, cache, cache_out, s);
+  }
+  const hipError_t e = run_fast<float, 1, 2, 1, 4, 4, 2>(g, a, s);
   if (e != hipSuccess) return e;
   return launch_cache_copy(g, x, cache, cache_out, s);
 }

@@ -81,10 +81,11 @@ def test_workload_routes():
 def test_pack_bytes_closed_form():
     for Ci, Co in [(384, 384), (192, 192), (96, 96), (320, 160), (640, 640), (48, 80), (3, 5)]:
         sp = spec(Ci=Ci, Co=Co, T=4, Tc=2, H=8, W=8)
-        chunks, frags = -(-Ci // 16), -(-Co // 32)
+        # bf16: 16-row x 32-channel fragments; fp32: 32-row x 2-channel fragments
+        chunks, frags = -(-Ci // 32), -(-Co // 16)
         assert c3c.weight_pack_bytes(sp, "bf16") == 27 * chunks * frags * 64 * 8 * 2
-        chunks2 = -(-Ci // 2)
-        assert c3c.weight_pack_bytes(sp, "f32") == 27 * chunks2 * frags * 64 * 4
+        chunks2, frags2 = -(-Ci // 2), -(-Co // 32)
+        assert c3c.weight_pack_bytes(sp, "f32") == 27 * chunks2 * frags2 * 64 * 4
     # no fast layout for a call that does not route fast
     assert c3c.weight_pack_bytes(spec(Ci=4, Co=4, Kt=1, Kh=1, Kw=1, T=2), "bf16") == 0
 
