@@ -36,6 +36,9 @@
  *      cache_out [N][Ci][L][H][W]          the new cache; NULL allowed iff L == 0
  *    where To is Eq. 3 with p_l = pad_t_base - Tc, Ho/Wo the spatial
  *    analogue, and L = min(pad_t_base, Tc + T).
+ *  - Size limits (EINVAL beyond them): every size below 2^31, one frame plane
+ *    (H*W and Ho*Wo elements) below 2^31 bytes, every tensor below 2^40
+ *    elements.
  */
 #ifndef C3C_H
 #define C3C_H

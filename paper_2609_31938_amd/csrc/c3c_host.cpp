@@ -88,6 +88,8 @@ const char* make_geo(const c3c_conv_desc* d, Geo* g) {
   if (g->Ho < 1 || g->Wo < 1) return "spatial output would be empty";
   g->L = d->pad_t_base < g->Z ? d->pad_t_base : g->Z;
   g->elem = elem_bytes(d->dtype);
+  if (d->H * d->W * g->elem >= big || g->Ho * g->Wo * g->elem >= big)
+    return "a frame plane exceeds 2^31 bytes";
   int64_t t;
   if (!mul_ok(d->N * d->Ci, g->Z, &t) || !mul_ok(t, d->H * d->W, &t)) return "input too large";
   if (!mul_ok(d->N * d->Co, g->To, &t) || !mul_ok(t, g->Ho * g->Wo, &t)) return "output too large";

@@ -40,63 +40,156 @@ struct FbArgs {
 };
 
 constexpr int FB_THREADS = 256;
+constexpr int FB_PPT = 2;                         // output pixels per thread
+constexpr int FB_COB = 32;                        // output channels per workgroup
+constexpr int FB_WROW = FB_COB + 4;               // LDS floats per staged pair (padded)
+constexpr int FB_PAIRS = 224;                     // (input channel, tap) pairs per chunk
+constexpr int FB_U = 8;                           // pairs whose loads are in flight together
 
-// One thread = one output pixel of one (n, t) frame, for COB output channels
-// of one group; the weights it reads are uniform across the block.
-template <typename T, int COB>
+template <typename T>
+struct Buf;
+template <>
+struct Buf<uint16_t> {
+  static __device__ inline float load(__amdgpu_buffer_rsrc_t r, uint32_t off, int is_f16) {
+    const uint16_t v = __builtin_amdgcn_raw_buffer_load_b16(r, off, 0, 0);
+    return is_f16 ? __half2float(__ushort_as_half(v)) : __uint_as_float(static_cast<uint32_t>(v) << 16);
+  }
+};
+template <>
+struct Buf<float> {
+  static __device__ inline float load(__amdgpu_buffer_rsrc_t r, uint32_t off, int) {
+    return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0));
+  }
+};
+
+// Workgroup = FB_THREADS * FB_PPT consecutive output pixels of one (n, t)
+// frame x FB_COB output channels of one group.  The weights of a chunk of
+// (input channel, tap) pairs for the FB_COB output channels are staged in
+// LDS as fp32 [pair][co]; every lane of a wave reads the same weight address
+// (a broadcast), so each input value a thread loads feeds FB_COB fp32 FMAs.
+// Input values are read through a buffer resource per source frame plane:
+// padding positions (and frames outside Z) are out-of-range offsets that
+// load as zero, so the loop has no branches and the loads of FB_U pairs are
+// in flight together.
+template <typename T>
 __global__ __launch_bounds__(FB_THREADS) void fallback_conv3d(FbArgs a, const T* __restrict__ x,
                                                               const T* __restrict__ cache,
                                                               const T* __restrict__ w,
                                                               const T* __restrict__ bias,
                                                               T* __restrict__ y) {
+  __shared__ __align__(16) float wl[FB_PAIRS * FB_WROW];
+  constexpr uint32_t OOB = 0x80000000u;
   const int64_t hwo = a.Ho * a.Wo;
-  const int64_t p = static_cast<int64_t>(blockIdx.x) * FB_THREADS + threadIdx.x;
   const int64_t cig = a.Ci / a.groups, cog = a.Co / a.groups;
-  const int64_t gblocks = (cog + COB - 1) / COB;
+  const int64_t gblocks = (cog + FB_COB - 1) / FB_COB;
   const int64_t g = blockIdx.y / gblocks;
-  const int64_t co0 = g * cog + (blockIdx.y % gblocks) * COB;
-  const int64_t co_end = min(co0 + COB, (g + 1) * cog);
+  const int64_t co0 = g * cog + (blockIdx.y % gblocks) * FB_COB;
+  const int ncob = static_cast<int>(min(static_cast<int64_t>(FB_COB), (g + 1) * cog - co0));
   const int64_t n = blockIdx.z / a.To, t = blockIdx.z % a.To;
-  const bool live = p < hwo;
-  const int64_t ho = live ? p / a.Wo : 0, wo = live ? p % a.Wo : 0;
-  const int64_t ktaps = a.Kt * a.Kh * a.Kw;
+  const int64_t taps = a.Kt * a.Kh * a.Kw;
   const int64_t hw = a.H * a.W;
+  const int64_t npairs = cig * taps;
+  const int esz = static_cast<int>(sizeof(T));
+  const int plane_bytes = static_cast<int>(hw * esz);
 
-  float acc[COB];
+  // per-pixel spatial origin of the receptive field (a plane is < 2^31 bytes)
+  int hb[FB_PPT], wb[FB_PPT];
+  bool live[FB_PPT];
+  int64_t pix[FB_PPT];
 #pragma unroll
-  for (int q = 0; q < COB; ++q) acc[q] = 0.f;
+  for (int q = 0; q < FB_PPT; ++q) {
+    const int64_t p = static_cast<int64_t>(blockIdx.x) * FB_THREADS * FB_PPT + q * FB_THREADS + threadIdx.x;
+    live[q] = p < hwo;
+    pix[q] = p;
+    const int pp = live[q] ? static_cast<int>(p) : 0;
+    const int wo = static_cast<int>(a.Wo);
+    hb[q] = (pp / wo) * static_cast<int>(a.sh) - static_cast<int>(a.ph);
+    wb[q] = (pp % wo) * static_cast<int>(a.sw) - static_cast<int>(a.pw);
+  }
+  float acc[FB_PPT][FB_COB];
+#pragma unroll
+  for (int q = 0; q < FB_PPT; ++q)
+#pragma unroll
+    for (int c = 0; c < FB_COB; ++c) acc[q][c] = 0.f;
 
-  for (int64_t c = 0; c < cig; ++c) {
-    const int64_t ci = g * cig + c;
-    for (int64_t k = 0; k < a.Kt; ++k) {
-      const int64_t tz = t * a.st + k * a.dt - a.p_l;  // Eq. 1 source frame in Z
-      if (tz < 0 || tz >= a.Z) continue;
-      const T* plane = tz < a.Tc ? cache + ((n * a.Ci + ci) * a.Tc + tz) * hw
-                                 : x + ((n * a.Ci + ci) * a.T + (tz - a.Tc)) * hw;
-      for (int64_t i = 0; i < a.Kh; ++i) {
-        const int64_t hz = ho * a.sh + i * a.dh - a.ph;
-        const bool hok = live && hz >= 0 && hz < a.H;
-        for (int64_t j = 0; j < a.Kw; ++j) {
-          const int64_t wz = wo * a.sw + j * a.dw - a.pw;
-          const bool ok = hok && wz >= 0 && wz < a.W;
-          const float v = ok ? load_f(plane, hz * a.W + wz, a.is_f16) : 0.f;
-          const int64_t widx = (c * a.Kt + k) * a.Kh * a.Kw + i * a.Kw + j;
+  const int Kt = static_cast<int>(a.Kt), Kh = static_cast<int>(a.Kh), Kw = static_cast<int>(a.Kw);
+  const int H = static_cast<int>(a.H), W = static_cast<int>(a.W);
+  const int dh = static_cast<int>(a.dh), dw = static_cast<int>(a.dw);
+  for (int64_t r0 = 0; r0 < npairs; r0 += FB_PAIRS) {
+    const int np = static_cast<int>(min(static_cast<int64_t>(FB_PAIRS), npairs - r0));
+    __syncthreads();
+    // stage w[co0 + co][pair r0 + r] -> wl[r * FB_WROW + co], pairs contiguous
+    // in global memory (pair = ci * taps + tap), so consecutive threads read
+    // consecutive pairs
+    for (int e = threadIdx.x; e < np * FB_COB; e += FB_THREADS) {
+      const int r = e % np, co = e / np;
+      wl[r * FB_WROW + co] = co < ncob ? load_f(w, (co0 + co) * npairs + r0 + r, a.is_f16) : 0.f;
+    }
+    __syncthreads();
+    // wave-uniform (ci, k, i, j) of the chunk's first pair, then advanced in order
+    int ci = static_cast<int>(r0 / taps);
+    int tap = static_cast<int>(r0 % taps);
+    int k = tap / (Kh * Kw), i = (tap / Kw) % Kh, j = tap % Kw;
+    for (int r = 0; r < np; r += FB_U) {
+      float v[FB_U][FB_PPT];
 #pragma unroll
-          for (int q = 0; q < COB; ++q) {
-            if (co0 + q < co_end) acc[q] += v * load_f(w, (co0 + q) * cig * ktaps + widx, a.is_f16);
+      for (int u = 0; u < FB_U; ++u) {
+        const int64_t tz = t * a.st + k * a.dt - a.p_l;  // Eq. 1 source frame in Z
+        const bool fok = (r + u < np) & (tz >= 0) & (tz < a.Z);
+        const int64_t cin = g * cig + ci;
+        const T* plane = !fok ? x : tz < a.Tc ? cache + ((n * a.Ci + cin) * a.Tc + tz) * hw
+                                              : x + ((n * a.Ci + cin) * a.T + (tz - a.Tc)) * hw;
+        const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<T*>(plane), 0, fok ? plane_bytes : 0, 0x00020000);
+#pragma unroll
+        for (int q = 0; q < FB_PPT; ++q) {
+          const int hz = hb[q] + i * dh, wz = wb[q] + j * dw;
+          const bool ok = live[q] & (hz >= 0) & (hz < H) & (wz >= 0) & (wz < W);
+          v[u][q] = Buf<T>::load(rs, ok ? static_cast<uint32_t>((hz * W + wz) * esz) : OOB, a.is_f16);
+        }
+        if (++j == Kw) {
+          j = 0;
+          if (++i == Kh) {
+            i = 0;
+            if (++k == Kt) {
+              k = 0;
+              ++ci;
+            }
+          }
+        }
+      }
+      // guards, never `break`: an early exit would make the accumulator
+      // indices dynamic and push the accumulators to scratch memory
+#pragma unroll
+      for (int u = 0; u < FB_U; ++u) {
+        if (r + u >= np) continue;
+        const float4* wv = reinterpret_cast<const float4*>(wl + (r + u) * FB_WROW);
+#pragma unroll
+        for (int c4 = 0; c4 < FB_COB / 4; ++c4) {
+          const float4 ww = wv[c4];
+#pragma unroll
+          for (int q = 0; q < FB_PPT; ++q) {
+            acc[q][4 * c4 + 0] += v[u][q] * ww.x;
+            acc[q][4 * c4 + 1] += v[u][q] * ww.y;
+            acc[q][4 * c4 + 2] += v[u][q] * ww.z;
+            acc[q][4 * c4 + 3] += v[u][q] * ww.w;
           }
         }
       }
     }
   }
-  if (!live) return;
 #pragma unroll
-  for (int q = 0; q < COB; ++q) {
-    const int64_t co = co0 + q;
-    if (co >= co_end) break;
-    float v = acc[q];
-    if (a.has_bias) v += load_f(bias, co, a.is_f16);  // bias added once, last
-    store_f(y, ((n * a.Co + co) * a.To + t) * hwo + p, v, a.is_f16);
+  for (int q = 0; q < FB_PPT; ++q) {
+    if (!live[q]) continue;
+    const int64_t p = pix[q];
+#pragma unroll
+    for (int c = 0; c < FB_COB; ++c) {
+      if (c >= ncob) continue;
+      const int64_t co = co0 + c;
+      float v = acc[q][c];
+      if (a.has_bias) v += load_f(bias, co, a.is_f16);  // bias added once, last
+      store_f(y, ((n * a.Co + co) * a.To + t) * hwo + p, v, a.is_f16);
+    }
   }
 }
 
@@ -113,14 +206,13 @@ hipError_t launch_fb(const Geo& g, const void* x, const void* cache, const void*
   a.Z = g.Z; a.To = g.To; a.Ho = g.Ho; a.Wo = g.Wo;
   a.has_bias = d.has_bias ? 1 : 0;
   a.is_f16 = d.dtype == C3C_DTYPE_F16;
-  constexpr int COB = 16;
   const int64_t cog = d.Co / d.groups;
-  const int64_t gx = (g.Ho * g.Wo + FB_THREADS - 1) / FB_THREADS;
-  const int64_t gy = d.groups * ((cog + COB - 1) / COB);
+  const int64_t gx = (g.Ho * g.Wo + FB_THREADS * FB_PPT - 1) / (FB_THREADS * FB_PPT);
+  const int64_t gy = d.groups * ((cog + FB_COB - 1) / FB_COB);
   const int64_t gz = d.N * g.To;
   if (gx == 0 || gz == 0) return hipSuccess;
   if (gx > 0x7fffffff || gy > 65535 || gz > 65535) return hipErrorInvalidConfiguration;
-  hipLaunchKernelGGL((fallback_conv3d<T, COB>), dim3(gx, gy, gz), dim3(FB_THREADS), 0, s, a,
+  hipLaunchKernelGGL((fallback_conv3d<T>), dim3(gx, gy, gz), dim3(FB_THREADS), 0, s, a,
                      static_cast<const T*>(x), static_cast<const T*>(cache),
                      static_cast<const T*>(w), static_cast<const T*>(bias), static_cast<T*>(y));
   return hipGetLastError();

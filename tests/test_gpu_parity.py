@@ -107,6 +107,10 @@ FALLBACK_CASES = FAST_CASES + [
     ("f32", dict(N=1, Ci=4, Co=4, T=2, Tc=2, H=6, W=6, p_r=2)),
     ("f32", dict(N=1, Ci=4, Co=4, T=4, Tc=2, H=6, W=6, p_r=-1)),
     ("f16", dict(N=1, Ci=16, Co=24, T=3, Tc=2, H=10, W=18)),
+    # (input channel, tap) pairs spanning several staged weight chunks
+    ("f32", dict(N=1, Ci=3, Co=5, T=7, Tc=0, H=9, W=9, Kt=7, Kh=7, Kw=7, p_base=6)),
+    ("bf16", dict(N=2, Ci=300, Co=70, T=2, Tc=0, H=6, W=21, Kt=1, Kh=1, Kw=1)),
+    ("bf16", dict(N=1, Ci=40, Co=33, T=3, Tc=2, H=5, W=600, Kh=3, Kw=5, p_w=2)),
 ]
 
 
