@@ -17,10 +17,11 @@
 //     the frame was loaded into, so it costs no extra read.
 //
 // GEMM view per output frame: D[co][px] = sum_K Wk[co][K] * Z[K][px], K =
-// (kt, kh, kw, ci).  The matrix-core instruction is v_mfma_f32_16x16x32_bf16:
-// A = weights (16 output channels x 32 input channels), B = activations
-// (32 input channels x 16 pixels), C/D = 16 x 16 fp32, lane l holding rows
-// 4*(l/16) .. +3 of column l % 16.
+// (kt, kh, kw, ci).  The matrix-core instruction is v_mfma_f32_16x16x32_bf16
+// computing D^T[px][co]: A = activations (16 pixels x 32 input channels),
+// B = weights (32 input channels x 16 output channels), C/D = 16 x 16 fp32,
+// lane l holding pixels 4*(l/16) .. +3 of output channel l % 16 -- four
+// consecutive output pixels, stored with one 8-byte write.
 //
 // Data movement
 //   * Weights (A) come pre-packed in fragment order (c3c_weight_repack): one
@@ -134,7 +135,11 @@ __global__ __launch_bounds__(64 * WAVES_CO * WAVES_PX, 1) void conv3d_bf16(Args 
   while (k_lo < a.Kt && o + k_lo * a.dt - a.p_l < 0) ++k_lo;
   int k_hi = a.Kt - 1;
   while (k_hi >= 0 && o + k_hi * a.dt - a.p_l >= a.Z) --k_hi;
-  const int nst = k_hi >= k_lo ? (k_hi - k_lo + 1) * a.chunks : 0;
+  // Stages run channel-chunk outer, tap inner: the workgroups of neighbouring
+  // output frames (which share source frames) then read the same 32-channel
+  // chunk of a frame close together in time, so the re-reads hit in L2.
+  const int ntap = k_hi >= k_lo ? k_hi - k_lo + 1 : 0;
+  const int nst = ntap * a.chunks;
 
   const int cofrag0 = (ct * WAVES_CO + wco) * WCO;
 
@@ -154,8 +159,8 @@ __global__ __launch_bounds__(64 * WAVES_CO * WAVES_PX, 1) void conv3d_bf16(Args 
   // pixel and every channel past Ci is an out-of-range offset and loads as 0.
   auto stage_src = [&](int s, int& f, int& c0, int& k, __amdgpu_buffer_rsrc_t& rs,
                        uint32_t& cs_bytes) {
-    k = k_lo + s / a.chunks;
-    c0 = (s % a.chunks) * BKC;
+    k = k_lo + s % ntap;
+    c0 = (s / ntap) * BKC;
     f = o + k * a.dt - a.p_l;
     const uint16_t* base;
     int64_t cstride;
@@ -168,6 +173,7 @@ __global__ __launch_bounds__(64 * WAVES_CO * WAVES_PX, 1) void conv3d_bf16(Args 
     }
     int64_t bytes = ((a.Ci - 1 - c0) * cstride + a.hw) * 2;
     if (bytes > 0x7fffffff) bytes = 0x7fffffff;
+    if (bytes < 0) bytes = 0;  // a stage past the last one: every load reads 0
     rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(base), 0,
                                            static_cast<int>(bytes), 0x00020000);
     cs_bytes = static_cast<uint32_t>(cstride * 2);
@@ -224,9 +230,10 @@ __global__ __launch_bounds__(64 * WAVES_CO * WAVES_PX, 1) void conv3d_bf16(Args 
   // workgroup also writes its interior rows of a cache frame to cache_out
   auto store_stage = [&](int s, int buf) {
     unsigned char* tile = lds + buf * BUF;
-    const int k = k_lo + s / a.chunks, c0 = (s % a.chunks) * BKC;
+    const int k = k_lo + s % ntap, c0 = (s / ntap) * BKC;
     const int f = o + k * a.dt - a.p_l;
-    const bool cw = a.write_cache && ct == 0 && f >= a.Z - a.L && (k == a.Kt - 1 || o < a.dt);
+    const bool cw = a.write_cache && s < nst && ct == 0 && f >= a.Z - a.L &&
+                    (k == a.Kt - 1 || o < a.dt);
 #pragma unroll
     for (int tt = 0; tt < TPT; ++tt) {
       const int t = tid + tt * NT;
@@ -277,7 +284,7 @@ __global__ __launch_bounds__(64 * WAVES_CO * WAVES_PX, 1) void conv3d_bf16(Args 
       const_cast<u32x4*>(a.wpack), 0, static_cast<int>(a.wpack_bytes), 0x00020000);
   const uint32_t wlane = static_cast<uint32_t>(lane) * 16u;
   auto load_w = [&](int s, int ij, u32x4 (&dst)[WCO]) {
-    const int k = k_lo + s / a.chunks, chunk = s % a.chunks;
+    const int k = k_lo + s % ntap, chunk = s / ntap;
     const uint32_t row = static_cast<uint32_t>((k * 9 + ij) * a.chunks + chunk) *
                          static_cast<uint32_t>(a.cofrags);
 #pragma unroll
@@ -315,10 +322,15 @@ __global__ __launch_bounds__(64 * WAVES_CO * WAVES_PX, 1) void conv3d_bf16(Args 
     }
   };
 
+  // Step order inside a stage: the B fragments of the next (kh, kw) step and
+  // the weights two steps ahead are issued between this step's MFMAs (an
+  // explicit interleave), so the matrix pipe is not left idle while loads
+  // issue.  Loads for a stage past the last one are issued anyway and read
+  // zeros (out-of-range offsets): keeping them unconditional keeps the step
+  // one basic block that the interleave can schedule.
   u32x4 bv[2][NPF];
   for (int s = 0; s < nst; ++s) {
     const unsigned char* tile = lds + (s & 1) * BUF + lane_off;
-    const bool more = s + 1 < nst;
     load_b(tile, 0, bv[0]);
 #pragma unroll
     for (int ij = 0; ij < 9; ++ij) {
@@ -326,47 +338,67 @@ __global__ __launch_bounds__(64 * WAVES_CO * WAVES_PX, 1) void conv3d_bf16(Args 
       // kh offsets overlap, and keeping them live across steps would cost
       // more registers than the LDS bandwidth it saves.
       asm volatile("" ::: "memory");
-      __builtin_amdgcn_sched_barrier(0);  // keep the step order: loads, then MFMAs
+      __builtin_amdgcn_sched_barrier(0);
       if (ij + 1 < 9) load_b(tile, ij + 1, bv[(ij + 1) & 1]);
-      // prefetch the weights two steps ahead (wrapping into the next stage)
-      if (ij + 2 < 9)
-        load_w(s, ij + 2, wr[(ij + 2) % 3]);
-      else if (more)
-        load_w(s + 1, ij + 2 - 9, wr[(ij + 2) % 3]);
-      if (ij == 0 && more) load_stage(s + 1);
+      load_w(s + (ij + 2) / 9, (ij + 2) % 9, wr[(ij + 2) % 3]);
+      if (ij == 0) load_stage(s + 1);
+      // The other LDS buffer was last read in stage s - 1, which every wave
+      // has finished (barrier below), so the next stage's tile is written
+      // here, mid-stage, interleaved with this stage's matrix-core work.
+      if (ij == 5) store_stage(s + 1, (s + 1) & 1);
 #pragma unroll
       for (int pf = 0; pf < NPF; ++pf)
 #pragma unroll
         for (int cf = 0; cf < WCO; ++cf)
           acc[cf][pf] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-              __builtin_bit_cast(bf16x8, wr[ij % 3][cf]), __builtin_bit_cast(bf16x8, bv[ij & 1][pf]),
+              __builtin_bit_cast(bf16x8, bv[ij & 1][pf]), __builtin_bit_cast(bf16x8, wr[ij % 3][cf]),
               acc[cf][pf], 0, 0, 0);
+      // interleave: LDS reads, then global reads, then LDS writes, each
+      // between pairs of MFMAs (masks: 0x008 MFMA, 0x100 DS read,
+      // 0x020 VMEM read, 0x200 DS write)
+      if (ij + 1 < 9)
+        for (int q = 0; q < NPF; ++q) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        }
+      for (int q = 0; q < (ij == 0 ? WCO + TPT * 8 + HPT : WCO); ++q) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+      }
+      if (ij == 5)
+        for (int q = 0; q < TPT * 8 + HPT; ++q) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);
+        }
     }
-    if (more) store_stage(s + 1, (s + 1) & 1);
     __syncthreads();
   }
 
-  // ---- epilogue: bias once, round to bf16, NCTHW store
+  // ---- epilogue: bias once, round to bf16, NCTHW store.  With the
+  // activations as the A operand, lane l holds output channel l % 16 for the
+  // four consecutive pixels 4 * (l / 16) .. + 3 of each fragment: one 8-byte
+  // store per fragment.
   const int64_t plane = static_cast<int64_t>(a.To) * a.hw;
   uint16_t* ybase = a.y + (static_cast<int64_t>(n) * a.Co) * plane + static_cast<int64_t>(o) * a.hw;
 #pragma unroll
   for (int cf = 0; cf < WCO; ++cf) {
-    const int co0 = (cofrag0 + cf) * 16 + 4 * (lane >> 4);
-    float bb[4];
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int co = co0 + r;
-      bb[r] = (a.has_bias && co < a.Co) ? __uint_as_float(static_cast<uint32_t>(a.bias[co]) << 16) : 0.f;
-    }
+    const int co = (cofrag0 + cf) * 16 + (lane & 15);
+    const float bb = (a.has_bias && co < a.Co) ? __uint_as_float(static_cast<uint32_t>(a.bias[co]) << 16) : 0.f;
 #pragma unroll
     for (int pf = 0; pf < NPF; ++pf) {
-      const int h = h0 + wpx * WR + pf / WCF, w = w0 + (pf % WCF) * 16 + (lane & 15);
-      if (h >= a.H || w >= a.W) continue;
+      const int h = h0 + wpx * WR + pf / WCF, w = w0 + (pf % WCF) * 16 + 4 * (lane >> 4);
+      if (co >= a.Co || h >= a.H || w >= a.W) continue;
+      uint16_t v[4];
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int co = co0 + r;
-        if (co < a.Co)
-          ybase[co * plane + static_cast<int64_t>(h) * a.W + w] = f32_to_bf16(acc[cf][pf][r] + bb[r]);
+      for (int r = 0; r < 4; ++r) v[r] = f32_to_bf16(acc[cf][pf][r] + bb);
+      uint16_t* dst = ybase + co * plane + static_cast<int64_t>(h) * a.W + w;
+      if (ALIGNED && w + 4 <= a.W) {
+        *reinterpret_cast<uint2*>(dst) = make_uint2(v[0] | (static_cast<uint32_t>(v[1]) << 16),
+                                                   v[2] | (static_cast<uint32_t>(v[3]) << 16));
+      } else {
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          if (w + r < a.W) dst[r] = v[r];
       }
     }
   }
