@@ -50,7 +50,7 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int BKC = 32;   // input channels per stage = K of one matrix-core step
-constexpr int PIXB = 80;  // LDS bytes per staged pixel: 32 ch * 2 B + 16 B pad
+constexpr int PIXB = 96;  // LDS bytes per staged pixel: 32 ch * 2 B + 32 B pad (bank-conflict-free B reads)
 
 struct Args {
   const uint16_t* x;
@@ -180,11 +180,15 @@ __global__ __launch_bounds__(64 * WAVES_CO * WAVES_PX, 1) void conv3d_bf16(Args 
   };
   constexpr uint32_t OOB = 0x80000000u;  // beyond every resource's size
 
-  auto load_stage = [&](int s) {
+  // part p of stage s's loads: channel rows 2p, 2p + 1 of every task for
+  // p = 0..3, the halo columns for p = 4 (spread over five steps so that no
+  // burst of loads sits in front of the weight loads that follow it)
+  auto load_stage = [&](int s, int part) {
     int f, c0, k;
     __amdgpu_buffer_rsrc_t rs;
     uint32_t cs;
     stage_src(s, f, c0, k, rs, cs);
+    if (part < 4)
 #pragma unroll
     for (int tt = 0; tt < TPT; ++tt) {
       const int t = tid + tt * NT;
@@ -197,6 +201,7 @@ __global__ __launch_bounds__(64 * WAVES_CO * WAVES_PX, 1) void conv3d_bf16(Args 
                            static_cast<uint32_t>(gh * a.W + w) * 2u;
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
+        if (j / 2 != part) continue;
         const bool chok = rowok & (c0 + 8 * g + j < a.Ci);
         if (ALIGNED) {
           const uint32_t oj = (chok & (w < a.W)) ? off + j * cs : OOB;
@@ -215,6 +220,7 @@ __global__ __launch_bounds__(64 * WAVES_CO * WAVES_PX, 1) void conv3d_bf16(Args 
         }
       }
     }
+    if (part == 4)
 #pragma unroll
     for (int hh = 0; hh < HPT; ++hh) {
       const int e = tid + hh * NT;
@@ -277,21 +283,24 @@ __global__ __launch_bounds__(64 * WAVES_CO * WAVES_PX, 1) void conv3d_bf16(Args 
   };
 
   // Weights of step (stage s, spatial offset ij) for this wave's fragments.
-  // A fragment index past the last one is clamped to it: it only feeds
-  // accumulator rows of output channels >= Co, which are never stored.
+  // The fragment index is clamped to the last packed fragment: past Co it
+  // only feeds accumulator rows that are never stored, and for the stage
+  // after the last one (prefetched, never used) it keeps the address inside
+  // the packed weights.
   u32x4 wr[3][WCO];
   const __amdgpu_buffer_rsrc_t wrs = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<u32x4*>(a.wpack), 0, static_cast<int>(a.wpack_bytes), 0x00020000);
   const uint32_t wlane = static_cast<uint32_t>(lane) * 16u;
+  const uint32_t nfrag = a.wpack_bytes / 1024u;
   auto load_w = [&](int s, int ij, u32x4 (&dst)[WCO]) {
     const int k = k_lo + s % ntap, chunk = s / ntap;
     const uint32_t row = static_cast<uint32_t>((k * 9 + ij) * a.chunks + chunk) *
                          static_cast<uint32_t>(a.cofrags);
 #pragma unroll
     for (int cf = 0; cf < WCO; ++cf) {
-      const int cfr = min(cofrag0 + cf, a.cofrags - 1);
+      const uint32_t frag = min(row + static_cast<uint32_t>(min(cofrag0 + cf, a.cofrags - 1)), nfrag - 1);
       dst[cf] = __builtin_bit_cast(
-          u32x4, __builtin_amdgcn_raw_buffer_load_b128(wrs, wlane, (row + cfr) * 1024u, 0));
+          u32x4, __builtin_amdgcn_raw_buffer_load_b128(wrs, wlane, frag * 1024u, 0));
     }
   };
 
@@ -307,7 +316,7 @@ __global__ __launch_bounds__(64 * WAVES_CO * WAVES_PX, 1) void conv3d_bf16(Args 
   if (nst > 0) {
     load_w(0, 0, wr[0]);
     load_w(0, 1, wr[1]);
-    load_stage(0);
+    for (int part = 0; part < 5; ++part) load_stage(0, part);
     store_stage(0, 0);
     __syncthreads();
   }
@@ -341,11 +350,11 @@ __global__ __launch_bounds__(64 * WAVES_CO * WAVES_PX, 1) void conv3d_bf16(Args 
       __builtin_amdgcn_sched_barrier(0);
       if (ij + 1 < 9) load_b(tile, ij + 1, bv[(ij + 1) & 1]);
       load_w(s + (ij + 2) / 9, (ij + 2) % 9, wr[(ij + 2) % 3]);
-      if (ij == 0) load_stage(s + 1);
+      if (ij < 5) load_stage(s + 1, ij);
       // The other LDS buffer was last read in stage s - 1, which every wave
       // has finished (barrier below), so the next stage's tile is written
       // here, mid-stage, interleaved with this stage's matrix-core work.
-      if (ij == 5) store_stage(s + 1, (s + 1) & 1);
+      if (ij == 7) store_stage(s + 1, (s + 1) & 1);
 #pragma unroll
       for (int pf = 0; pf < NPF; ++pf)
 #pragma unroll
@@ -361,11 +370,11 @@ __global__ __launch_bounds__(64 * WAVES_CO * WAVES_PX, 1) void conv3d_bf16(Args 
           __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
           __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
         }
-      for (int q = 0; q < (ij == 0 ? WCO + TPT * 8 + HPT : WCO); ++q) {
+      for (int q = 0; q < WCO + (ij < 4 ? TPT * 2 : ij == 4 ? HPT : 0); ++q) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
         __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
       }
-      if (ij == 5)
+      if (ij == 7)
         for (int q = 0; q < TPT * 8 + HPT; ++q) {
           __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
           __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);
