@@ -44,6 +44,9 @@ def main():
     ap.add_argument("--workload", default="stack_720p")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="run only a plain 512 MiB device copy (the reference kernel "
+                         "for scaling FETCH_SIZE / WRITE_SIZE counters) and exit")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
@@ -52,6 +55,10 @@ def main():
 
     import torch
     from paper_2609_31938_amd import c3c, inputs
+
+    if args.copy_calibration:
+        copy_calibration()
+        return
 
     wl = inputs.WORKLOADS[args.workload]
     dtype = wl["dtype"]
@@ -148,8 +155,9 @@ def main():
     achieved = dom["gflop"] * 1e9 / (dom_mean_ms * 1e-3) / 1e12
     peak = PEAK_BF16_TFLOPS if dtype == "bf16" else PEAK_F32_TFLOPS
     roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak,
-                "unit": "TFLOP/s", "frac": round(achieved / peak, 4), "traffic": None,
-                "kernel": f"fast conv, layer {dom['layer']}"}
+                "unit": "TFLOP/s", "frac": round(achieved / peak, 4),
+                "traffic": measured_traffic(dom["layer"]),
+                "kernel": f"conv3d_bf16 (fast route), layer {dom['layer']}"}
 
     out = {
         "metric": METRIC,
@@ -177,6 +185,47 @@ def main():
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(layers[dom_i], dtype, args.cpu_seconds)
     print(json.dumps(out), flush=True)
+
+
+def copy_calibration():
+    """A plain device-to-device copy of 512 MiB, three times: the kernel of
+    known traffic against which the FETCH_SIZE / WRITE_SIZE counters are
+    scaled."""
+    import torch
+    n = 256 * 1024 * 1024
+    a = torch.ones(n, dtype=torch.bfloat16, device="cuda")
+    b = torch.empty_like(a)
+    for _ in range(3):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes_each_way": a.numel() * 2, "launches": 3}),
+          flush=True)
+
+
+def kernel_source_sha256():
+    import hashlib
+    src = os.path.join(ROOT, "paper_2609_31938_amd", "csrc", "conv_bf16.hip")
+    return hashlib.sha256(open(src, "rb").read()).hexdigest()
+
+
+def measured_traffic(layer):
+    """HBM bytes per launch of the dominant kernel, from the committed
+    rocprofv3 counter summary, or None when that summary was taken on a
+    different kernel source (or does not exist)."""
+    path = os.path.join(ROOT, "profiles", f"conv3d_bf16_{layer}_traffic.md")
+    if not os.path.exists(path):
+        return None
+    fields = {}
+    for line in open(path):
+        if line.startswith("- ") and ": " in line:
+            k, v = line[2:].split(": ", 1)
+            fields[k.strip("` ")] = v.strip().strip("`")
+    if fields.get("kernel_source_sha256") != kernel_source_sha256():
+        return None
+    try:
+        return float(fields["traffic_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
 
 
 def cpu_baseline(L_, dtype, budget_s):
