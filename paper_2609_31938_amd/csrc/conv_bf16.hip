@@ -24,22 +24,27 @@
 // consecutive output pixels, stored with one 8-byte write.
 //
 // Data movement
-//   * Weights (A) come pre-packed in fragment order (c3c_weight_repack): one
-//     16-byte load per lane per fragment, straight from L2 into registers,
-//     two kernel taps ahead of their use (a 3-slot register ring).
-//   * Activations (B) are staged per (tap, 32-channel chunk) as a halo tile
-//     [BH+2][BW+2][32 ch] in LDS, channel-innermost with an 80-byte pixel
-//     pitch, so that each lane reads its 8 K-consecutive channels with one
-//     ds_read_b128 and the nine (kh, kw) offsets of the 3x3 kernel are nine
-//     immediate address offsets into the same tile.  Global reads are
-//     16-byte row segments of the NCTHW planes; an 8x8 register transpose
-//     (v_perm) turns 8 channel rows x 8 pixels into 8 pixel records.  The
-//     tile is double-buffered: the next stage's global loads are in flight
-//     while the current stage computes.
+//   * Weights (B operand) come pre-packed in fragment order
+//     (c3c_weight_repack): one 16-byte load per lane per fragment, straight
+//     from L2 into registers, two (kh, kw) steps ahead of their use (a
+//     3-slot register ring).
+//   * Activations (A operand) are staged per (tap, 32-channel chunk) as a
+//     halo tile [BH+2][BW+2][32 ch] in LDS, channel-innermost with a 96-byte
+//     pixel pitch (bank-conflict-free for the operand reads), so that each
+//     lane reads its 8 K-consecutive channels with one ds_read_b128 and the
+//     nine (kh, kw) offsets of the 3x3 kernel are nine immediate address
+//     offsets into the same tile.  Global reads are 16-byte row segments of
+//     the NCTHW planes; an 8x8 register transpose (v_perm) turns 8 channel
+//     rows x 8 pixels into 8 pixel records.  Tiles rotate through NBUF LDS
+//     buffers: the next stage's global loads are in flight while the current
+//     stage computes, and each operand fragment is re-read from LDS right
+//     after its last use (one register set, no double buffer).
 //   * Workgroups are numbered so that each of the 8 XCDs (which take
 //     workgroups round-robin) runs a contiguous range of tiles -- consecutive
 //     output frames of the same spatial tile, then neighbouring tiles -- so
 //     the frames shared by neighbouring taps and the halos are L2 hits.
+#include <atomic>
+
 #include "c3c_internal.h"
 
 namespace c3c {
@@ -91,8 +96,11 @@ __device__ inline void transpose8x8(const u32x4 (&v)[8], u32x4 (&o)[8]) {
 
 // Workgroup tile: BCO = 16*WCO*WAVES_CO output channels x BH = WR*WAVES_PX
 // rows x BW = 16*WCF columns of one output frame.  Wave (wco, wpx) owns WCO
-// x (WR*WCF) accumulator fragments of 16 x 16.
-template <int WCO, int WR, int WCF, int WAVES_CO, int WAVES_PX, bool ALIGNED>
+// x (WR*WCF) accumulator fragments of 16 x 16.  NBUF (2 or 3) LDS tile
+// buffers: with 3, the barrier that publishes the next stage's tile sits
+// inside the current stage, so the first operand reads of the next stage
+// overlap the current stage's last matrix-core step.
+template <int WCO, int WR, int WCF, int WAVES_CO, int WAVES_PX, int NBUF, bool ALIGNED>
 __global__ __launch_bounds__(64 * WAVES_CO * WAVES_PX, 1) void conv3d_bf16(Args a) {
   constexpr int NT = 64 * WAVES_CO * WAVES_PX;
   constexpr int BH = WR * WAVES_PX, BW = 16 * WCF;
@@ -106,7 +114,9 @@ __global__ __launch_bounds__(64 * WAVES_CO * WAVES_PX, 1) void conv3d_bf16(Args 
   constexpr int BUF = TH * TW * PIXB;
   constexpr int NPF = WR * WCF;                 // pixel fragments per wave
   static_assert(TW % 8 == 2, "the staging lane order assumes TW = 2 mod 8");
-  __shared__ __align__(16) unsigned char lds[2 * BUF];
+  static_assert(NBUF == 2 || NBUF == 3, "two or three tile buffers");
+  static_assert(NBUF * BUF <= 160 * 1024, "LDS tile buffers exceed 160 KiB");
+  __shared__ __align__(16) unsigned char lds[NBUF * BUF];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
@@ -140,80 +150,106 @@ __global__ __launch_bounds__(64 * WAVES_CO * WAVES_PX, 1) void conv3d_bf16(Args 
   // chunk of a frame close together in time, so the re-reads hit in L2.
   const int ntap = k_hi >= k_lo ? k_hi - k_lo + 1 : 0;
   const int nst = ntap * a.chunks;
+  constexpr uint32_t OOB = 0x80000000u;  // beyond every resource's size
 
-  const int cofrag0 = (ct * WAVES_CO + wco) * WCO;
-
-  // ---- staging task decode: lane bits (g0, r0, r1, g1) first so that the
-  // 8 lanes of one LDS write cycle hit 8 distinct 16-byte bank groups
-  auto task = [&](int t, int& g, int& rr, int& q) {
-    g = (t & 1) | (((t >> 3) & 1) << 1);
-    rr = ((t >> 1) & 3) | (((t >> 4) % (TH4 / 4)) << 2);
-    q = (t >> 4) / (TH4 / 4);
+  // One stage = (active tap k, 32-channel chunk c0).  Its activations are read
+  // through a buffer resource that starts at channel c0 of source frame f and
+  // ends after the last real channel, so every padding pixel and every
+  // channel past Ci is an out-of-range offset and loads as 0; a chunk past
+  // the last one has an empty resource.  wbase is the byte offset of the
+  // stage's (kh, kw) = (0, 0) weight row in the packed weights.
+  struct Stage {
+    __amdgpu_buffer_rsrc_t rs;
+    uint32_t cs;     // bytes between channel planes of the source
+    uint32_t wbase;
+    int k, c0, f;
   };
+  auto stage_at = [&](int ki, int chunk) {
+    Stage st;
+    st.k = k_lo + ki;
+    st.c0 = chunk * BKC;
+    st.f = o + st.k * a.dt - a.p_l;
+    const uint16_t* base;
+    int64_t cstride;
+    if (st.f < a.Tc) {
+      cstride = static_cast<int64_t>(a.Tc) * a.hw;
+      base = a.cache + (static_cast<int64_t>(n) * a.Ci + st.c0) * cstride + st.f * a.hw;
+    } else {
+      cstride = static_cast<int64_t>(a.T) * a.hw;
+      base = a.x + (static_cast<int64_t>(n) * a.Ci + st.c0) * cstride + (st.f - a.Tc) * a.hw;
+    }
+    int64_t bytes = ((a.Ci - 1 - st.c0) * cstride + a.hw) * 2;
+    if (bytes > 0x7fffffff) bytes = 0x7fffffff;
+    if (bytes < 0) bytes = 0;
+    st.rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(base), 0,
+                                              static_cast<int>(bytes), 0x00020000);
+    st.cs = static_cast<uint32_t>(cstride * 2);
+    st.wbase = static_cast<uint32_t>((st.k * 9 * a.chunks + chunk) * a.cofrags) * 1024u;
+    return st;
+  };
+
+  // ---- per-thread staging constants.  Task decode: lane bits (g0, r0, r1,
+  // g1) first so that the 8 lanes of one LDS write cycle hit 8 distinct
+  // 16-byte bank groups.  A task is 8 channels (8g ..) x 8 pixels of one
+  // halo-tile row.
+  uint32_t t_g8[TPT], t_pix[TPT], t_lds[TPT];
+  bool t_st[TPT], t_ok[TPT], t_in[TPT];
+  int t_w[TPT];
+#pragma unroll
+  for (int tt = 0; tt < TPT; ++tt) {
+    const int t = tid + tt * NT;
+    const int g = (t & 1) | (((t >> 3) & 1) << 1);
+    const int rr = ((t >> 1) & 3) | (((t >> 4) % (TH4 / 4)) << 2);
+    const int q = (t >> 4) / (TH4 / 4);
+    const int gh = h0 - 1 + rr, w = w0 + 8 * q;
+    t_st[tt] = (t < NTASK) & (rr < TH);
+    // bitwise & (not &&): validity must become selects, not branches
+    t_ok[tt] = t_st[tt] & (gh >= 0) & (gh < a.H) & (w < a.W);
+    t_g8[tt] = static_cast<uint32_t>(8 * g);
+    t_pix[tt] = static_cast<uint32_t>(gh * a.W + w) * 2u;
+    t_lds[tt] = static_cast<uint32_t>((rr * TW + 1 + 8 * q) * PIXB + 16 * g);
+    t_w[tt] = w;
+    // interior rows of the tile (the cache write covers only those)
+    t_in[tt] = t_st[tt] & (rr >= 1) & (rr <= BH) & (gh < a.H) & (w < a.W);
+  }
+  uint32_t h_ch[HPT], h_pix[HPT], h_lds[HPT];
+  bool h_ok[HPT], h_in[HPT];
+#pragma unroll
+  for (int hh = 0; hh < HPT; ++hh) {
+    const int e = tid + hh * NT;
+    const int ch = e % BKC, side = (e / BKC) % 2, rr = e / (2 * BKC);
+    const int gh = h0 - 1 + rr, gw = side ? w0 + BW : w0 - 1;
+    h_in[hh] = e < NHALO;
+    h_ok[hh] = h_in[hh] & (gh >= 0) & (gh < a.H) & (gw >= 0) & (gw < a.W);
+    h_ch[hh] = static_cast<uint32_t>(ch);
+    h_pix[hh] = static_cast<uint32_t>(gh * a.W + gw) * 2u;
+    h_lds[hh] = static_cast<uint32_t>((rr * TW + (side ? TW - 1 : 0)) * PIXB + 2 * ch);
+  }
 
   u32x4 sv[TPT][8];
   uint16_t hv[HPT];
 
-  // Stage s reads the 32-channel chunk c0 of source frame f through a buffer
-  // resource that ends after the last real channel, so that every padding
-  // pixel and every channel past Ci is an out-of-range offset and loads as 0.
-  auto stage_src = [&](int s, int& f, int& c0, int& k, __amdgpu_buffer_rsrc_t& rs,
-                       uint32_t& cs_bytes) {
-    k = k_lo + s % ntap;
-    c0 = (s / ntap) * BKC;
-    f = o + k * a.dt - a.p_l;
-    const uint16_t* base;
-    int64_t cstride;
-    if (f < a.Tc) {
-      cstride = static_cast<int64_t>(a.Tc) * a.hw;
-      base = a.cache + (static_cast<int64_t>(n) * a.Ci + c0) * cstride + f * a.hw;
-    } else {
-      cstride = static_cast<int64_t>(a.T) * a.hw;
-      base = a.x + (static_cast<int64_t>(n) * a.Ci + c0) * cstride + (f - a.Tc) * a.hw;
-    }
-    int64_t bytes = ((a.Ci - 1 - c0) * cstride + a.hw) * 2;
-    if (bytes > 0x7fffffff) bytes = 0x7fffffff;
-    if (bytes < 0) bytes = 0;  // a stage past the last one: every load reads 0
-    rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(base), 0,
-                                           static_cast<int>(bytes), 0x00020000);
-    cs_bytes = static_cast<uint32_t>(cstride * 2);
-  };
-  constexpr uint32_t OOB = 0x80000000u;  // beyond every resource's size
-
-  // part p of stage s's loads: channel rows 2p, 2p + 1 of every task for
+  // part p of a stage's loads: channel rows 2p, 2p + 1 of every task for
   // p = 0..3, the halo columns for p = 4 (spread over five steps so that no
   // burst of loads sits in front of the weight loads that follow it)
-  auto load_stage = [&](int s, int part) {
-    int f, c0, k;
-    __amdgpu_buffer_rsrc_t rs;
-    uint32_t cs;
-    stage_src(s, f, c0, k, rs, cs);
+  auto load_stage = [&](const Stage& st, int part) {
     if (part < 4)
 #pragma unroll
     for (int tt = 0; tt < TPT; ++tt) {
-      const int t = tid + tt * NT;
-      int g, rr, q;
-      task(t, g, rr, q);
-      const int gh = h0 - 1 + rr, w = w0 + 8 * q;
-      // bitwise & (not &&): validity must become selects, not branches
-      const bool rowok = (t < NTASK) & (rr < TH) & (gh >= 0) & (gh < a.H);
-      const uint32_t off = static_cast<uint32_t>(8 * g) * cs +
-                           static_cast<uint32_t>(gh * a.W + w) * 2u;
+      const uint32_t off = t_ok[tt] ? t_g8[tt] * st.cs + t_pix[tt] : OOB;
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        if (j / 2 != part) continue;
-        const bool chok = rowok & (c0 + 8 * g + j < a.Ci);
+      for (int j = 2 * part; j < 2 * part + 2; ++j) {
         if (ALIGNED) {
-          const uint32_t oj = (chok & (w < a.W)) ? off + j * cs : OOB;
-          sv[tt][j] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, oj, 0, 0));
+          sv[tt][j] = __builtin_bit_cast(
+              u32x4, __builtin_amdgcn_raw_buffer_load_b128(st.rs, off + j * st.cs, 0, 0));
         } else {
           uint32_t wd[4];
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
-            const uint32_t o0 = (chok & (w + 2 * e < a.W)) ? off + j * cs + 4u * e : OOB;
-            const uint32_t o1 = (chok & (w + 2 * e + 1 < a.W)) ? off + j * cs + 4u * e + 2u : OOB;
-            const uint32_t lo = __builtin_amdgcn_raw_buffer_load_b16(rs, o0, 0, 0);
-            const uint32_t hi = __builtin_amdgcn_raw_buffer_load_b16(rs, o1, 0, 0);
+            const uint32_t o0 = (t_w[tt] + 2 * e < a.W) ? off + j * st.cs + 4u * e : OOB;
+            const uint32_t o1 = (t_w[tt] + 2 * e + 1 < a.W) ? off + j * st.cs + 4u * e + 2u : OOB;
+            const uint32_t lo = __builtin_amdgcn_raw_buffer_load_b16(st.rs, o0, 0, 0);
+            const uint32_t hi = __builtin_amdgcn_raw_buffer_load_b16(st.rs, o1, 0, 0);
             wd[e] = (lo & 0xffffu) | (hi << 16);
           }
           sv[tt][j] = u32x4{wd[0], wd[1], wd[2], wd[3]};
@@ -222,86 +258,81 @@ __global__ __launch_bounds__(64 * WAVES_CO * WAVES_PX, 1) void conv3d_bf16(Args 
     }
     if (part == 4)
 #pragma unroll
-    for (int hh = 0; hh < HPT; ++hh) {
-      const int e = tid + hh * NT;
-      const int ch = e % BKC, side = (e / BKC) % 2, rr = e / (2 * BKC);
-      const int gh = h0 - 1 + rr, gw = side ? w0 + BW : w0 - 1;
-      const bool ok = (e < NHALO) & (gh >= 0) & (gh < a.H) & (gw >= 0) & (gw < a.W) & (c0 + ch < a.Ci);
-      const uint32_t oh = ok ? static_cast<uint32_t>(ch) * cs + static_cast<uint32_t>(gh * a.W + gw) * 2u : OOB;
-      hv[hh] = __builtin_amdgcn_raw_buffer_load_b16(rs, oh, 0, 0);
-    }
+    for (int hh = 0; hh < HPT; ++hh)
+      hv[hh] = __builtin_amdgcn_raw_buffer_load_b16(
+          st.rs, h_ok[hh] ? h_ch[hh] * st.cs + h_pix[hh] : OOB, 0, 0);
   };
 
   // transpose the staged registers into LDS buffer `buf`; the designated
-  // workgroup also writes its interior rows of a cache frame to cache_out
-  auto store_stage = [&](int s, int buf) {
+  // workgroup also writes its interior rows of a cache frame to cache_out,
+  // through a buffer resource that ends after the last real channel (stores
+  // at out-of-range offsets are dropped)
+  auto store_stage = [&](const Stage& st, bool real, int buf) {
     unsigned char* tile = lds + buf * BUF;
-    const int k = k_lo + s % ntap, c0 = (s / ntap) * BKC;
-    const int f = o + k * a.dt - a.p_l;
-    const bool cw = a.write_cache && s < nst && ct == 0 && f >= a.Z - a.L &&
-                    (k == a.Kt - 1 || o < a.dt);
+    const bool cw = a.write_cache && real && ct == 0 && st.f >= a.Z - a.L &&
+                    (st.k == a.Kt - 1 || o < a.dt);
+    __amdgpu_buffer_rsrc_t crs;
+    uint32_t ccs = 0;
+    if (cw) {
+      const int64_t cstride = static_cast<int64_t>(a.L) * a.hw;
+      uint16_t* cbase = a.cache_out + (static_cast<int64_t>(n) * a.Ci + st.c0) * cstride +
+                        static_cast<int64_t>(st.f - (a.Z - a.L)) * a.hw;
+      int64_t bytes = ((a.Ci - 1 - st.c0) * cstride + a.hw) * 2;
+      if (bytes > 0x7fffffff) bytes = 0x7fffffff;
+      crs = __builtin_amdgcn_make_buffer_rsrc(cbase, 0, static_cast<int>(bytes), 0x00020000);
+      ccs = static_cast<uint32_t>(cstride * 2);
+    }
 #pragma unroll
     for (int tt = 0; tt < TPT; ++tt) {
-      const int t = tid + tt * NT;
-      int g, rr, q;
-      task(t, g, rr, q);
-      if (t < NTASK && rr < TH) {
+      if (t_st[tt]) {
         u32x4 pr[8];
         transpose8x8(sv[tt], pr);
 #pragma unroll
         for (int p = 0; p < 8; ++p)
-          *reinterpret_cast<u32x4*>(tile + (rr * TW + 1 + 8 * q + p) * PIXB + 16 * g) = pr[p];
-        const int gh = h0 - 1 + rr, w = w0 + 8 * q;
-        if (cw && rr >= 1 && rr <= BH && gh < a.H && w < a.W) {
-          const int fo = f - (a.Z - a.L);
+          *reinterpret_cast<u32x4*>(tile + t_lds[tt] + p * PIXB) = pr[p];
+      }
+      if (cw) {
+        const uint32_t off = t_in[tt] ? t_g8[tt] * ccs + t_pix[tt] : OOB;
 #pragma unroll
-          for (int j = 0; j < 8; ++j) {
-            const int c = c0 + 8 * g + j;
-            if (c >= a.Ci) break;
-            uint16_t* dst = a.cache_out +
-                            ((static_cast<int64_t>(n) * a.Ci + c) * a.L + fo) * a.hw +
-                            static_cast<int64_t>(gh) * a.W + w;
-            if (ALIGNED) {
-              *reinterpret_cast<u32x4*>(dst) = sv[tt][j];
-            } else {
+        for (int j = 0; j < 8; ++j) {
+          if (ALIGNED) {
+            __builtin_amdgcn_raw_buffer_store_b128(sv[tt][j], crs, off + j * ccs, 0, 0);
+          } else {
 #pragma unroll
-              for (int e = 0; e < 8; ++e)
-                if (w + e < a.W) dst[e] = static_cast<uint16_t>(sv[tt][j][e >> 1] >> (16 * (e & 1)));
-            }
+            for (int e = 0; e < 8; ++e)
+              __builtin_amdgcn_raw_buffer_store_b16(
+                  static_cast<uint16_t>(sv[tt][j][e >> 1] >> (16 * (e & 1))), crs,
+                  t_w[tt] + e < a.W ? off + j * ccs + 2u * e : OOB, 0, 0);
           }
         }
       }
     }
 #pragma unroll
-    for (int hh = 0; hh < HPT; ++hh) {
-      const int e = tid + hh * NT;
-      if (e < NHALO) {
-        const int ch = e % BKC, side = (e / BKC) % 2, rr = e / (2 * BKC);
-        *reinterpret_cast<uint16_t*>(tile + (rr * TW + (side ? TW - 1 : 0)) * PIXB + 2 * ch) = hv[hh];
-      }
-    }
+    for (int hh = 0; hh < HPT; ++hh)
+      if (h_in[hh]) *reinterpret_cast<uint16_t*>(tile + h_lds[hh]) = hv[hh];
   };
 
-  // Weights of step (stage s, spatial offset ij) for this wave's fragments.
-  // The fragment index is clamped to the last packed fragment: past Co it
-  // only feeds accumulator rows that are never stored, and for the stage
-  // after the last one (prefetched, never used) it keeps the address inside
-  // the packed weights.
+  // Weights of (kh, kw) step ij of a stage for this wave's fragments: one
+  // 16-byte load per lane per fragment at wbase + ij * (bytes per (kh, kw)
+  // row) + the fragment's offset.  Output-channel fragments past Co are
+  // clamped to the last one: they only feed accumulator rows that are never
+  // stored.  The prefetch for the stage after the last one reads row
+  // (k_lo, chunk = chunks), which is still inside the packed weights.
   u32x4 wr[3][WCO];
   const __amdgpu_buffer_rsrc_t wrs = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<u32x4*>(a.wpack), 0, static_cast<int>(a.wpack_bytes), 0x00020000);
-  const uint32_t wlane = static_cast<uint32_t>(lane) * 16u;
-  const uint32_t nfrag = a.wpack_bytes / 1024u;
-  auto load_w = [&](int s, int ij, u32x4 (&dst)[WCO]) {
-    const int k = k_lo + s % ntap, chunk = s / ntap;
-    const uint32_t row = static_cast<uint32_t>((k * 9 + ij) * a.chunks + chunk) *
-                         static_cast<uint32_t>(a.cofrags);
+  const uint32_t wrow = static_cast<uint32_t>(a.chunks * a.cofrags) * 1024u;
+  const int cofrag0 = (ct * WAVES_CO + wco) * WCO;
+  uint32_t wv[WCO];
 #pragma unroll
-    for (int cf = 0; cf < WCO; ++cf) {
-      const uint32_t frag = min(row + static_cast<uint32_t>(min(cofrag0 + cf, a.cofrags - 1)), nfrag - 1);
-      dst[cf] = __builtin_bit_cast(
-          u32x4, __builtin_amdgcn_raw_buffer_load_b128(wrs, wlane, frag * 1024u, 0));
-    }
+  for (int cf = 0; cf < WCO; ++cf)
+    wv[cf] = static_cast<uint32_t>(lane) * 16u +
+             static_cast<uint32_t>(min(cofrag0 + cf, a.cofrags - 1)) * 1024u;
+  auto load_w = [&](uint32_t wbase, int ij, u32x4 (&dst)[WCO]) {
+    const uint32_t so = wbase + static_cast<uint32_t>(ij) * wrow;
+#pragma unroll
+    for (int cf = 0; cf < WCO; ++cf)
+      dst[cf] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(wrs, wv[cf], so, 0));
   };
 
   f32x4 acc[WCO][NPF];
@@ -310,77 +341,99 @@ __global__ __launch_bounds__(64 * WAVES_CO * WAVES_PX, 1) void conv3d_bf16(Args 
 #pragma unroll
     for (int j = 0; j < NPF; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  // per-lane LDS offset of this wave's B operand (pixel l % 16, channel group l / 16)
+  // per-lane LDS offset of this wave's activation operand (pixel l % 16,
+  // channel group l / 16)
   const int lane_off = (wpx * WR * TW + (lane & 15)) * PIXB + (lane >> 4) * 16;
 
-  if (nst > 0) {
-    load_w(0, 0, wr[0]);
-    load_w(0, 1, wr[1]);
-    for (int part = 0; part < 5; ++part) load_stage(0, part);
-    store_stage(0, 0);
-    __syncthreads();
-  }
-
-  // B fragments of one (kh, kw) step for this wave
-  auto load_b = [&](const unsigned char* tile, int ij, u32x4 (&dst)[NPF]) {
-    const int ki = ij / 3, kj = ij % 3;
-#pragma unroll
-    for (int pf = 0; pf < NPF; ++pf) {
-      const int rp = pf / WCF, cfb = pf % WCF;
-      dst[pf] = *reinterpret_cast<const u32x4*>(tile + ((rp + ki) * TW + cfb * 16 + kj) * PIXB);
-    }
+  // activation fragment pf of (kh, kw) step ij
+  auto read_a = [&](const unsigned char* tile, int ij, int pf) {
+    const int ki = ij / 3, kj = ij % 3, rp = pf / WCF, cfb = pf % WCF;
+    return *reinterpret_cast<const u32x4*>(tile + ((rp + ki) * TW + cfb * 16 + kj) * PIXB);
   };
 
-  // Step order inside a stage: the B fragments of the next (kh, kw) step and
-  // the weights two steps ahead are issued between this step's MFMAs (an
-  // explicit interleave), so the matrix pipe is not left idle while loads
-  // issue.  Loads for a stage past the last one are issued anyway and read
-  // zeros (out-of-range offsets): keeping them unconditional keeps the step
-  // one basic block that the interleave can schedule.
-  u32x4 bv[2][NPF];
+  u32x4 av[NPF];
+  // (tap index, chunk) of the next stage, advanced incrementally
+  int nk = 0, nc = 0;
+  auto advance = [&]() {
+    if (++nk == ntap) {
+      nk = 0;
+      ++nc;
+    }
+  };
+  Stage cst = stage_at(0, 0);
+  if (nst > 0) {
+    load_w(cst.wbase, 0, wr[0]);
+    load_w(cst.wbase, 1, wr[1]);
+    for (int part = 0; part < 5; ++part) load_stage(cst, part);
+    store_stage(cst, true, 0);
+    __syncthreads();
+#pragma unroll
+    for (int pf = 0; pf < NPF; ++pf) av[pf] = read_a(lds + lane_off, 0, pf);
+  }
+
+  // Step (s, ij): the weights two steps ahead and part ij of the next
+  // stage's activation loads are issued first; fragment pf's matrix-core
+  // products are followed by the re-read of that fragment for the next step
+  // (or, with three buffers, for step 0 of the next stage, whose tile was
+  // published by the barrier at the end of step 7).  Loads for a stage past
+  // the last one are issued anyway and read zeros (an empty resource):
+  // keeping them unconditional keeps the step one basic block that the
+  // explicit interleave can schedule.
+  int cur = 0;
   for (int s = 0; s < nst; ++s) {
-    const unsigned char* tile = lds + (s & 1) * BUF + lane_off;
-    load_b(tile, 0, bv[0]);
+    advance();
+    const Stage nst_ = stage_at(nk, nc);
+    const int nxt = cur + 1 == NBUF ? 0 : cur + 1;
+    const unsigned char* tile = lds + cur * BUF + lane_off;
+    const unsigned char* ntile = lds + nxt * BUF + lane_off;
 #pragma unroll
     for (int ij = 0; ij < 9; ++ij) {
-      // One fresh LDS read per fragment and step: the rows of neighbouring
-      // kh offsets overlap, and keeping them live across steps would cost
-      // more registers than the LDS bandwidth it saves.
+      // keep every LDS read inside its own step: re-reading is cheaper in
+      // registers than keeping overlapping rows of neighbouring kh live
       asm volatile("" ::: "memory");
       __builtin_amdgcn_sched_barrier(0);
-      if (ij + 1 < 9) load_b(tile, ij + 1, bv[(ij + 1) & 1]);
-      load_w(s + (ij + 2) / 9, (ij + 2) % 9, wr[(ij + 2) % 3]);
-      if (ij < 5) load_stage(s + 1, ij);
-      // The other LDS buffer was last read in stage s - 1, which every wave
-      // has finished (barrier below), so the next stage's tile is written
-      // here, mid-stage, interleaved with this stage's matrix-core work.
-      if (ij == 7) store_stage(s + 1, (s + 1) & 1);
+      load_w(ij + 2 < 9 ? cst.wbase : nst_.wbase, (ij + 2) % 9, wr[(ij + 2) % 3]);
+      if (ij < 5) load_stage(nst_, ij);
+      // The buffer written here was last read two stages ago (three
+      // buffers) or in the previous stage (two buffers); a barrier has
+      // passed since in both cases.
+      if (ij == 7) store_stage(nst_, s + 1 < nst, nxt);
 #pragma unroll
-      for (int pf = 0; pf < NPF; ++pf)
+      for (int pf = 0; pf < NPF; ++pf) {
 #pragma unroll
         for (int cf = 0; cf < WCO; ++cf)
           acc[cf][pf] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-              __builtin_bit_cast(bf16x8, bv[ij & 1][pf]), __builtin_bit_cast(bf16x8, wr[ij % 3][cf]),
+              __builtin_bit_cast(bf16x8, av[pf]), __builtin_bit_cast(bf16x8, wr[ij % 3][cf]),
               acc[cf][pf], 0, 0, 0);
-      // interleave: LDS reads, then global reads, then LDS writes, each
-      // between pairs of MFMAs (masks: 0x008 MFMA, 0x100 DS read,
-      // 0x020 VMEM read, 0x200 DS write)
-      if (ij + 1 < 9)
-        for (int q = 0; q < NPF; ++q) {
-          __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
-          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-        }
-      for (int q = 0; q < WCO + (ij < 4 ? TPT * 2 : ij == 4 ? HPT : 0); ++q) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-        __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+        if (ij + 1 < 9)
+          av[pf] = read_a(tile, ij + 1, pf);
+        else if (NBUF == 3)
+          av[pf] = read_a(ntile, 0, pf);
       }
-      if (ij == 7)
-        for (int q = 0; q < TPT * 8 + HPT; ++q) {
-          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      // explicit interleave (masks: 0x008 MFMA, 0x100 DS read, 0x020 VMEM
+      // read, 0x200 DS write): after each fragment's products, its re-read;
+      // global reads spread over the first groups, LDS writes over all
+      constexpr int nvm_stage = 2 * TPT;
+      const int nvm = WCO + (ij < 4 ? nvm_stage : ij == 4 ? HPT : 0);
+      const int ndw = ij == 7 ? TPT * 8 + HPT : 0;
+      const bool rd = ij + 1 < 9 || NBUF == 3;
+      for (int g = 0; g < NPF; ++g) {
+        __builtin_amdgcn_sched_group_barrier(0x008, WCO, 0);
+        if (rd) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        for (int q = (nvm * g) / NPF; q < (nvm * (g + 1)) / NPF; ++q)
+          __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+        for (int q = (ndw * g) / NPF; q < (ndw * (g + 1)) / NPF; ++q)
           __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);
-        }
+      }
+      if (NBUF == 3 && ij == 7) __syncthreads();
     }
-    __syncthreads();
+    if (NBUF == 2) {
+      __syncthreads();
+#pragma unroll
+      for (int pf = 0; pf < NPF; ++pf) av[pf] = read_a(ntile, 0, pf);
+    }
+    cst = nst_;
+    cur = nxt;
   }
 
   // ---- epilogue: bias once, round to bf16, NCTHW store.  With the
@@ -413,7 +466,7 @@ __global__ __launch_bounds__(64 * WAVES_CO * WAVES_PX, 1) void conv3d_bf16(Args 
   }
 }
 
-template <int WCO, int WR, int WCF, int WAVES_CO, int WAVES_PX>
+template <int WCO, int WR, int WCF, int WAVES_CO, int WAVES_PX, int NBUF>
 hipError_t run(const Geo& g, Args a, bool aligned, hipStream_t s) {
   constexpr int BCO = 16 * WCO * WAVES_CO, BH = WR * WAVES_PX, BW = 16 * WCF;
   a.tiles_co = static_cast<int>((g.d.Co + BCO - 1) / BCO);
@@ -425,9 +478,9 @@ hipError_t run(const Geo& g, Args a, bool aligned, hipStream_t s) {
   a.nblocks = static_cast<int>(blocks);
   const dim3 grid(static_cast<unsigned>(blocks)), block(64 * WAVES_CO * WAVES_PX);
   if (aligned)
-    hipLaunchKernelGGL((conv3d_bf16<WCO, WR, WCF, WAVES_CO, WAVES_PX, true>), grid, block, 0, s, a);
+    hipLaunchKernelGGL((conv3d_bf16<WCO, WR, WCF, WAVES_CO, WAVES_PX, NBUF, true>), grid, block, 0, s, a);
   else
-    hipLaunchKernelGGL((conv3d_bf16<WCO, WR, WCF, WAVES_CO, WAVES_PX, false>), grid, block, 0, s, a);
+    hipLaunchKernelGGL((conv3d_bf16<WCO, WR, WCF, WAVES_CO, WAVES_PX, NBUF, false>), grid, block, 0, s, a);
   return hipGetLastError();
 }
 
@@ -446,6 +499,20 @@ bool cache_covered(const Geo& g) {
 }
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// compute units of the current device (queried once per device)
+int64_t compute_units() {
+  static std::atomic<int> cache[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  int n = cache[dev].load(std::memory_order_relaxed);
+  if (n == 0) {
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+      n = 256;
+    cache[dev].store(n, std::memory_order_relaxed);
+  }
+  return n;
+}
 
 }  // namespace
 
@@ -477,9 +544,10 @@ hipError_t launch_fast_bf16(const Geo& g, const void* x, const void* cache, cons
   a.chunks = static_cast<int>(p.chunks);
   a.cofrags = static_cast<int>(p.cofrags);
   a.wpack_bytes = static_cast<uint32_t>(p.elems() * 2);
-  // 32-bit buffer offsets: one 32-channel chunk of a source frame and the
-  // packed weights must each span less than 2 GiB
-  const int64_t frames = g.d.T > g.d.Tc ? g.d.T : g.d.Tc;
+  // 32-bit buffer offsets: one 32-channel chunk of a source or cache frame
+  // and the packed weights must each span less than 2 GiB
+  int64_t frames = g.d.T > g.d.Tc ? g.d.T : g.d.Tc;
+  if (g.L > frames) frames = g.L;
   if (static_cast<int64_t>(BKC) * frames * a.hw * 2 >= 0x7fffffff || p.elems() * 2 >= 0x7fffffff)
     return hipErrorInvalidValue;
   a.has_bias = g.d.has_bias ? 1 : 0;
@@ -489,9 +557,19 @@ hipError_t launch_fast_bf16(const Geo& g, const void* x, const void* cache, cons
                        (cache == nullptr || aligned16(cache)) &&
                        (cache_out == nullptr || aligned16(cache_out));
   const int64_t Co = g.d.Co;
-  if (Co > 128 && Co % 192 == 0) return run<6, 2, 4, 2, 2>(g, a, aligned, s);
-  if (Co <= 96) return run<6, 2, 4, 1, 4>(g, a, aligned, s);
-  return run<5, 2, 4, 2, 2>(g, a, aligned, s);
+  if (Co > 128 && Co % 192 == 0) return run<6, 2, 4, 2, 2, 3>(g, a, aligned, s);
+  if (Co <= 96) return run<6, 2, 4, 1, 4, 2>(g, a, aligned, s);
+  // 160-channel tiles of 10 x 32 or 4 x 80 pixels: the shape with fewer
+  // rounds of workgroups over the device's compute units wins; a halo pixel
+  // is weighted as a quarter of an output pixel (it costs staging only)
+  const int64_t cus = compute_units();
+  auto cost = [&](int64_t bh, int64_t bw) {
+    const int64_t blocks = (Co + 159) / 160 * ((g.Wo + bw - 1) / bw) * ((g.Ho + bh - 1) / bh) *
+                           g.To * g.d.N;
+    return (blocks + cus - 1) / cus * (4 * bh * bw + (bh + 2) * (bw + 2) - bh * bw);
+  };
+  if (cost(4, 80) <= cost(10, 32)) return run<5, 2, 5, 2, 2, 3>(g, a, aligned, s);
+  return run<5, 5, 2, 2, 2, 3>(g, a, aligned, s);
 }
 
 }  // namespace c3c
