@@ -48,6 +48,11 @@ hipError_t launch_fast(const Geo& g, const void* x, const void* cache, const voi
 hipError_t launch_fast_bf16(const Geo& g, const void* x, const void* cache, const void* wpack,
                             const void* bias, void* y, void* cache_out, bool* cache_written,
                             hipStream_t s);
+// fallback, pointwise case (pointwise.hip): 1x1x1, unit spatial stride, no
+// spatial padding, one group, bf16 / fp16, aligned buffers
+bool pointwise_eligible(const Geo& g, const void* x, const void* cache, const void* w, const void* y);
+hipError_t launch_pointwise(const Geo& g, const void* x, const void* cache, const void* w,
+                            const void* bias, void* y, hipStream_t s);
 hipError_t launch_fallback(const Geo& g, const void* x, const void* cache, const void* w,
                            const void* bias, void* y, hipStream_t s);
 hipError_t launch_cache_copy(const Geo& g, const void* x, const void* cache, void* cache_out,

@@ -4,7 +4,8 @@
 // The fallback takes every call the fast route does not (the paper returns
 // unsupported calls to the original Conv3D, Alg. 1): any kernel size, stride,
 // dilation, groups, padding (including a negative effective left pad and a
-// right pad), and bf16 / fp16 / fp32 storage, accumulating in fp32.
+// right pad), and bf16 / fp16 / fp32 storage, accumulating in fp32.  Pointwise
+// (1x1x1) bf16 / fp16 calls go to the matrix-core kernel in pointwise.hip.
 #include "c3c_internal.h"
 
 #include <hip/hip_fp16.h>
@@ -259,6 +260,7 @@ bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) %
 hipError_t launch_fallback(const Geo& g, const void* x, const void* cache, const void* w,
                            const void* bias, void* y, hipStream_t s) {
   if (g.To == 0) return hipSuccess;
+  if (pointwise_eligible(g, x, cache, w, y)) return launch_pointwise(g, x, cache, w, bias, y, s);
   if (g.d.dtype == C3C_DTYPE_F32) return launch_fb<float>(g, x, cache, w, bias, y, s);
   return launch_fb<uint16_t>(g, x, cache, w, bias, y, s);
 }

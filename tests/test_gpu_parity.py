@@ -111,6 +111,19 @@ FALLBACK_CASES = FAST_CASES + [
     ("f32", dict(N=1, Ci=3, Co=5, T=7, Tc=0, H=9, W=9, Kt=7, Kh=7, Kw=7, p_base=6)),
     ("bf16", dict(N=2, Ci=300, Co=70, T=2, Tc=0, H=6, W=21, Kt=1, Kh=1, Kw=1)),
     ("bf16", dict(N=1, Ci=40, Co=33, T=3, Tc=2, H=5, W=600, Kh=3, Kw=5, p_w=2)),
+    # pointwise (1x1x1) calls on the matrix-core fallback kernel: ragged pixel
+    # tile, channel-chunk tail, two output-channel tiles
+    ("bf16", dict(N=1, Ci=40, Co=200, T=3, Tc=0, H=9, W=24, Kt=1, Kh=1, Kw=1)),
+    # fp16, a cached frame read and carried (p_base = 1)
+    ("f16", dict(N=2, Ci=64, Co=24, T=2, Tc=1, H=4, W=34, Kt=1, Kh=1, Kw=1, p_base=1)),
+    # temporal stride 2
+    ("bf16", dict(N=1, Ci=16, Co=8, T=5, Tc=0, H=8, W=16, Kt=1, Kh=1, Kw=1, s_t=2)),
+    # left pad past the cache: the first output frames are the bias alone
+    ("bf16", dict(N=1, Ci=24, Co=48, T=2, Tc=0, H=8, W=8, Kt=1, Kh=1, Kw=1, p_base=2)),
+    ("bf16", dict(N=1, Ci=24, Co=48, T=2, Tc=0, H=8, W=8, Kt=1, Kh=1, Kw=1, p_base=2,
+                  has_bias=0)),
+    # H*W not a multiple of 8: the generic kernel
+    ("bf16", dict(N=1, Ci=8, Co=16, T=2, Tc=0, H=3, W=5, Kt=1, Kh=1, Kw=1)),
 ]
 
 
