@@ -5,13 +5,18 @@
 // outside it), plus the bias once (the cached-conv definition, Eq. 1-2, with
 // Kt = Kh = Kw = 1).  bf16 / fp16 storage, matrix cores, fp32 accumulation.
 //
-// Workgroup = 160 output channels x 128 consecutive pixels of one (n, t)
-// frame; four waves of 80 channels x 64 pixels.  Per 32-channel chunk the
-// activation tile [32 ch][128 px] is copied into LDS as it lies in memory
+// Workgroup = 160 output channels x 256 consecutive pixels of one (n, t)
+// frame; eight waves of 80 channels x 64 pixels (each output row segment a
+// workgroup writes is 512 contiguous bytes).  Per 32-channel chunk the
+// activation tile [32 ch][256 px] is copied into LDS as it lies in memory
 // (pixels contiguous, as NCTHW stores them), and the transposing LDS read
 // ds_read_b64_tr_b16 turns it into the matrix-core operand (8 consecutive
-// channels of one pixel per lane).  Weights come straight from the unpacked
-// w[co][ci] rows (8 consecutive channels of one output channel per lane).
+// channels of one pixel per lane).  The chunk's weights w[co][32 ch] are
+// staged beside it.  Chunks stream through a ring of PD register sets: the
+// global loads of chunk c + PD are issued while chunk c computes.  The chunk
+// count is padded to a multiple of PD with chunks that read zeros, so every
+// step of the loop is unconditional (the wait counts for the ring's loads
+// then stay exact instead of falling back to the worst case).
 #include "c3c_internal.h"
 
 namespace c3c {
@@ -26,15 +31,23 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
 constexpr int PW_K = 32;       // input channels per chunk (one matrix-core K step)
-constexpr int PW_PX = 128;     // pixels per workgroup
+constexpr int PW_PX = 256;     // pixels per workgroup
+constexpr int PW_NT = 512;     // threads per workgroup: 2 x 4 waves
 constexpr int PW_WCO = 5;      // 16-channel output fragments per wave
 constexpr int PW_NPF = 4;      // 16-pixel fragments per wave
 constexpr int PW_CO = 2 * 16 * PW_WCO;  // output channels per workgroup
-// LDS bytes per staged channel row: 128 px * 2 B + 32 B.  The pad makes the
-// row stride 8 banks mod 64, so the 4 channel rows x 4 pixel groups that one
-// 16-lane block of a transposing read touches fall in distinct banks.
+// LDS bytes per staged activation channel row: 256 px * 2 B + 32 B.  The pad
+// makes the row stride 8 banks mod 64, so the 4 channel rows x 4 pixel groups
+// that one 16-lane block of a transposing read touches fall in distinct banks.
 constexpr int PW_PITCH = PW_PX * 2 + 32;
-constexpr int PW_BUF = PW_K * PW_PITCH;
+// LDS bytes per staged weight row (32 channels of one output channel): 64 B
+// + 16 B, so that 8 consecutive rows read with 16-byte loads hit distinct
+// 4-bank groups.
+constexpr int PW_WPITCH = 80;
+constexpr int PW_WOFF = PW_K * PW_PITCH;            // weights after the activations
+constexpr int PW_BUF = PW_WOFF + PW_CO * PW_WPITCH;
+constexpr int PW_WPIECES = PW_CO * PW_K * 2 / 16;    // 16-byte pieces of a weight chunk
+constexpr int PW_WPT = (PW_WPIECES + PW_NT - 1) / PW_NT;  // per thread
 
 struct PwArgs {
   const uint16_t* x;
@@ -72,15 +85,23 @@ __device__ inline f32x4 mma(i16x8 a, u32x4 b, f32x4 c) {
                                                    __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
 }
 
-template <bool F16>
-__global__ __launch_bounds__(256) void pointwise_conv(PwArgs a) {
+template <bool F16, int PD>
+__global__ __launch_bounds__(PW_NT, 1) void pointwise_conv(PwArgs a) {
   __shared__ __align__(16) unsigned char lds[2 * PW_BUF];
   constexpr uint32_t OOB = 0x80000000u;  // beyond every resource's size
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wco = wave & 1, wpx = wave >> 1;
 
-  int b = blockIdx.x;
+  // workgroups numbered so that each of the 8 XCDs (which take workgroups
+  // round-robin) runs a contiguous range of pixel tiles: neighbouring tiles
+  // of a channel row are then read close together in time
+  int b;
+  {
+    const int nb = static_cast<int>(gridDim.x), per = nb / 8, rem = nb % 8;
+    const int xcd = blockIdx.x % 8, slot = blockIdx.x / 8;
+    b = (xcd < rem ? xcd * (per + 1) : rem * (per + 1) + (xcd - rem) * per) + slot;
+  }
   const int pt = b % a.px_tiles;
   b /= a.px_tiles;
   const int ctile = b % a.co_tiles;
@@ -114,37 +135,46 @@ __global__ __launch_bounds__(256) void pointwise_conv(PwArgs a) {
                                              static_cast<int>(bytes), 0x00020000);
   };
 
-  // staging: thread -> channel row tid / 8, pixels 16 * (tid % 8) .. + 15
-  const int sch = tid >> 3, spx = (tid & 7) * 16;
+  // staging: thread -> activation channel row tid / 16, pixels 8 (tid % 16)
+  // .. + 7 and 128 + 8 (tid % 16) .. + 7 (16 lanes read 256 contiguous bytes);
+  // weight pieces tid + 512 i -> row piece / 4, channels 8 (piece % 4) .. + 7
+  const int sch = tid >> 4, spx = (tid & 15) * 8;
   const uint32_t soff = static_cast<uint32_t>(sch) * cs + static_cast<uint32_t>(spx) * 2u;
   const int slds = sch * PW_PITCH + spx * 2;
-  u32x4 sv[2];
-  auto load_chunk = [&](int c) {
-    const __amdgpu_buffer_rsrc_t rs = chunk_rsrc(c);
-    sv[0] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, soff, 0, 0));
-    sv[1] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, soff + 16u, 0, 0));
-  };
-  auto store_chunk = [&](int buf) {
-    *reinterpret_cast<u32x4*>(lds + buf * PW_BUF + slds) = sv[0];
-    *reinterpret_cast<u32x4*>(lds + buf * PW_BUF + slds + 16) = sv[1];
-  };
-
-  // weights: lane l holds w[co = frag * 16 + l % 16][ci = 32c + 8 (l / 16) .. + 7];
   // rows past Co and channels past Ci are out-of-range offsets (zeros)
   const __amdgpu_buffer_rsrc_t wrs = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint16_t*>(a.w), 0, static_cast<int>(static_cast<int64_t>(a.Co) * a.Ci * 2), 0x00020000);
-  const int cof0 = ctile * PW_CO + wco * 16 * PW_WCO + (lane & 15);
-  const int wci = 8 * (lane >> 4);
-  u32x4 wv[PW_WCO];
-  auto load_w = [&](int c) {
-    const int ci = c * PW_K + wci;
+  int wrow[PW_WPT], wq[PW_WPT];
 #pragma unroll
-    for (int cf = 0; cf < PW_WCO; ++cf) {
-      const int co = cof0 + 16 * cf;
-      const uint32_t off = (co < a.Co) & (ci < a.Ci)
-                               ? static_cast<uint32_t>(co * a.Ci + ci) * 2u : OOB;
-      wv[cf] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(wrs, off, 0, 0));
+  for (int i = 0; i < PW_WPT; ++i) {
+    const int piece = tid + PW_NT * i;
+    wrow[i] = piece >> 2;
+    wq[i] = (piece & 3) * 8;
+  }
+  struct Chunk {
+    u32x4 x[2];
+    u32x4 w[PW_WPT];
+  };
+  auto load_chunk = [&](int c, Chunk& ck) {
+    const __amdgpu_buffer_rsrc_t rs = chunk_rsrc(c);
+    ck.x[0] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, soff, 0, 0));
+    ck.x[1] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, soff + 256u, 0, 0));
+#pragma unroll
+    for (int i = 0; i < PW_WPT; ++i) {
+      const int co = ctile * PW_CO + wrow[i], ci = c * PW_K + wq[i];
+      const bool ok = (wrow[i] < PW_CO) & (co < a.Co) & (ci < a.Ci);
+      ck.w[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                                              wrs, ok ? static_cast<uint32_t>(co * a.Ci + ci) * 2u : OOB, 0, 0));
     }
+  };
+  auto store_chunk = [&](const Chunk& ck, int buf) {
+    unsigned char* base = lds + buf * PW_BUF;
+    *reinterpret_cast<u32x4*>(base + slds) = ck.x[0];
+    *reinterpret_cast<u32x4*>(base + slds + 256) = ck.x[1];
+#pragma unroll
+    for (int i = 0; i < PW_WPT; ++i)
+      if (wrow[i] < PW_CO)
+        *reinterpret_cast<u32x4*>(base + PW_WOFF + wrow[i] * PW_WPITCH + wq[i] * 2) = ck.w[i];
   };
 
   // transposing operand read: within each 16-lane block (channel group
@@ -159,6 +189,12 @@ __global__ __launch_bounds__(256) void pointwise_conv(PwArgs a) {
     const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p + 4 * PW_PITCH));
     return i16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
   };
+  // weight operand: lane l holds w[co = frag * 16 + l % 16][ci = 8 (l / 16) .. + 7]
+  const int cof0 = ctile * PW_CO + wco * 16 * PW_WCO + (lane & 15);
+  const int rb = PW_WOFF + (wco * 16 * PW_WCO + j) * PW_WPITCH + 16 * g;
+  auto read_b = [&](int buf, int cf) {
+    return *reinterpret_cast<const u32x4*>(lds + buf * PW_BUF + rb + cf * 16 * PW_WPITCH);
+  };
 
   f32x4 acc[PW_WCO][PW_NPF];
 #pragma unroll
@@ -166,24 +202,30 @@ __global__ __launch_bounds__(256) void pointwise_conv(PwArgs a) {
 #pragma unroll
     for (int pf = 0; pf < PW_NPF; ++pf) acc[cf][pf] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  load_chunk(0);
-  store_chunk(0);
-  __syncthreads();
-  for (int c = 0; c < a.chunks; ++c) {
-    const int buf = c & 1;
-    if (c + 1 < a.chunks) load_chunk(c + 1);
-    load_w(c);
-    i16x8 av[PW_NPF];
+  Chunk ring[PD];
 #pragma unroll
-    for (int pf = 0; pf < PW_NPF; ++pf) av[pf] = read_a(buf, pf);
+  for (int u = 0; u < PD; ++u) load_chunk(u, ring[u]);
+  const int padded = (a.chunks + PD - 1) / PD * PD;
+  for (int c0 = 0; c0 < padded; c0 += PD) {
 #pragma unroll
-    for (int pf = 0; pf < PW_NPF; ++pf)
+    for (int u = 0; u < PD; ++u) {
+      const int c = c0 + u, buf = c & 1;
+      // buffer `buf` was last read while computing chunk c - 2, which every
+      // wave finished before the barrier of chunk c - 1
+      store_chunk(ring[u], buf);
+      load_chunk(c + PD, ring[u]);
+      __syncthreads();
+      i16x8 av[PW_NPF];
+      u32x4 bv[PW_WCO];
 #pragma unroll
-      for (int cf = 0; cf < PW_WCO; ++cf) acc[cf][pf] = mma<F16>(av[pf], wv[cf], acc[cf][pf]);
-    // the other buffer was last read in chunk c - 1, before the barrier that
-    // ended it
-    if (c + 1 < a.chunks) store_chunk(buf ^ 1);
-    __syncthreads();
+      for (int pf = 0; pf < PW_NPF; ++pf) av[pf] = read_a(buf, pf);
+#pragma unroll
+      for (int cf = 0; cf < PW_WCO; ++cf) bv[cf] = read_b(buf, cf);
+#pragma unroll
+      for (int pf = 0; pf < PW_NPF; ++pf)
+#pragma unroll
+        for (int cf = 0; cf < PW_WCO; ++cf) acc[cf][pf] = mma<F16>(av[pf], bv[cf], acc[cf][pf]);
+    }
   }
 
   // epilogue: lane l holds pixels 4 (l / 16) .. + 3 of output channel l % 16
@@ -261,10 +303,22 @@ hipError_t launch_pointwise(const Geo& g, const void* x, const void* cache, cons
   const int64_t blocks = static_cast<int64_t>(a.px_tiles) * a.co_tiles * g.To * d.N;
   if (blocks == 0) return hipSuccess;
   if (blocks > 0x7fffffff) return hipErrorInvalidConfiguration;
-  if (d.dtype == C3C_DTYPE_F16)
-    hipLaunchKernelGGL(pointwise_conv<true>, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, s, a);
-  else
-    hipLaunchKernelGGL(pointwise_conv<false>, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, s, a);
+  // ring depth: the one of 4, 3, 2 that pads the chunk count least
+  int pd = 4;
+  for (int cand : {3, 2})
+    if ((a.chunks + cand - 1) / cand * cand < (a.chunks + pd - 1) / pd * pd) pd = cand;
+  const dim3 grid(static_cast<unsigned>(blocks)), block(PW_NT);
+  const bool f16 = d.dtype == C3C_DTYPE_F16;
+  if (pd == 2) {
+    if (f16) hipLaunchKernelGGL((pointwise_conv<true, 2>), grid, block, 0, s, a);
+    else hipLaunchKernelGGL((pointwise_conv<false, 2>), grid, block, 0, s, a);
+  } else if (pd == 4) {
+    if (f16) hipLaunchKernelGGL((pointwise_conv<true, 4>), grid, block, 0, s, a);
+    else hipLaunchKernelGGL((pointwise_conv<false, 4>), grid, block, 0, s, a);
+  } else {
+    if (f16) hipLaunchKernelGGL((pointwise_conv<true, 3>), grid, block, 0, s, a);
+    else hipLaunchKernelGGL((pointwise_conv<false, 3>), grid, block, 0, s, a);
+  }
   return hipGetLastError();
 }
 
