@@ -105,9 +105,8 @@ __global__ __launch_bounds__(64 * WAVES_CO * WAVES_PX, 1) void conv3d_bf16(Args 
   constexpr int NT = 64 * WAVES_CO * WAVES_PX;
   constexpr int BH = WR * WAVES_PX, BW = 16 * WCF;
   constexpr int TH = BH + 2, TW = BW + 2;
-  constexpr int TH4 = (TH + 3) / 4 * 4;
   constexpr int NCH = BW / 8;                   // 8-pixel segments per tile row
-  constexpr int NTASK = TH4 * NCH * (BKC / 8);  // (row, segment, 8-channel group)
+  constexpr int NTASK = TH * NCH * (BKC / 8);   // (row, segment, 8-channel group)
   constexpr int TPT = (NTASK + NT - 1) / NT;
   constexpr int NHALO = TH * 2 * BKC;           // left / right halo column elements
   constexpr int HPT = (NHALO + NT - 1) / NT;
@@ -188,19 +187,17 @@ __global__ __launch_bounds__(64 * WAVES_CO * WAVES_PX, 1) void conv3d_bf16(Args 
     return st;
   };
 
-  // ---- per-thread staging constants.  Task decode: lane bits (g0, r0, r1,
-  // g1) first so that the 8 lanes of one LDS write cycle hit 8 distinct
-  // 16-byte bank groups.  A task is 8 channels (8g ..) x 8 pixels of one
-  // halo-tile row.
+  // ---- per-thread staging constants.  A task is 8 channels (8g ..) x 8
+  // pixels of one halo-tile row; tasks are numbered channel group fastest,
+  // then row, so that the 8 lanes of one LDS write cycle (4 groups x 2 rows)
+  // hit 8 distinct 16-byte bank groups.
   uint32_t t_g8[TPT], t_pix[TPT], t_lds[TPT];
   bool t_st[TPT], t_ok[TPT], t_in[TPT];
   int t_w[TPT];
 #pragma unroll
   for (int tt = 0; tt < TPT; ++tt) {
     const int t = tid + tt * NT;
-    const int g = (t & 1) | (((t >> 3) & 1) << 1);
-    const int rr = ((t >> 1) & 3) | (((t >> 4) % (TH4 / 4)) << 2);
-    const int q = (t >> 4) / (TH4 / 4);
+    const int g = t & 3, rr = (t >> 2) % TH, q = (t >> 2) / TH;
     const int gh = h0 - 1 + rr, w = w0 + 8 * q;
     t_st[tt] = (t < NTASK) & (rr < TH);
     // bitwise & (not &&): validity must become selects, not branches
