@@ -53,6 +53,8 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
 
 constexpr int BKC = 32;   // input channels per stage = K of one matrix-core step
 constexpr int PIXB = 96;  // LDS bytes per staged pixel: 32 ch * 2 B + 32 B pad (bank-conflict-free B reads)
@@ -74,13 +76,6 @@ struct Args {
   int has_bias;
   int write_cache;
 };
-
-__device__ inline uint16_t f32_to_bf16(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return static_cast<uint16_t>((u >> 16) | 0x40u);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return static_cast<uint16_t>(u >> 16);
-}
 
 // 8 channel rows of 8 pixels (v[c] = pixels 0..7 of channel c) -> 8 pixel
 // records of 8 channels (o[p] = channels 0..7 of pixel p).
@@ -447,14 +442,17 @@ __global__ __launch_bounds__(64 * WAVES_CO * WAVES_PX, 1) void conv3d_bf16(Args 
     for (int pf = 0; pf < NPF; ++pf) {
       const int h = h0 + wpx * WR + pf / WCF, w = w0 + (pf % WCF) * 16 + 4 * (lane >> 4);
       if (co >= a.Co || h >= a.H || w >= a.W) continue;
-      uint16_t v[4];
-#pragma unroll
-      for (int r = 0; r < 4; ++r) v[r] = f32_to_bf16(acc[cf][pf][r] + bb);
+      // one round-to-nearest-even conversion per value (hardware, two at a time)
+      const uint32_t v01 = __builtin_bit_cast(
+          uint32_t, __builtin_convertvector((f32x2{acc[cf][pf][0] + bb, acc[cf][pf][1] + bb}), bf16x2));
+      const uint32_t v23 = __builtin_bit_cast(
+          uint32_t, __builtin_convertvector((f32x2{acc[cf][pf][2] + bb, acc[cf][pf][3] + bb}), bf16x2));
       uint16_t* dst = ybase + co * plane + static_cast<int64_t>(h) * a.W + w;
       if (ALIGNED && w + 4 <= a.W) {
-        *reinterpret_cast<uint2*>(dst) = make_uint2(v[0] | (static_cast<uint32_t>(v[1]) << 16),
-                                                   v[2] | (static_cast<uint32_t>(v[3]) << 16));
+        *reinterpret_cast<uint2*>(dst) = make_uint2(v01, v23);
       } else {
+        const uint16_t v[4] = {static_cast<uint16_t>(v01), static_cast<uint16_t>(v01 >> 16),
+                               static_cast<uint16_t>(v23), static_cast<uint16_t>(v23 >> 16)};
 #pragma unroll
         for (int r = 0; r < 4; ++r)
           if (w + r < a.W) dst[r] = v[r];
