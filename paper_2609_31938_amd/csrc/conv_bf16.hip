@@ -109,8 +109,14 @@ __global__ __launch_bounds__(64 * WAVES_CO * WAVES_PX, 1) void conv3d_bf16(Args 
   constexpr int NPF = WR * WCF;                 // pixel fragments per wave
   static_assert(TW % 8 == 2, "the staging lane order assumes TW = 2 mod 8");
   static_assert(NBUF == 2 || NBUF == 3, "two or three tile buffers");
-  static_assert(NBUF * BUF <= 160 * 1024, "LDS tile buffers exceed 160 KiB");
-  __shared__ __align__(16) unsigned char lds[NBUF * BUF];
+  // Lanes without a staging task or halo element still write, to a private
+  // slot of a dummy region after the tile buffers: the tile write is then
+  // free of branches, so it interleaves with the matrix-core steps and no
+  // load is left outstanding on a skipped path.
+  constexpr int DUMMY = NBUF * BUF;
+  constexpr int DUMMY_BYTES = 64 * 16 + 7 * PIXB;
+  static_assert(NBUF * BUF + DUMMY_BYTES <= 160 * 1024, "LDS tile buffers exceed 160 KiB");
+  __shared__ __align__(16) unsigned char lds[NBUF * BUF + DUMMY_BYTES];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
@@ -163,18 +169,15 @@ __global__ __launch_bounds__(64 * WAVES_CO * WAVES_PX, 1) void conv3d_bf16(Args 
     st.k = k_lo + ki;
     st.c0 = chunk * BKC;
     st.f = o + st.k * a.dt - a.p_l;
-    const uint16_t* base;
-    int64_t cstride;
-    if (st.f < a.Tc) {
-      cstride = static_cast<int64_t>(a.Tc) * a.hw;
-      base = a.cache + (static_cast<int64_t>(n) * a.Ci + st.c0) * cstride + st.f * a.hw;
-    } else {
-      cstride = static_cast<int64_t>(a.T) * a.hw;
-      base = a.x + (static_cast<int64_t>(n) * a.Ci + st.c0) * cstride + (st.f - a.Tc) * a.hw;
-    }
+    // selects, not a branch: the stage loop stays one basic block
+    const bool in_cache = st.f < a.Tc;
+    const int64_t cstride = static_cast<int64_t>(in_cache ? a.Tc : a.T) * a.hw;
+    const uint16_t* src = in_cache ? a.cache : a.x;
+    const int64_t fr = in_cache ? st.f : st.f - a.Tc;
+    const uint16_t* base = src + (static_cast<int64_t>(n) * a.Ci + st.c0) * cstride + fr * a.hw;
     int64_t bytes = ((a.Ci - 1 - st.c0) * cstride + a.hw) * 2;
-    if (bytes > 0x7fffffff) bytes = 0x7fffffff;
-    if (bytes < 0) bytes = 0;
+    bytes = bytes > 0x7fffffff ? 0x7fffffff : bytes;
+    bytes = bytes < 0 ? 0 : bytes;
     st.rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(base), 0,
                                               static_cast<int>(bytes), 0x00020000);
     st.cs = static_cast<uint32_t>(cstride * 2);
@@ -255,53 +258,63 @@ __global__ __launch_bounds__(64 * WAVES_CO * WAVES_PX, 1) void conv3d_bf16(Args 
           st.rs, h_ok[hh] ? h_ch[hh] * st.cs + h_pix[hh] : OOB, 0, 0);
   };
 
-  // transpose the staged registers into LDS buffer `buf`; the designated
-  // workgroup also writes its interior rows of a cache frame to cache_out,
-  // through a buffer resource that ends after the last real channel (stores
-  // at out-of-range offsets are dropped)
-  auto store_stage = [&](const Stage& st, bool real, int buf) {
-    unsigned char* tile = lds + buf * BUF;
-    const bool cw = a.write_cache && real && ct == 0 && st.f >= a.Z - a.L &&
-                    (st.k == a.Kt - 1 || o < a.dt);
-    __amdgpu_buffer_rsrc_t crs;
-    uint32_t ccs = 0;
-    if (cw) {
-      const int64_t cstride = static_cast<int64_t>(a.L) * a.hw;
-      uint16_t* cbase = a.cache_out + (static_cast<int64_t>(n) * a.Ci + st.c0) * cstride +
-                        static_cast<int64_t>(st.f - (a.Z - a.L)) * a.hw;
-      int64_t bytes = ((a.Ci - 1 - st.c0) * cstride + a.hw) * 2;
-      if (bytes > 0x7fffffff) bytes = 0x7fffffff;
-      crs = __builtin_amdgcn_make_buffer_rsrc(cbase, 0, static_cast<int>(bytes), 0x00020000);
-      ccs = static_cast<uint32_t>(cstride * 2);
-    }
+  // transpose the staged registers into LDS buffer `buf` (no branches:
+  // lanes without a task or halo element write to their dummy slot)
+  auto store_stage = [&](int buf) {
 #pragma unroll
     for (int tt = 0; tt < TPT; ++tt) {
-      if (t_st[tt]) {
-        u32x4 pr[8];
-        transpose8x8(sv[tt], pr);
+      u32x4 pr[8];
+      transpose8x8(sv[tt], pr);
+      const uint32_t at = t_st[tt] ? static_cast<uint32_t>(buf * BUF) + t_lds[tt]
+                                   : static_cast<uint32_t>(DUMMY + 16 * lane);
 #pragma unroll
-        for (int p = 0; p < 8; ++p)
-          *reinterpret_cast<u32x4*>(tile + t_lds[tt] + p * PIXB) = pr[p];
-      }
-      if (cw) {
-        const uint32_t off = t_in[tt] ? t_g8[tt] * ccs + t_pix[tt] : OOB;
+      for (int p = 0; p < 8; ++p)
+        *reinterpret_cast<u32x4*>(lds + at + p * PIXB) = pr[p];
+    }
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          if (ALIGNED) {
-            __builtin_amdgcn_raw_buffer_store_b128(sv[tt][j], crs, off + j * ccs, 0, 0);
-          } else {
+    for (int hh = 0; hh < HPT; ++hh) {
+      const uint32_t at = h_in[hh] ? static_cast<uint32_t>(buf * BUF) + h_lds[hh]
+                                   : static_cast<uint32_t>(DUMMY + 2 * lane);
+      *reinterpret_cast<uint16_t*>(lds + at) = hv[hh];
+    }
+  };
+
+  // The designated workgroup writes its interior rows of a cache frame to
+  // cache_out from the staging registers, through a buffer resource that ends
+  // after the last real channel (stores at out-of-range offsets are dropped).
+  // The condition is uniform over the workgroup.
+  // The writers of a frame's chunks are spread over the output-channel tiles
+  // (chunk c is written by tile c mod tiles_co), so that no tile carries the
+  // whole cache write.
+  auto cache_needed = [&](const Stage& st, bool real) {
+    return a.write_cache && real && (st.c0 / BKC) % a.tiles_co == ct && st.f >= a.Z - a.L &&
+           (st.k == a.Kt - 1 || o < a.dt);
+  };
+  auto cache_store = [&](const Stage& st) {
+    const int64_t cstride = static_cast<int64_t>(a.L) * a.hw;
+    uint16_t* cbase = a.cache_out + (static_cast<int64_t>(n) * a.Ci + st.c0) * cstride +
+                      static_cast<int64_t>(st.f - (a.Z - a.L)) * a.hw;
+    int64_t bytes = ((a.Ci - 1 - st.c0) * cstride + a.hw) * 2;
+    bytes = bytes > 0x7fffffff ? 0x7fffffff : bytes;
+    const __amdgpu_buffer_rsrc_t crs =
+        __builtin_amdgcn_make_buffer_rsrc(cbase, 0, static_cast<int>(bytes), 0x00020000);
+    const uint32_t ccs = static_cast<uint32_t>(cstride * 2);
 #pragma unroll
-            for (int e = 0; e < 8; ++e)
-              __builtin_amdgcn_raw_buffer_store_b16(
-                  static_cast<uint16_t>(sv[tt][j][e >> 1] >> (16 * (e & 1))), crs,
-                  t_w[tt] + e < a.W ? off + j * ccs + 2u * e : OOB, 0, 0);
-          }
+    for (int tt = 0; tt < TPT; ++tt) {
+      const uint32_t off = t_in[tt] ? t_g8[tt] * ccs + t_pix[tt] : OOB;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        if (ALIGNED) {
+          __builtin_amdgcn_raw_buffer_store_b128(sv[tt][j], crs, off + j * ccs, 0, 0);
+        } else {
+#pragma unroll
+          for (int e = 0; e < 8; ++e)
+            __builtin_amdgcn_raw_buffer_store_b16(
+                static_cast<uint16_t>(sv[tt][j][e >> 1] >> (16 * (e & 1))), crs,
+                t_w[tt] + e < a.W ? off + j * ccs + 2u * e : OOB, 0, 0);
         }
       }
     }
-#pragma unroll
-    for (int hh = 0; hh < HPT; ++hh)
-      if (h_in[hh]) *reinterpret_cast<uint16_t*>(tile + h_lds[hh]) = hv[hh];
   };
 
   // Weights of (kh, kw) step ij of a stage for this wave's fragments: one
@@ -357,7 +370,8 @@ __global__ __launch_bounds__(64 * WAVES_CO * WAVES_PX, 1) void conv3d_bf16(Args 
     load_w(cst.wbase, 0, wr[0]);
     load_w(cst.wbase, 1, wr[1]);
     for (int part = 0; part < 5; ++part) load_stage(cst, part);
-    store_stage(cst, true, 0);
+    if (cache_needed(cst, true)) cache_store(cst);
+    store_stage(0);
     __syncthreads();
 #pragma unroll
     for (int pf = 0; pf < NPF; ++pf) av[pf] = read_a(lds + lane_off, 0, pf);
@@ -380,6 +394,9 @@ __global__ __launch_bounds__(64 * WAVES_CO * WAVES_PX, 1) void conv3d_bf16(Args 
     const unsigned char* ntile = lds + nxt * BUF + lane_off;
 #pragma unroll
     for (int ij = 0; ij < 9; ++ij) {
+      // the cache write (rare, workgroup-uniform) is its own block ahead of
+      // the scheduled region of step 7
+      if (ij == 7 && cache_needed(nst_, s + 1 < nst)) cache_store(nst_);
       // keep every LDS read inside its own step: re-reading is cheaper in
       // registers than keeping overlapping rows of neighbouring kh live
       asm volatile("" ::: "memory");
@@ -389,7 +406,7 @@ __global__ __launch_bounds__(64 * WAVES_CO * WAVES_PX, 1) void conv3d_bf16(Args 
       // The buffer written here was last read two stages ago (three
       // buffers) or in the previous stage (two buffers); a barrier has
       // passed since in both cases.
-      if (ij == 7) store_stage(nst_, s + 1 < nst, nxt);
+      if (ij == 7) store_stage(nxt);
 #pragma unroll
       for (int pf = 0; pf < NPF; ++pf) {
 #pragma unroll
@@ -554,16 +571,17 @@ hipError_t launch_fast_bf16(const Geo& g, const void* x, const void* cache, cons
   const int64_t Co = g.d.Co;
   if (Co > 128 && Co % 192 == 0) return run<6, 2, 4, 2, 2, 3>(g, a, aligned, s);
   if (Co <= 96) return run<6, 2, 4, 1, 4, 2>(g, a, aligned, s);
-  // 160-channel tiles of 10 x 32 or 4 x 80 pixels: the shape with fewer
-  // rounds of workgroups over the device's compute units wins; a halo pixel
-  // is weighted as a quarter of an output pixel (it costs staging only)
+  // 160-channel tiles of 4 x 80 or 10 x 32 pixels.  A workgroup of either
+  // shape takes about the same time (measured), so the shape with fewer
+  // rounds of workgroups over the device's compute units wins; on a tie,
+  // 4 x 80 (half the halo-column loads).
   const int64_t cus = compute_units();
-  auto cost = [&](int64_t bh, int64_t bw) {
+  auto rounds = [&](int64_t bh, int64_t bw) {
     const int64_t blocks = (Co + 159) / 160 * ((g.Wo + bw - 1) / bw) * ((g.Ho + bh - 1) / bh) *
                            g.To * g.d.N;
-    return (blocks + cus - 1) / cus * (4 * bh * bw + (bh + 2) * (bw + 2) - bh * bw);
+    return (blocks + cus - 1) / cus;
   };
-  if (cost(4, 80) <= cost(10, 32)) return run<5, 2, 5, 2, 2, 3>(g, a, aligned, s);
+  if (rounds(4, 80) <= rounds(10, 32)) return run<5, 2, 5, 2, 2, 3>(g, a, aligned, s);
   return run<5, 5, 2, 2, 2, 3>(g, a, aligned, s);
 }
 
