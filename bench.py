@@ -34,6 +34,7 @@ METRIC = ("causal Conv3D TFLOP/s and % of bf16 MFMA peak per layer shape; "
           "chunk latency (ms)")
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 matrix peak (published)
 PEAK_F32_TFLOPS = 157.3     # MI355X fp32 matrix peak (published)
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E peak (published)
 
 
 def main():
@@ -47,6 +48,13 @@ def main():
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a plain 512 MiB device copy (the reference kernel "
                          "for scaling FETCH_SIZE / WRITE_SIZE counters) and exit")
+    ap.add_argument("--layer", default=None,
+                    help="time only this layer of the workload (for per-layer profiles); "
+                         "the JSON line then covers that layer alone")
+    ap.add_argument("--gemm-reference", action="store_true",
+                    help="time the vendor bf16 GEMM (torch.matmul) on square and "
+                         "conv-shaped problems and exit: what the matrix cores reach "
+                         "on this device outside this library")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
@@ -59,6 +67,9 @@ def main():
     if args.copy_calibration:
         copy_calibration()
         return
+    if args.gemm_reference:
+        gemm_reference()
+        return
 
     wl = inputs.WORKLOADS[args.workload]
     dtype = wl["dtype"]
@@ -69,13 +80,20 @@ def main():
 
     # ---------------------------------------------------------------- setup
     layers = []
+    names = [lname for lname, _ in wl["layers"]]
+    if args.layer is not None and args.layer not in names:
+        print(f"unknown layer {args.layer!r}; the workload has {names}", file=sys.stderr)
+        sys.exit(2)
     for lid, (lname, sp) in enumerate(wl["layers"]):
+        if args.layer is not None and lname != args.layer:
+            continue
         w, b = inputs.layer_tensors(sp, dtype, wl["id"], lid, dev)
         route, why = c3c.route_query(None, sp, dtype)
+        torch.cuda.synchronize()
         t0 = time.perf_counter()
         wpack = c3c.weight_repack(ctx, sp, w) if route == "fast" else None
         torch.cuda.synchronize()
-        repack_ms = (time.perf_counter() - t0) * 1e3
+        repack_ms = (time.perf_counter() - t0) * 1e3 if route == "fast" else None
         To, Ho, Wo, L = c3c.output_dims(sp, dtype)
         xs = [inputs.chunk_input(sp, dtype, wl["id"], lid, c, dev) for c in range(chunks)]
         y = torch.empty((sp["N"], sp["Co"], To, Ho, Wo), dtype=w.dtype, device=dev)
@@ -144,20 +162,30 @@ def main():
                               gflop=round(fl / 1e9, 3), ms_median=round(med, 4),
                               ms_mean=round(sum(times) / len(times), 4),
                               tflops=round(tf, 2), frac_peak=round(tf / peak, 4),
-                              repack_ms=round(L_["repack_ms"], 3)))
+                              repack_ms=(round(L_["repack_ms"], 3)
+                                         if L_["repack_ms"] is not None else None)))
     value = total_flops / (total_ms * 1e-3) / 1e12
 
     # dominant kernel: the fast conv on the largest layer
-    fast_layers = [p for p in per_layer if p["route"] == "fast"]
+    fast_layers = [p for p in per_layer if p["route"] == "fast"] or per_layer
     dom = max(fast_layers, key=lambda p: p["gflop"])
     dom_i = [p["layer"] for p in per_layer].index(dom["layer"])
     dom_mean_ms = dom["ms_mean"]
     achieved = dom["gflop"] * 1e9 / (dom_mean_ms * 1e-3) / 1e12
     peak = PEAK_BF16_TFLOPS if dtype == "bf16" else PEAK_F32_TFLOPS
-    roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak,
-                "unit": "TFLOP/s", "frac": round(achieved / peak, 4),
-                "traffic": measured_traffic(dom["layer"]),
-                "kernel": f"conv3d_bf16 (fast route), layer {dom['layer']}"}
+    if dom["route"] == "fast":
+        roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak,
+                    "unit": "TFLOP/s", "frac": round(achieved / peak, 4),
+                    "traffic": measured_traffic(dom["layer"]),
+                    "kernel": f"conv3d_bf16 (fast route), layer {dom['layer']}"}
+    else:
+        # a fallback layer timed alone (--layer): HBM-bound, algorithmic bytes
+        gbs = algorithmic_bytes(layers[dom_i]["sp"], dtype) / (dom_mean_ms * 1e-3) / 1e9
+        roofline = {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS,
+                    "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4), "traffic": None,
+                    "kernel": f"fallback route, layer {dom['layer']}"}
+    shapes = sorted({(L_["sp"]["T"], L_["sp"]["Tc"]) for L_ in layers})
+    frames = ", ".join(f"T={t} new + {tc} cached frames" for t, tc in shapes)
 
     out = {
         "metric": METRIC,
@@ -173,7 +201,7 @@ def main():
         "dtype": dtype,
         "data": "synthetic",
         "config": {"workload": f"{args.workload}: " + ", ".join(
-            f"{L_['name']}" for L_ in layers) + f"; N=1, T=4 new + 2 cached frames, "
+            f"{L_['name']}" for L_ in layers) + f"; N=1, {frames}, "
             f"{chunks}-chunk cache carry; step = one chunk through every layer",
             "global_batch": 1, "chunks_per_stream": chunks},
         "chunk_latency_ms": round(total_ms / args.steps, 4),
@@ -185,6 +213,23 @@ def main():
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(layers[dom_i], dtype, args.cpu_seconds)
     print(json.dumps(out), flush=True)
+
+
+def algorithmic_bytes(sp, dtype):
+    """Bytes one call must move at least: read x, cache, w and bias once,
+    write y and the new cache once."""
+    es = 4 if dtype == "f32" else 2
+    hw = sp["H"] * sp["W"]
+    Z = sp["Tc"] + sp["T"]
+    L = min(sp["p_base"], Z)
+    p_l = sp["p_base"] - sp["Tc"]
+    To = (Z + p_l + sp["p_r"] - sp["d_t"] * (sp["Kt"] - 1) - 1) // sp["s_t"] + 1
+    Ho = (sp["H"] + 2 * sp["p_h"] - sp["d_h"] * (sp["Kh"] - 1) - 1) // sp["s_h"] + 1
+    Wo = (sp["W"] + 2 * sp["p_w"] - sp["d_w"] * (sp["Kw"] - 1) - 1) // sp["s_w"] + 1
+    n_in = sp["N"] * sp["Ci"] * Z * hw
+    n_w = sp["Co"] * (sp["Ci"] // sp["groups"]) * sp["Kt"] * sp["Kh"] * sp["Kw"]
+    n_out = sp["N"] * sp["Co"] * To * Ho * Wo + sp["N"] * sp["Ci"] * L * hw
+    return es * (n_in + n_w + sp["Co"] * sp["has_bias"] + n_out)
 
 
 def copy_calibration():
@@ -200,6 +245,38 @@ def copy_calibration():
     torch.cuda.synchronize()
     print(json.dumps({"copy_calibration_bytes_each_way": a.numel() * 2, "launches": 3}),
           flush=True)
+
+
+def gemm_reference():
+    """bf16 GEMM rates of the vendor library (torch.matmul -> hipBLASLt) on
+    this device: two square problems, and the plain GEMMs with the shapes of
+    the 720p layers as implicit GEMMs (M = output pixels of one frame times
+    T_o, K = 27 Ci, N = Co).  A reference for what the matrix cores reach at
+    this device's sustained clock; no part of this library."""
+    import torch
+    dev = torch.device("cuda", 0)
+    out = []
+    for (M, K, N) in ((8192, 8192, 8192), (16384, 16384, 16384),
+                      (4 * 704 * 1280, 27 * 160, 160), (4 * 352 * 640, 27 * 320, 160),
+                      (4 * 176 * 320, 27 * 320, 320), (4 * 44 * 80, 27 * 640, 640)):
+        a = torch.randn(M, K, device=dev, dtype=torch.bfloat16)
+        b = torch.randn(K, N, device=dev, dtype=torch.bfloat16)
+        iters = 3 if M * K * N > 2 ** 42 else 10
+        for _ in range(3):
+            c = a @ b
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(iters):
+            c = a @ b
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / iters
+        tf = 2.0 * M * K * N / (ms * 1e-3) / 1e12
+        out.append(dict(M=M, K=K, N=N, ms=round(ms, 4), tflops=round(tf, 1),
+                        frac_peak=round(tf / PEAK_BF16_TFLOPS, 4)))
+        del a, b, c
+    print(json.dumps({"gemm_reference": "torch.matmul bf16", "results": out}), flush=True)
 
 
 def kernel_source_sha256():
