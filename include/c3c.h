@@ -178,6 +178,31 @@ int c3c_flops(const c3c_conv_desc* d, double* flops);
 int c3c_route_query(const c3c_ctx* ctx, const c3c_conv_desc* d, int* route,
                     int* reason);
 
+/* ---------------------------------------------------------------- workspace */
+/* Split-K workspace.  A bf16 fast call whose output tiles cannot fill the
+ * device's compute units (few output frames at a low resolution, such as one
+ * new frame at 60x104) can split each tile's (tap, 32-channel chunk) stages
+ * -- the K dimension of the lowered GEMM, Eq. 2 summed over the active taps
+ * of Eq. 4 -- over several workgroups.  Each split writes fp32 partial sums
+ * to the workspace; a second kernel adds the splits in a fixed order, adds
+ * the bias once and rounds once (so results are deterministic).
+ *
+ * c3c_workspace_bytes: the bytes a call with this descriptor would use, 0
+ * when it would run unsplit (large calls, non-bf16, or not routing fast).
+ * Depends on the current device's compute-unit count (256 is assumed when no
+ * device is visible).  EINVAL for an invalid descriptor or NULL bytes.
+ *
+ * c3c_ctx_set_workspace: attach a device buffer (caller-owned, 16-byte
+ * aligned) to the context; (NULL, 0) detaches.  A call splits only when the
+ * attached buffer holds at least c3c_workspace_bytes; otherwise it runs
+ * unsplit, with the same results up to summation order.  The buffer must not
+ * overlap any tensor of a call (EINVAL at the call), and calls that share a
+ * context must not run concurrently on different streams while they use it.
+ * EINVAL on NULL ctx, a NULL buffer with nonzero bytes (or the reverse), or a
+ * misaligned buffer. */
+int c3c_workspace_bytes(const c3c_conv_desc* d, size_t* bytes);
+int c3c_ctx_set_workspace(c3c_ctx* ctx, void* ws, size_t bytes);
+
 /* ---------------------------------------------------------------- weights */
 /* Size in bytes of the packed fast-route weights for this layer (the paper's
  * derived per-tap weight slices, Alg. 1, kept as one matrix-core-ready copy).

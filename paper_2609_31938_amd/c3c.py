@@ -67,6 +67,8 @@ lib.c3c_tap_interval.argtypes = [_P(Desc), _i64, _P(_i64), _P(_i64)]
 lib.c3c_flops.argtypes = [_P(Desc), _P(C.c_double)]
 lib.c3c_route_query.argtypes = [_vp, _P(Desc), _P(C.c_int), _P(C.c_int)]
 lib.c3c_weight_pack_bytes.argtypes = [_P(Desc), _P(C.c_size_t)]
+lib.c3c_workspace_bytes.argtypes = [_P(Desc), _P(C.c_size_t)]
+lib.c3c_ctx_set_workspace.argtypes = [_vp, _vp, C.c_size_t]
 lib.c3c_weight_repack.argtypes = [_vp, _P(Desc), _vp, _vp, _vp]
 lib.c3c_weight_unpack.argtypes = [_P(Desc), _vp, _vp, _vp]
 lib.c3c_conv3d_causal_cached.argtypes = [_vp, _P(Desc), _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp]
@@ -163,6 +165,20 @@ class Context:
     def last_error(self) -> str:
         return lib.c3c_last_error(self._h).decode()
 
+    def set_workspace(self, ws=None):
+        """Attach a device tensor as the split-K workspace (None detaches).
+        The context keeps a reference so the memory outlives its use."""
+        if ws is None:
+            _raise(lib.c3c_ctx_set_workspace(self._h, None, 0), self, "c3c_ctx_set_workspace")
+            self._ws = None
+            return
+        if not ws.is_cuda or not ws.is_contiguous():
+            raise ValueError("workspace must be a contiguous device tensor")
+        nbytes = ws.numel() * ws.element_size()
+        _raise(lib.c3c_ctx_set_workspace(self._h, ws.data_ptr() or None, nbytes), self,
+               "c3c_ctx_set_workspace")
+        self._ws = ws
+
 
 # ---------------------------------------------------------------- host maths
 
@@ -198,6 +214,14 @@ def weight_pack_bytes(spec: dict, dtype: str) -> int:
     n = C.c_size_t()
     _raise(lib.c3c_weight_pack_bytes(C.byref(make_desc(spec, dtype)), C.byref(n)),
            what="c3c_weight_pack_bytes")
+    return int(n.value)
+
+
+def workspace_bytes(spec: dict, dtype: str) -> int:
+    """Split-K workspace bytes this call would use (0: it runs unsplit)."""
+    n = C.c_size_t()
+    _raise(lib.c3c_workspace_bytes(C.byref(make_desc(spec, dtype)), C.byref(n)),
+           what="c3c_workspace_bytes")
     return int(n.value)
 
 

@@ -20,6 +20,8 @@ struct c3c_ctx {
   c3c_counters ctr{};
   std::vector<c3c_sig_count> shapes;
   std::string last_error;
+  void* ws = nullptr;      // caller's split-K workspace (device memory)
+  size_t ws_bytes = 0;
 };
 
 namespace c3c {
@@ -240,6 +242,23 @@ int c3c_route_query(const c3c_ctx* ctx, const c3c_conv_desc* d, int* route, int*
   return C3C_OK;
 }
 
+int c3c_workspace_bytes(const c3c_conv_desc* d, size_t* bytes) {
+  Geo g;
+  if (*make_geo(d, &g) || !bytes) return C3C_E_INVAL;
+  *bytes = 0;
+  if (decide(g, 0u) == C3C_REASON_NONE && d->dtype == C3C_DTYPE_BF16)
+    *bytes = static_cast<size_t>(fast_bf16_workspace_bytes(g));
+  return C3C_OK;
+}
+
+int c3c_ctx_set_workspace(c3c_ctx* ctx, void* ws, size_t bytes) {
+  if (!ctx || (ws == nullptr) != (bytes == 0)) return C3C_E_INVAL;
+  if ((reinterpret_cast<uintptr_t>(ws) & 15u) != 0) return C3C_E_INVAL;
+  ctx->ws = ws;
+  ctx->ws_bytes = bytes;
+  return C3C_OK;
+}
+
 int c3c_weight_pack_bytes(const c3c_conv_desc* d, size_t* bytes) {
   Geo g;
   if (*make_geo(d, &g) || !bytes) return C3C_E_INVAL;
@@ -311,6 +330,11 @@ int c3c_conv3d_causal_cached(c3c_ctx* ctx, const c3c_conv_desc* d, const void* x
   if (overlap(y, yb, x, xb) || overlap(y, yb, cache, cb) || overlap(y, yb, w, wb) ||
       overlap(y, yb, bias, bb) || overlap(y, yb, cache_out, ob))
     return fail(ctx, C3C_E_INVAL, "y overlaps another tensor");
+  const int64_t wsb = static_cast<int64_t>(ctx->ws_bytes);
+  if (overlap(ctx->ws, wsb, x, xb) || overlap(ctx->ws, wsb, cache, cb) ||
+      overlap(ctx->ws, wsb, w, wb) || overlap(ctx->ws, wsb, bias, bb) ||
+      overlap(ctx->ws, wsb, y, yb) || overlap(ctx->ws, wsb, cache_out, ob))
+    return fail(ctx, C3C_E_INVAL, "the context's workspace overlaps a tensor");
 
   const int reason = decide(g, ctx->mode);
   size_t pb = 0;
@@ -318,8 +342,9 @@ int c3c_conv3d_causal_cached(c3c_ctx* ctx, const c3c_conv_desc* d, const void* x
     c3c_weight_pack_bytes(d, &pb);
     if (!wpack) return fail(ctx, C3C_E_INVAL, "wpack is NULL on a call that routes fast");
     if (overlap(y, yb, wpack, static_cast<int64_t>(pb)) ||
-        overlap(cache_out, ob, wpack, static_cast<int64_t>(pb)))
-      return fail(ctx, C3C_E_INVAL, "an output overlaps wpack");
+        overlap(cache_out, ob, wpack, static_cast<int64_t>(pb)) ||
+        overlap(ctx->ws, wsb, wpack, static_cast<int64_t>(pb)))
+      return fail(ctx, C3C_E_INVAL, "an output or the workspace overlaps wpack");
   }
 
   hipStream_t s = static_cast<hipStream_t>(stream);
@@ -336,7 +361,8 @@ int c3c_conv3d_causal_cached(c3c_ctx* ctx, const c3c_conv_desc* d, const void* x
       }
       e = hipErrorLaunchFailure;  // stands for a failure before any launch
     } else {
-      e = launch_fast(g, x, cache, wpack, bias, y, cache_out, s);
+      e = launch_fast(g, x, cache, wpack, bias, y, cache_out, ctx->ws,
+                      static_cast<int64_t>(ctx->ws_bytes), s);
     }
     if (e == hipSuccess) {
       ++ctx->ctr.fast;

@@ -41,13 +41,19 @@ PackDims pack_dims(const c3c_conv_desc& d);
 
 hipError_t launch_repack(const Geo& g, const void* w, void* wpack, hipStream_t s);
 hipError_t launch_unpack(const Geo& g, const void* wpack, void* w, hipStream_t s);
+// ws / ws_bytes: the caller's split-K workspace (may be NULL / 0).
 hipError_t launch_fast(const Geo& g, const void* x, const void* cache, const void* wpack,
-                       const void* bias, void* y, void* cache_out, hipStream_t s);
+                       const void* bias, void* y, void* cache_out, void* ws, int64_t ws_bytes,
+                       hipStream_t s);
 // bf16 fast kernel (conv_bf16.hip); writes cache_out itself when it can
-// (returns *cache_written = true), else the caller copies the cache.
+// (returns *cache_written = true), else the caller copies the cache.  Splits
+// the stages of a call too small to fill the device over several workgroups
+// when ws holds at least fast_bf16_workspace_bytes(g) bytes (16-byte aligned).
 hipError_t launch_fast_bf16(const Geo& g, const void* x, const void* cache, const void* wpack,
-                            const void* bias, void* y, void* cache_out, bool* cache_written,
-                            hipStream_t s);
+                            const void* bias, void* y, void* cache_out, void* ws,
+                            int64_t ws_bytes, bool* cache_written, hipStream_t s);
+// fp32 partial-sum bytes a bf16 fast call would split into (0: it runs unsplit)
+int64_t fast_bf16_workspace_bytes(const Geo& g);
 // fallback, pointwise case (pointwise.hip): 1x1x1, unit spatial stride, no
 // spatial padding, one group, bf16 / fp16, aligned buffers
 bool pointwise_eligible(const Geo& g, const void* x, const void* cache, const void* w, const void* y);

@@ -75,6 +75,11 @@ struct Args {
   int nblocks;
   int has_bias;
   int write_cache;
+  // split-K: with splits > 1, workgroup split sp runs stages [sp nst / splits,
+  // (sp + 1) nst / splits) of its tile and writes fp32 partial sums (no bias)
+  // to part[sp][n][co][o][h][w]; splitk_reduce then adds them and the bias
+  int splits;
+  float* part;
 };
 
 // 8 channel rows of 8 pixels (v[c] = pixels 0..7 of channel c) -> 8 pixel
@@ -123,7 +128,7 @@ __global__ __launch_bounds__(64 * WAVES_CO * WAVES_PX, 1) void conv3d_bf16(Args 
   const int wco = wave % WAVES_CO, wpx = wave / WAVES_CO;
 
   // ---- workgroup -> tile, XCD-contiguous
-  int o, tw, th, n, ct;
+  int o, tw, th, n, ct, sp;
   {
     const int b = blockIdx.x;
     const int per = a.nblocks / 8, rem = a.nblocks % 8;
@@ -136,7 +141,9 @@ __global__ __launch_bounds__(64 * WAVES_CO * WAVES_PX, 1) void conv3d_bf16(Args 
     th = L % a.tiles_h;
     L /= a.tiles_h;
     n = L % a.N;
-    ct = L / a.N;
+    L /= a.N;
+    ct = L % a.tiles_co;
+    sp = L / a.tiles_co;
   }
   const int h0 = th * BH, w0 = tw * BW;
 
@@ -150,6 +157,9 @@ __global__ __launch_bounds__(64 * WAVES_CO * WAVES_PX, 1) void conv3d_bf16(Args 
   // chunk of a frame close together in time, so the re-reads hit in L2.
   const int ntap = k_hi >= k_lo ? k_hi - k_lo + 1 : 0;
   const int nst = ntap * a.chunks;
+  // this workgroup's share of the stages (all of them unless split-K)
+  const int s_lo = (sp * nst) / a.splits, s_hi = ((sp + 1) * nst) / a.splits;
+  const int cnt = s_hi - s_lo;
   constexpr uint32_t OOB = 0x80000000u;  // beyond every resource's size
 
   // One stage = (active tap k, 32-channel chunk c0).  Its activations are read
@@ -358,15 +368,15 @@ __global__ __launch_bounds__(64 * WAVES_CO * WAVES_PX, 1) void conv3d_bf16(Args 
 
   u32x4 av[NPF];
   // (tap index, chunk) of the next stage, advanced incrementally
-  int nk = 0, nc = 0;
+  int nk = ntap > 0 ? s_lo % ntap : 0, nc = ntap > 0 ? s_lo / ntap : 0;
   auto advance = [&]() {
     if (++nk == ntap) {
       nk = 0;
       ++nc;
     }
   };
-  Stage cst = stage_at(0, 0);
-  if (nst > 0) {
+  Stage cst = stage_at(nk, nc);
+  if (cnt > 0) {
     load_w(cst.wbase, 0, wr[0]);
     load_w(cst.wbase, 1, wr[1]);
     for (int part = 0; part < 5; ++part) load_stage(cst, part);
@@ -386,7 +396,7 @@ __global__ __launch_bounds__(64 * WAVES_CO * WAVES_PX, 1) void conv3d_bf16(Args 
   // keeping them unconditional keeps the step one basic block that the
   // explicit interleave can schedule.
   int cur = 0;
-  for (int s = 0; s < nst; ++s) {
+  for (int s = 0; s < cnt; ++s) {
     advance();
     const Stage nst_ = stage_at(nk, nc);
     const int nxt = cur + 1 == NBUF ? 0 : cur + 1;
@@ -396,7 +406,7 @@ __global__ __launch_bounds__(64 * WAVES_CO * WAVES_PX, 1) void conv3d_bf16(Args 
     for (int ij = 0; ij < 9; ++ij) {
       // the cache write (rare, workgroup-uniform) is its own block ahead of
       // the scheduled region of step 7
-      if (ij == 7 && cache_needed(nst_, s + 1 < nst)) cache_store(nst_);
+      if (ij == 7 && cache_needed(nst_, s + 1 < cnt)) cache_store(nst_);
       // keep every LDS read inside its own step: re-reading is cheaper in
       // registers than keeping overlapping rows of neighbouring kh live
       asm volatile("" ::: "memory");
@@ -448,8 +458,31 @@ __global__ __launch_bounds__(64 * WAVES_CO * WAVES_PX, 1) void conv3d_bf16(Args 
   // ---- epilogue: bias once, round to bf16, NCTHW store.  With the
   // activations as the A operand, lane l holds output channel l % 16 for the
   // four consecutive pixels 4 * (l / 16) .. + 3 of each fragment: one 8-byte
-  // store per fragment.
+  // store per fragment.  Under split-K the fp32 sums go to the partial
+  // buffer instead (one 16-byte store per fragment), without the bias.
   const int64_t plane = static_cast<int64_t>(a.To) * a.hw;
+  if (a.splits > 1) {
+    float* pbase = a.part + (static_cast<int64_t>(sp) * a.N + n) * a.Co * plane +
+                   static_cast<int64_t>(o) * a.hw;
+#pragma unroll
+    for (int cf = 0; cf < WCO; ++cf) {
+      const int co = (cofrag0 + cf) * 16 + (lane & 15);
+#pragma unroll
+      for (int pf = 0; pf < NPF; ++pf) {
+        const int h = h0 + wpx * WR + pf / WCF, w = w0 + (pf % WCF) * 16 + 4 * (lane >> 4);
+        if (co >= a.Co || h >= a.H || w >= a.W) continue;
+        float* dst = pbase + co * plane + static_cast<int64_t>(h) * a.W + w;
+        if (ALIGNED && w + 4 <= a.W) {
+          *reinterpret_cast<f32x4*>(dst) = acc[cf][pf];
+        } else {
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            if (w + r < a.W) dst[r] = acc[cf][pf][r];
+        }
+      }
+    }
+    return;
+  }
   uint16_t* ybase = a.y + (static_cast<int64_t>(n) * a.Co) * plane + static_cast<int64_t>(o) * a.hw;
 #pragma unroll
   for (int cf = 0; cf < WCO; ++cf) {
@@ -478,13 +511,64 @@ __global__ __launch_bounds__(64 * WAVES_CO * WAVES_PX, 1) void conv3d_bf16(Args 
   }
 }
 
+// Split-K reduction: y = bf16(sum of the splits' partial sums + bias), each
+// element summed in split order (deterministic), the bias added once, one
+// round-to-nearest-even.  Four consecutive elements of one output-channel
+// plane per thread when the plane length is a multiple of 4.
+template <bool VEC4>
+__global__ __launch_bounds__(256) void splitk_reduce(const float* __restrict__ part,
+                                                     const uint16_t* __restrict__ bias,
+                                                     uint16_t* __restrict__ y, int64_t total,
+                                                     int64_t plane, int Co, int splits,
+                                                     int has_bias) {
+  constexpr int V = VEC4 ? 4 : 1;
+  for (int64_t i = (static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x) * V; i < total;
+       i += static_cast<int64_t>(gridDim.x) * 256 * V) {
+    const int co = static_cast<int>((i / plane) % Co);
+    const float bb = has_bias ? __uint_as_float(static_cast<uint32_t>(bias[co]) << 16) : 0.f;
+    if constexpr (VEC4) {
+      f32x4 v = *reinterpret_cast<const f32x4*>(part + i);
+      for (int s = 1; s < splits; ++s)
+        v += *reinterpret_cast<const f32x4*>(part + static_cast<int64_t>(s) * total + i);
+      const uint32_t v01 = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2{v[0] + bb, v[1] + bb}), bf16x2));
+      const uint32_t v23 = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2{v[2] + bb, v[3] + bb}), bf16x2));
+      *reinterpret_cast<uint2*>(y + i) = make_uint2(v01, v23);
+    } else {
+      float v = part[i];
+      for (int s = 1; s < splits; ++s) v += part[static_cast<int64_t>(s) * total + i];
+      const uint32_t r = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2{v + bb, 0.f}), bf16x2));
+      y[i] = static_cast<uint16_t>(r);
+    }
+  }
+}
+
+// Tile configurations of the bf16 kernel (template arguments of run()).
+enum Cfg { CFG_C192, CFG_C96, CFG_C160_4X80, CFG_C160_10X32 };
+
+// Launch plan of one bf16 fast call: tile configuration, workgroups of one
+// split, split-K factor, and the fp32 partial-sum bytes the split needs.
+struct Plan {
+  Cfg cfg;
+  int64_t tiles_co, tiles_w, tiles_h, blocks;
+  int64_t tile_flop_px;  // output channels x pixels of one tile
+  int splits;
+  int64_t part_bytes;
+};
+
+void set_tiles(const Geo& g, int64_t bco, int64_t bh, int64_t bw, Plan* p) {
+  p->tiles_co = (g.d.Co + bco - 1) / bco;
+  p->tiles_w = (g.Wo + bw - 1) / bw;
+  p->tiles_h = (g.Ho + bh - 1) / bh;
+  p->blocks = p->tiles_co * p->tiles_w * p->tiles_h * g.To * g.d.N;
+  p->tile_flop_px = bco * bh * bw;
+}
+
 template <int WCO, int WR, int WCF, int WAVES_CO, int WAVES_PX, int NBUF>
-hipError_t run(const Geo& g, Args a, bool aligned, hipStream_t s) {
-  constexpr int BCO = 16 * WCO * WAVES_CO, BH = WR * WAVES_PX, BW = 16 * WCF;
-  a.tiles_co = static_cast<int>((g.d.Co + BCO - 1) / BCO);
-  a.tiles_w = static_cast<int>((g.Wo + BW - 1) / BW);
-  a.tiles_h = static_cast<int>((g.Ho + BH - 1) / BH);
-  const int64_t blocks = static_cast<int64_t>(a.tiles_co) * a.tiles_w * a.tiles_h * g.To * g.d.N;
+hipError_t run(const Geo& g, Args a, const Plan& p, bool aligned, hipStream_t s) {
+  a.tiles_co = static_cast<int>(p.tiles_co);
+  a.tiles_w = static_cast<int>(p.tiles_w);
+  a.tiles_h = static_cast<int>(p.tiles_h);
+  const int64_t blocks = p.blocks * a.splits;
   if (blocks == 0) return hipSuccess;
   if (blocks > 0x7fffffff) return hipErrorInvalidConfiguration;
   a.nblocks = static_cast<int>(blocks);
@@ -493,6 +577,18 @@ hipError_t run(const Geo& g, Args a, bool aligned, hipStream_t s) {
     hipLaunchKernelGGL((conv3d_bf16<WCO, WR, WCF, WAVES_CO, WAVES_PX, NBUF, true>), grid, block, 0, s, a);
   else
     hipLaunchKernelGGL((conv3d_bf16<WCO, WR, WCF, WAVES_CO, WAVES_PX, NBUF, false>), grid, block, 0, s, a);
+  if (a.splits == 1) return hipGetLastError();
+  const int64_t plane = static_cast<int64_t>(a.To) * a.hw;
+  const int64_t total = static_cast<int64_t>(a.N) * a.Co * plane;
+  const bool vec4 = plane % 4 == 0 && (reinterpret_cast<uintptr_t>(a.y) & 7u) == 0;
+  int64_t rb = (total / (vec4 ? 4 : 1) + 255) / 256;
+  if (rb > 65536) rb = 65536;
+  if (vec4)
+    hipLaunchKernelGGL(splitk_reduce<true>, dim3(static_cast<unsigned>(rb)), dim3(256), 0, s, a.part,
+                       a.bias, a.y, total, plane, a.Co, a.splits, a.has_bias);
+  else
+    hipLaunchKernelGGL(splitk_reduce<false>, dim3(static_cast<unsigned>(rb)), dim3(256), 0, s, a.part,
+                       a.bias, a.y, total, plane, a.Co, a.splits, a.has_bias);
   return hipGetLastError();
 }
 
@@ -526,11 +622,77 @@ int64_t compute_units() {
   return n;
 }
 
+
+// The tile configuration by output-channel count, and the split-K factor: a
+// call whose workgroups fill less than one round of the compute units splits
+// each tile's stages over S workgroups when the modelled time (microseconds)
+//   rounds(blocks * S) * (stages per split + 3) * t_stage
+//   + (S > 1) * (2 * S * output elements * 4 B / 5 TB/s + 5)
+// is lower than unsplit.  t_stage is one stage's FLOP (2 * 288 * tile) at
+// 6.9 TFLOP/s per compute unit, the measured main-loop rate; 3 stages stand
+// for a workgroup's fixed cost; the last term is the fp32 partial sums
+// written and read back, and the reduction launch.
+Plan plan_bf16(const Geo& g) {
+  Plan p;
+  const int64_t Co = g.d.Co;
+  const int64_t cus = compute_units();
+  if (Co > 128 && Co % 192 == 0) {
+    p.cfg = CFG_C192;
+    set_tiles(g, 192, 4, 64, &p);
+  } else if (Co <= 96) {
+    p.cfg = CFG_C96;
+    set_tiles(g, 96, 8, 64, &p);
+  } else {
+    // 160-channel tiles of 4 x 80 or 10 x 32 pixels.  A workgroup of either
+    // shape takes about the same time (measured), so the shape with fewer
+    // rounds of workgroups over the device's compute units wins; on a tie,
+    // 4 x 80 (half the halo-column loads).
+    Plan q;
+    set_tiles(g, 160, 4, 80, &p);
+    set_tiles(g, 160, 10, 32, &q);
+    if ((p.blocks + cus - 1) / cus <= (q.blocks + cus - 1) / cus) {
+      p.cfg = CFG_C160_4X80;
+    } else {
+      p = q;
+      p.cfg = CFG_C160_10X32;
+    }
+  }
+  p.splits = 1;
+  p.part_bytes = 0;
+  if (p.blocks > 0 && p.blocks < cus) {
+    int64_t ntap = 0;  // most active taps of any output frame (Eq. 4)
+    for (int64_t o = 0; o < g.To; ++o) {
+      int64_t n = 0;
+      for (int64_t k = 0; k < g.d.Kt; ++k) {
+        const int64_t f = o + k * g.d.dil_t - g.p_l;
+        n += f >= 0 && f < g.Z;
+      }
+      ntap = n > ntap ? n : ntap;
+    }
+    const int64_t nst = ntap * ((g.d.Ci + BKC - 1) / BKC);
+    const double t_stage = 2.0 * 9 * BKC * static_cast<double>(p.tile_flop_px) / 6.9e6;
+    const double out_elems = static_cast<double>(g.d.N * Co * g.To * g.Ho * g.Wo);
+    auto cost = [&](int64_t S) {
+      const double rounds = static_cast<double>((p.blocks * S + cus - 1) / cus);
+      return rounds * static_cast<double>((nst + S - 1) / S + 3) * t_stage +
+             (S > 1 ? 2.0 * static_cast<double>(S) * out_elems * 4.0 / 5e6 + 5.0 : 0.0);
+    };
+    int64_t best = 1;
+    for (int64_t S = 2; S <= 8; ++S)
+      if (nst / S >= 4 && cost(S) < cost(best)) best = S;
+    p.splits = static_cast<int>(best);
+    if (best > 1) p.part_bytes = best * g.d.N * Co * g.To * g.Ho * g.Wo * 4;
+  }
+  return p;
+}
+
 }  // namespace
 
+int64_t fast_bf16_workspace_bytes(const Geo& g) { return plan_bf16(g).part_bytes; }
+
 hipError_t launch_fast_bf16(const Geo& g, const void* x, const void* cache, const void* wpack,
-                            const void* bias, void* y, void* cache_out, bool* cache_written,
-                            hipStream_t s) {
+                            const void* bias, void* y, void* cache_out, void* ws,
+                            int64_t ws_bytes, bool* cache_written, hipStream_t s) {
   const PackDims p = pack_dims(g.d);
   Args a;
   a.x = static_cast<const uint16_t*>(x);
@@ -568,21 +730,18 @@ hipError_t launch_fast_bf16(const Geo& g, const void* x, const void* cache, cons
   const bool aligned = (g.d.W % 8 == 0) && (x == nullptr || aligned16(x)) &&
                        (cache == nullptr || aligned16(cache)) &&
                        (cache_out == nullptr || aligned16(cache_out));
-  const int64_t Co = g.d.Co;
-  if (Co > 128 && Co % 192 == 0) return run<6, 2, 4, 2, 2, 3>(g, a, aligned, s);
-  if (Co <= 96) return run<6, 2, 4, 1, 4, 2>(g, a, aligned, s);
-  // 160-channel tiles of 4 x 80 or 10 x 32 pixels.  A workgroup of either
-  // shape takes about the same time (measured), so the shape with fewer
-  // rounds of workgroups over the device's compute units wins; on a tie,
-  // 4 x 80 (half the halo-column loads).
-  const int64_t cus = compute_units();
-  auto rounds = [&](int64_t bh, int64_t bw) {
-    const int64_t blocks = (Co + 159) / 160 * ((g.Wo + bw - 1) / bw) * ((g.Ho + bh - 1) / bh) *
-                           g.To * g.d.N;
-    return (blocks + cus - 1) / cus;
-  };
-  if (rounds(4, 80) <= rounds(10, 32)) return run<5, 2, 5, 2, 2, 3>(g, a, aligned, s);
-  return run<5, 5, 2, 2, 2, 3>(g, a, aligned, s);
+  const Plan pl = plan_bf16(g);
+  // split-K only with a large enough, 16-byte-aligned workspace; else unsplit
+  const bool split = pl.splits > 1 && ws != nullptr && ws_bytes >= pl.part_bytes &&
+                     (reinterpret_cast<uintptr_t>(ws) & 15u) == 0;
+  a.splits = split ? pl.splits : 1;
+  a.part = split ? static_cast<float*>(ws) : nullptr;
+  switch (pl.cfg) {
+    case CFG_C192: return run<6, 2, 4, 2, 2, 3>(g, a, pl, aligned, s);
+    case CFG_C96: return run<6, 2, 4, 1, 4, 2>(g, a, pl, aligned, s);
+    case CFG_C160_4X80: return run<5, 2, 5, 2, 2, 3>(g, a, pl, aligned, s);
+    default: return run<5, 5, 2, 2, 2, 3>(g, a, pl, aligned, s);
+  }
 }
 
 }  // namespace c3c

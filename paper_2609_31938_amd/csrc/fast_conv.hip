@@ -300,7 +300,8 @@ hipError_t launch_unpack(const Geo& g, const void* wpack, void* w, hipStream_t s
 }
 
 hipError_t launch_fast(const Geo& g, const void* x, const void* cache, const void* wpack,
-                       const void* bias, void* y, void* cache_out, hipStream_t s) {
+                       const void* bias, void* y, void* cache_out, void* ws, int64_t ws_bytes,
+                       hipStream_t s) {
   const PackDims p = pack_dims(g.d);
   FastArgs a;
   a.x = x; a.cache = cache; a.wpack = wpack; a.bias = bias; a.y = y;
@@ -311,7 +312,8 @@ hipError_t launch_fast(const Geo& g, const void* x, const void* cache, const voi
   a.tiles_co = a.tiles_w = a.tiles_h = 0;
   if (g.d.dtype == C3C_DTYPE_BF16) {
     bool written = false;
-    const hipError_t e = launch_fast_bf16(g, x, cache, wpack, bias, y, cache_out, &written, s);
+    const hipError_t e =
+        launch_fast_bf16(g, x, cache, wpack, bias, y, cache_out, ws, ws_bytes, &written, s);
     if (e != hipSuccess || written) return e;
     return launch_cache_copy(g, x, cache, cache_out, s);
   }

@@ -32,7 +32,8 @@ def test_every_declared_symbol_is_exported():
         "c3c_output_dims", "c3c_tap_interval", "c3c_flops", "c3c_route_query",
         "c3c_weight_pack_bytes", "c3c_weight_repack", "c3c_weight_unpack",
         "c3c_conv3d_causal_cached", "c3c_counters_get", "c3c_counters_reset",
-        "c3c_fallback_shapes", "c3c_strerror", "c3c_last_error"])
+        "c3c_fallback_shapes", "c3c_strerror", "c3c_last_error",
+        "c3c_workspace_bytes", "c3c_ctx_set_workspace"])
     for n in names:
         assert hasattr(c3c.lib, n), n
 
@@ -178,4 +179,58 @@ def test_strict_mode_rejects_without_device_work():
     assert c["fast"] == c["fallback"] == 0
     assert ctx.fallback_shapes() == []
     ctx.reset()
+    assert ctx.counters()["calls"] == 0
+
+
+# ---------------------------------------------------------------------------
+# split-K workspace (host side)
+# ---------------------------------------------------------------------------
+
+@no_gpu
+def test_workspace_bytes_of_the_workloads():
+    """With 256 compute units (what the library assumes without a device),
+    only the 60x104 single-frame layer splits (60 workgroups of 36 stages,
+    into 4 splits of fp32 partial sums the size of the output).  The 44x80
+    640-channel layer (176 workgroups) would spend more on moving its large
+    partial sums than it gains, and stays unsplit."""
+    from paper_2609_31938_amd.inputs import WORKLOADS
+    got = {}
+    for name, wl in WORKLOADS.items():
+        for lname, sp in wl["layers"]:
+            got[lname] = c3c.workspace_bytes(sp, wl["dtype"])
+    assert got["c384_60x104"] == 4 * 384 * 1 * 60 * 104 * 4
+    for lname, v in got.items():
+        if lname != "c384_60x104":
+            assert v == 0, lname
+
+
+def test_workspace_bytes_only_for_fast_bf16():
+    sp = spec(N=1, Ci=384, Co=384, T=1, Tc=2, H=60, W=104)
+    assert c3c.workspace_bytes(sp, "f32") == 0
+    assert c3c.workspace_bytes(sp, "f16") == 0
+    assert c3c.workspace_bytes(dict(sp, groups=2), "bf16") == 0
+    n = C.c_size_t()
+    assert c3c.lib.c3c_workspace_bytes(None, C.byref(n)) == c3c.E_INVAL
+    assert c3c.lib.c3c_workspace_bytes(C.byref(c3c.make_desc(sp, "bf16")), None) == c3c.E_INVAL
+
+
+def test_set_workspace_arguments():
+    ctx = c3c.Context()
+    f = c3c.lib.c3c_ctx_set_workspace
+    assert f(None, 0x10000000, 1024) == c3c.E_INVAL
+    assert f(ctx._h, None, 1024) == c3c.E_INVAL
+    assert f(ctx._h, 0x10000000, 0) == c3c.E_INVAL
+    assert f(ctx._h, 0x10000008, 1024) == c3c.E_INVAL      # not 16-byte aligned
+    assert f(ctx._h, 0x10000000, 1024) == c3c.OK
+    assert f(ctx._h, None, 0) == c3c.OK                     # detach
+
+
+@no_gpu
+def test_workspace_overlapping_a_tensor_is_rejected():
+    sp = spec(N=1, Ci=4, Co=4, T=2, Tc=2, H=8, W=8)
+    ctx = c3c.Context()
+    for name in ("x", "cache", "w", "wpack", "b", "y", "co"):
+        assert c3c.lib.c3c_ctx_set_workspace(ctx._h, FAKE[name] - 16, 4096) == c3c.OK
+        assert _call(ctx, sp) == c3c.E_INVAL, name
+        assert "workspace" in ctx.last_error
     assert ctx.counters()["calls"] == 0
