@@ -174,10 +174,11 @@ def main():
     achieved = dom["gflop"] * 1e9 / (dom_mean_ms * 1e-3) / 1e12
     peak = PEAK_BF16_TFLOPS if dtype == "bf16" else PEAK_F32_TFLOPS
     if dom["route"] == "fast":
+        kname = "conv3d_bf16" if layers[dom_i]["sp"]["Kh"] == 3 else "pointwise_conv (1x1 spatial)"
         roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak,
                     "unit": "TFLOP/s", "frac": round(achieved / peak, 4),
-                    "traffic": measured_traffic(dom["layer"]),
-                    "kernel": f"conv3d_bf16 (fast route), layer {dom['layer']}"}
+                    "traffic": measured_traffic(dom["layer"]) if kname == "conv3d_bf16" else None,
+                    "kernel": f"{kname} (fast route), layer {dom['layer']}"}
     else:
         # a fallback layer timed alone (--layer): HBM-bound, algorithmic bytes
         gbs = algorithmic_bytes(layers[dom_i]["sp"], dtype) / (dom_mean_ms * 1e-3) / 1e9

@@ -83,19 +83,24 @@ enum {
 typedef enum c3c_route { C3C_ROUTE_FAST = 0, C3C_ROUTE_FALLBACK = 1 } c3c_route;
 
 /* Why a call does not route fast: the first failing clause, tested in this
- * order.  Clauses 2-7 are the paper's guard (Alg. 1); 8-9 state what the
- * fast kernel is specialised for. */
+ * order.  Clauses 2-7 are the paper's guard (Alg. 1), except that clause 4
+ * is widened: a 1x1 spatial kernel (a temporal convolution) is accepted at
+ * any temporal stride.  Clauses 8-9 state what the fast kernels are
+ * specialised for: the 3x3 form (stride 1, pad 1, dilation 1) of the
+ * decoder's main convolutions and the 1x1 form (stride 1, pad 0) of its
+ * temporal convolutions. */
 typedef enum c3c_reason {
   C3C_REASON_NONE = 0,      /* routes fast                                   */
   C3C_REASON_FORCED = 1,    /* C3C_MODE_FORCE_FALLBACK                       */
   C3C_REASON_DTYPE = 2,     /* dtype has no fast kernel (f16)                */
   C3C_REASON_GROUPS = 3,    /* groups != 1                                   */
-  C3C_REASON_STRIDE_T = 4,  /* temporal stride != 1                          */
+  C3C_REASON_STRIDE_T = 4,  /* temporal stride != 1, spatial kernel not 1x1 */
   C3C_REASON_PAD_RIGHT = 5, /* pad_t_right < 0                               */
   C3C_REASON_NO_OUTPUT = 6, /* To < 1                                        */
-  C3C_REASON_NO_TAP = 7,    /* no temporal tap has a nonempty Eq. 4 interval */
+  C3C_REASON_NO_TAP = 7,    /* no (output frame, tap) pair reads a frame of Z */
   C3C_REASON_KT1 = 8,       /* Kt < 2 (e.g. a 1x1x1 shortcut conv)           */
-  C3C_REASON_SPATIAL = 9,   /* spatial kernel is not 3x3, stride 1, pad 1, dil 1 */
+  C3C_REASON_SPATIAL = 9,   /* spatial kernel is neither 3x3 (stride 1, pad 1,
+                               dil 1) nor 1x1 (stride 1, pad 0)              */
   /* not a predicate clause: the call routed fast, the fast route failed and
    * the call fell back (appears only in the fallback-shape histogram) */
   C3C_REASON_FAST_ERROR = 10
@@ -225,7 +230,8 @@ int c3c_weight_unpack(const c3c_conv_desc* d, const void* wpack, void* w_out,
  *
  * Fast route: one kernel launch evaluates every active tap into fp32
  * registers, adds the bias once, rounds to `dtype` (nearest even), stores
- * NCTHW, and writes cache_out.  It reads wpack (required, from
+ * NCTHW, and writes cache_out (3x3 kernels write it in the same launch; 1x1
+ * kernels and fp32 calls copy it with a second kernel).  It reads wpack (required, from
  * c3c_weight_repack on the same w); w itself is not read.
  * Fallback route: the direct-Conv3D kernel reads w (wpack may be NULL), then a
  * copy kernel writes cache_out.

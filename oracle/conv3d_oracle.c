@@ -32,8 +32,11 @@
  * with brute-force enumeration.
  *
  * The route rule (which calls the lowered fast route accepts) is the written
- * guard of Alg. 1 plus two clauses of this library's fast-kernel contract
- * (K_t >= 2, and a 3x3 / stride 1 / pad 1 / dilation 1 spatial kernel).
+ * guard of Alg. 1 plus this library's fast-kernel contract: K_t >= 2, and
+ * one of two spatial forms, 3x3 / stride 1 / pad 1 / dilation 1 or 1x1 /
+ * stride 1 / pad 0.  The guard's unit-temporal-stride clause is kept for the
+ * 3x3 form; the 1x1 form (a temporal convolution, one matrix product per
+ * output frame and tap) also accepts other temporal strides.
  */
 #include <math.h>
 #include <stdint.h>
@@ -133,6 +136,10 @@ int ora_route(const ora_desc* d, int dtype_ok, int force_fallback, int* route,
               int* reason) {
   int64_t To;
   if (ora_output_dims(d, &To, NULL, NULL, NULL)) return -1;
+  const int k3x3 = d->Kh == 3 && d->Kw == 3 && d->s_h == 1 && d->s_w == 1 &&
+                   d->p_h == 1 && d->p_w == 1 && d->d_h == 1 && d->d_w == 1;
+  const int k1x1 = d->Kh == 1 && d->Kw == 1 && d->s_h == 1 && d->s_w == 1 &&
+                   d->p_h == 0 && d->p_w == 0 && d->d_h == 1 && d->d_w == 1;
   int r = ORA_OK;
   if (force_fallback)
     r = ORA_FORCED;
@@ -140,25 +147,34 @@ int ora_route(const ora_desc* d, int dtype_ok, int force_fallback, int* route,
     r = ORA_DTYPE;
   else if (d->groups != 1)
     r = ORA_GROUPS;
-  else if (d->s_t != 1)
+  else if (d->s_t != 1 && !k1x1)
     r = ORA_STRIDE_T;
   else if (d->p_r < 0)
     r = ORA_PAD_RIGHT;
   else if (To < 1)
     r = ORA_NO_OUTPUT;
   else {
+    /* some (output frame, tap) pair reads a frame of Z: Eq. 4 with unit
+     * stride, the source time t s_t + k d_t - p_l counted out otherwise */
+    const int64_t Z = d->Tc + d->T, p_l = d->p_base - d->Tc;
     int any = 0;
     for (int64_t k = 0; k < d->Kt; ++k) {
-      int64_t lo, hi;
-      ora_tap_interval(d, k, &lo, &hi);
-      if (lo < hi) any = 1;
+      if (d->s_t == 1) {
+        int64_t lo, hi;
+        ora_tap_interval(d, k, &lo, &hi);
+        if (lo < hi) any = 1;
+      } else {
+        for (int64_t t = 0; t < To; ++t) {
+          const int64_t f = t * d->s_t + k * d->d_t - p_l;
+          if (f >= 0 && f < Z) any = 1;
+        }
+      }
     }
     if (!any)
       r = ORA_NO_TAP;
     else if (d->Kt < 2)
       r = ORA_KT1;
-    else if (!(d->Kh == 3 && d->Kw == 3 && d->s_h == 1 && d->s_w == 1 &&
-               d->p_h == 1 && d->p_w == 1 && d->d_h == 1 && d->d_w == 1))
+    else if (!k3x3 && !k1x1)
       r = ORA_SPATIAL;
   }
   *route = (r == ORA_OK) ? 0 : 1;

@@ -117,20 +117,31 @@ bool any_active_tap(const Geo& g) {
   return false;
 }
 
-// The route predicate: the first failing clause is the reason.
+// The two spatial forms of the fast route: 3x3 with stride 1, pad 1,
+// dilation 1 (the decoder's main convolutions), and 1x1 with stride 1, pad 0
+// (its temporal convolutions, per-frame matrix products).
+bool spatial_3x3(const c3c_conv_desc& d) {
+  return d.Kh == 3 && d.Kw == 3 && d.stride_h == 1 && d.stride_w == 1 && d.pad_h == 1 &&
+         d.pad_w == 1 && d.dil_h == 1 && d.dil_w == 1;
+}
+bool spatial_1x1(const c3c_conv_desc& d) {
+  return d.Kh == 1 && d.Kw == 1 && d.stride_h == 1 && d.stride_w == 1 && d.pad_h == 0 &&
+         d.pad_w == 0 && d.dil_h == 1 && d.dil_w == 1;
+}
+
+// The route predicate: the first failing clause is the reason.  Temporal
+// stride other than 1 is accepted for the 1x1 spatial form only.
 int decide(const Geo& g, uint32_t mode) {
   const c3c_conv_desc& d = g.d;
   if (mode & C3C_MODE_FORCE_FALLBACK) return C3C_REASON_FORCED;
   if (d.dtype != C3C_DTYPE_BF16 && d.dtype != C3C_DTYPE_F32) return C3C_REASON_DTYPE;
   if (d.groups != 1) return C3C_REASON_GROUPS;
-  if (d.stride_t != 1) return C3C_REASON_STRIDE_T;
+  if (d.stride_t != 1 && !spatial_1x1(d)) return C3C_REASON_STRIDE_T;
   if (d.pad_t_right < 0) return C3C_REASON_PAD_RIGHT;
   if (g.To < 1) return C3C_REASON_NO_OUTPUT;
   if (!any_active_tap(g)) return C3C_REASON_NO_TAP;
   if (d.Kt < 2) return C3C_REASON_KT1;
-  if (!(d.Kh == 3 && d.Kw == 3 && d.stride_h == 1 && d.stride_w == 1 && d.pad_h == 1 &&
-        d.pad_w == 1 && d.dil_h == 1 && d.dil_w == 1))
-    return C3C_REASON_SPATIAL;
+  if (!spatial_3x3(d) && !spatial_1x1(d)) return C3C_REASON_SPATIAL;
   return C3C_REASON_NONE;
 }
 
@@ -246,7 +257,7 @@ int c3c_workspace_bytes(const c3c_conv_desc* d, size_t* bytes) {
   Geo g;
   if (*make_geo(d, &g) || !bytes) return C3C_E_INVAL;
   *bytes = 0;
-  if (decide(g, 0u) == C3C_REASON_NONE && d->dtype == C3C_DTYPE_BF16)
+  if (decide(g, 0u) == C3C_REASON_NONE && d->dtype == C3C_DTYPE_BF16 && spatial_3x3(*d))
     *bytes = static_cast<size_t>(fast_bf16_workspace_bytes(g));
   return C3C_OK;
 }

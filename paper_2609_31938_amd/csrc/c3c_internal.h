@@ -59,6 +59,12 @@ int64_t fast_bf16_workspace_bytes(const Geo& g);
 bool pointwise_eligible(const Geo& g, const void* x, const void* cache, const void* w, const void* y);
 hipError_t launch_pointwise(const Geo& g, const void* x, const void* cache, const void* w,
                             const void* bias, void* y, hipStream_t s);
+// fast route, bf16, 1x1 spatial kernel (pointwise.hip): every active temporal
+// tap of a call as per-frame matrix products, reading the packed weights; any
+// temporal stride and dilation, any H * W and alignment.  The caller copies
+// the cache.
+hipError_t launch_fast_tap1x1(const Geo& g, const void* x, const void* cache, const void* wpack,
+                              const void* bias, void* y, hipStream_t s);
 hipError_t launch_fallback(const Geo& g, const void* x, const void* cache, const void* w,
                            const void* bias, void* y, hipStream_t s);
 hipError_t launch_cache_copy(const Geo& g, const void* x, const void* cache, void* cache_out,

@@ -19,9 +19,11 @@
 // GEMM view per output frame: D[co][px] = sum_K A[co][K] * B[K][px] with
 // K = (tap kt, kh, kw, input channel).  A (weights) comes pre-packed in
 // matrix-core fragment order; B (activations) is staged through LDS as a halo
-// tile [BH+2][BW+2][channels], channel-innermost, so that each lane reads its
-// K-contiguous operand with one LDS load and the nine spatial offsets of a
-// 3x3 kernel are nine address shifts into the same tile.
+// tile [BH+KS-1][BW+KS-1][channels], channel-innermost, so that each lane
+// reads its K-contiguous operand with one LDS load and the KS x KS spatial
+// offsets (a 3x3 kernel with pad 1, or 1x1) are address shifts into the same
+// tile.  Source frame of tap k for output frame o: o s_t + k d_t - p_l (the
+// temporal stride is 1 for 3x3 kernels).
 #include "c3c_internal.h"
 
 namespace c3c {
@@ -125,7 +127,7 @@ struct FastArgs {
   const void* bias;
   void* y;
   int64_t Ci, Co, T, Tc, H, W;
-  int64_t Kt, dt, p_l, Z, To;
+  int64_t Kt, dt, st, p_l, Z, To;
   int64_t chunks, cofrags;
   int tiles_co, tiles_w, tiles_h;
   int has_bias;
@@ -134,13 +136,14 @@ struct FastArgs {
 // Workgroup tile: BCO = 32 * CO_FRAGS * WAVES_CO output channels by
 // BH rows x (32 * BWF) columns of one output frame.  Wave (wco, wpx) owns
 // CO_FRAGS x PX_FRAGS 32x32 accumulator fragments.
-template <typename T, int CO_FRAGS, int PX_FRAGS, int WAVES_CO, int WAVES_PX, int BH, int BWF>
+template <typename T, int CO_FRAGS, int PX_FRAGS, int WAVES_CO, int WAVES_PX, int BH, int BWF, int KS>
 __global__ __launch_bounds__(64 * WAVES_CO * WAVES_PX) void fast_conv3d(FastArgs a) {
   using M = Mma<T>;
   static_assert(WAVES_PX * PX_FRAGS == BH * BWF, "pixel fragments must tile the block");
   constexpr int NT = 64 * WAVES_CO * WAVES_PX;
   constexpr int BW = 32 * BWF;
-  constexpr int TW = BW + 2, TH = BH + 2;  // halo tile for a 3x3 kernel, pad 1
+  constexpr int TW = BW + KS - 1, TH = BH + KS - 1;  // halo tile, pad (KS - 1) / 2
+  constexpr int PAD = (KS - 1) / 2;
   constexpr int BKC = M::BKC, PIXS = M::PIXS, KSTEP = M::KSTEP, KPL = M::KPL;
   __shared__ __align__(16) T tile[TH * TW * PIXS];
 
@@ -175,7 +178,7 @@ __global__ __launch_bounds__(64 * WAVES_CO * WAVES_PX) void fast_conv3d(FastArgs
 
   for (int64_t k = 0; k < a.Kt; ++k) {
     // Eq. 4: tap k is active for this frame iff its source frame lies in Z.
-    const int64_t f = o + k * a.dt - a.p_l;
+    const int64_t f = o * a.st + k * a.dt - a.p_l;
     if (f < 0 || f >= a.Z) continue;
     const T* src;
     int64_t cstride;
@@ -191,7 +194,7 @@ __global__ __launch_bounds__(64 * WAVES_CO * WAVES_PX) void fast_conv3d(FastArgs
       // stage the halo tile: rows h0-1 .. h0+BH, cols w0-1 .. w0+BW, BKC channels
       for (int e = tid; e < BKC * TH * TW; e += NT) {
         const int cc = e % TW, rr = (e / TW) % TH, ch = e / (TW * TH);
-        const int gh = h0 - 1 + rr, gw = w0 - 1 + cc;
+        const int gh = h0 - PAD + rr, gw = w0 - PAD + cc;
         T v = T(0);
         if (c0 + ch < a.Ci && gh >= 0 && gh < a.H && gw >= 0 && gw < a.W)
           v = src[(c0 + ch) * cstride + static_cast<int64_t>(gh) * a.W + gw];
@@ -199,9 +202,9 @@ __global__ __launch_bounds__(64 * WAVES_CO * WAVES_PX) void fast_conv3d(FastArgs
       }
       __syncthreads();
 #pragma unroll 1
-      for (int ij = 0; ij < 9; ++ij) {
-        const int ki = ij / 3, kj = ij % 3;
-        const int64_t tap = k * 9 + ij;
+      for (int ij = 0; ij < KS * KS; ++ij) {
+        const int ki = ij / KS, kj = ij % KS;
+        const int64_t tap = k * KS * KS + ij;
 #pragma unroll
         for (int ks = 0; ks < BKC / KSTEP; ++ks) {
           const int64_t chunk = c0 / KSTEP + ks;
@@ -251,7 +254,7 @@ __global__ __launch_bounds__(64 * WAVES_CO * WAVES_PX) void fast_conv3d(FastArgs
   }
 }
 
-template <typename T, int CO_FRAGS, int PX_FRAGS, int WAVES_CO, int WAVES_PX, int BH, int BWF>
+template <typename T, int CO_FRAGS, int PX_FRAGS, int WAVES_CO, int WAVES_PX, int BH, int BWF, int KS>
 hipError_t run_fast(const Geo& g, FastArgs a, hipStream_t s) {
   constexpr int BCO = 32 * CO_FRAGS * WAVES_CO, BW = 32 * BWF;
   a.tiles_co = static_cast<int>((g.d.Co + BCO - 1) / BCO);
@@ -260,7 +263,7 @@ hipError_t run_fast(const Geo& g, FastArgs a, hipStream_t s) {
   const int64_t blocks = static_cast<int64_t>(a.tiles_co) * a.tiles_w * a.tiles_h * g.To * g.d.N;
   if (blocks == 0) return hipSuccess;
   if (blocks > 0x7fffffff) return hipErrorInvalidConfiguration;
-  hipLaunchKernelGGL((fast_conv3d<T, CO_FRAGS, PX_FRAGS, WAVES_CO, WAVES_PX, BH, BWF>),
+  hipLaunchKernelGGL((fast_conv3d<T, CO_FRAGS, PX_FRAGS, WAVES_CO, WAVES_PX, BH, BWF, KS>),
                      dim3(static_cast<unsigned>(blocks)), dim3(64 * WAVES_CO * WAVES_PX), 0, s, a);
   return hipGetLastError();
 }
@@ -306,18 +309,24 @@ hipError_t launch_fast(const Geo& g, const void* x, const void* cache, const voi
   FastArgs a;
   a.x = x; a.cache = cache; a.wpack = wpack; a.bias = bias; a.y = y;
   a.Ci = g.d.Ci; a.Co = g.d.Co; a.T = g.d.T; a.Tc = g.d.Tc; a.H = g.d.H; a.W = g.d.W;
-  a.Kt = g.d.Kt; a.dt = g.d.dil_t; a.p_l = g.p_l; a.Z = g.Z; a.To = g.To;
+  a.Kt = g.d.Kt; a.dt = g.d.dil_t; a.st = g.d.stride_t; a.p_l = g.p_l; a.Z = g.Z; a.To = g.To;
   a.chunks = p.chunks; a.cofrags = p.cofrags;
   a.has_bias = g.d.has_bias ? 1 : 0;
   a.tiles_co = a.tiles_w = a.tiles_h = 0;
+  // the fast route's two spatial forms: 3x3 / stride 1 / pad 1, and 1x1
+  const bool one = g.d.Kh == 1;
+  hipError_t e;
   if (g.d.dtype == C3C_DTYPE_BF16) {
-    bool written = false;
-    const hipError_t e =
-        launch_fast_bf16(g, x, cache, wpack, bias, y, cache_out, ws, ws_bytes, &written, s);
-    if (e != hipSuccess || written) return e;
-    return launch_cache_copy(g, x, cache, cache_out, s);
+    if (one) {
+      e = launch_fast_tap1x1(g, x, cache, wpack, bias, y, s);
+    } else {
+      bool written = false;
+      e = launch_fast_bf16(g, x, cache, wpack, bias, y, cache_out, ws, ws_bytes, &written, s);
+      if (e != hipSuccess || written) return e;
+    }
+  } else {
+    e = one ? run_fast<float, 1, 2, 1, 4, 4, 2, 1>(g, a, s) : run_fast<float, 1, 2, 1, 4, 4, 2, 3>(g, a, s);
   }
-  const hipError_t e = run_fast<float, 1, 2, 1, 4, 4, 2>(g, a, s);
   if (e != hipSuccess) return e;
   return launch_cache_copy(g, x, cache, cache_out, s);
 }

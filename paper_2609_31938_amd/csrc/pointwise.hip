@@ -1,22 +1,32 @@
-// Fallback route, pointwise case.  A 1x1x1 Conv3D (stride 1 and no padding in
-// H and W, one group) reads a single temporal tap: output frame t is, for each
-// batch element, the matrix product y[co][p] = sum_ci w[co][ci] z[ci][p] over
-// the pixels p of source frame f = t * s_t - p_l of [cache; x] (zero when f is
-// outside it), plus the bias once (the cached-conv definition, Eq. 1-2, with
-// Kt = Kh = Kw = 1).  bf16 / fp16 storage, matrix cores, fp32 accumulation.
+// Convolutions with a 1x1 spatial kernel (stride 1 and no padding in H and
+// W, one group) as per-frame matrix products on matrix cores: output frame t
+// is, for each batch element,
+//   y[co][p] = b[co] + sum_{k active} sum_ci w[co][ci][k] z[ci][f_k][p],
+//   f_k = t * s_t + k * d_t - p_l,
+// over the frames f_k of [cache; x] that exist (Eq. 2 with the source time of
+// Eq. 1 and the stride of Eq. 3; a tap whose frame lies outside Z contributes
+// nothing, Eq. 4).  bf16 / fp16 storage, fp32 accumulation, the bias once.
+// Two users:
+//   * the fast route, for temporal convolutions with a 1x1 spatial kernel
+//     (Kt >= 2, any temporal stride and dilation; bf16), reading the packed
+//     weights: fragment (tap k, chunk c, output fragment) is one 1 KiB block;
+//   * the fallback route, for 1x1x1 calls (bf16 / fp16), reading w[co][ci].
 //
 // Workgroup = 160 output channels x 256 consecutive pixels of one (n, t)
 // frame; eight waves of 80 channels x 64 pixels (each output row segment a
-// workgroup writes is 512 contiguous bytes).  Per 32-channel chunk the
-// activation tile [32 ch][256 px] is copied into LDS as it lies in memory
-// (pixels contiguous, as NCTHW stores them), and the transposing LDS read
-// ds_read_b64_tr_b16 turns it into the matrix-core operand (8 consecutive
-// channels of one pixel per lane).  The chunk's weights w[co][32 ch] are
-// staged beside it.  Chunks stream through a ring of PD register sets: the
-// global loads of chunk c + PD are issued while chunk c computes.  The chunk
-// count is padded to a multiple of PD with chunks that read zeros, so every
-// step of the loop is unconditional (the wait counts for the ring's loads
-// then stay exact instead of falling back to the worst case).
+// workgroup writes is 512 contiguous bytes).  One stage = one active tap and
+// one 32-channel chunk.  Its activation tile [32 ch][256 px] is copied into
+// LDS as it lies in memory (pixels contiguous, as NCTHW stores them), and the
+// transposing LDS read ds_read_b64_tr_b16 turns it into the matrix-core
+// operand (8 consecutive channels of one pixel per lane).  The stage's
+// weights are staged beside it.  Stages stream through a ring of PD register
+// sets: the global loads of stage s + PD are issued while stage s computes.
+// The stage count is padded to a multiple of PD with stages that read zeros,
+// so every step of the loop is unconditional (the wait counts for the ring's
+// loads then stay exact instead of falling back to the worst case).  Pixels
+// past the end of a frame plane are loaded (from the next plane, or as zeros
+// past the tensor) but only feed outputs that are never stored: a 1x1 kernel
+// maps each output pixel to the same input pixel.
 #include "c3c_internal.h"
 
 namespace c3c {
@@ -48,16 +58,18 @@ constexpr int PW_WOFF = PW_K * PW_PITCH;            // weights after the activat
 constexpr int PW_BUF = PW_WOFF + PW_CO * PW_WPITCH;
 constexpr int PW_WPIECES = PW_CO * PW_K * 2 / 16;    // 16-byte pieces of a weight chunk
 constexpr int PW_WPT = (PW_WPIECES + PW_NT - 1) / PW_NT;  // per thread
+static_assert(PW_CO * PW_K * 2 <= PW_CO * PW_WPITCH, "packed weights fit the weight area");
 
 struct PwArgs {
   const uint16_t* x;
   const uint16_t* cache;
-  const uint16_t* w;
+  const uint16_t* w;      // w[co][ci] (unpacked, Kt = 1) or the packed weights
   const uint16_t* bias;
   uint16_t* y;
   int64_t hw;
-  int N, Ci, Co, T, Tc, To, Z, st, p_l;
-  int chunks, px_tiles, co_tiles;
+  int N, Ci, Co, T, Tc, To, Z, st, dt, p_l, Kt;
+  int chunks, px_tiles, co_tiles, cofrags;
+  uint32_t w_bytes;
   int has_bias;
 };
 
@@ -85,7 +97,11 @@ __device__ inline f32x4 mma(i16x8 a, u32x4 b, f32x4 c) {
                                                    __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
 }
 
-template <bool F16, int PD>
+// PACKED: weights in matrix-core fragment order (fast route, bf16); else
+// w[co][ci] (fallback, Kt = 1).  ALIGNED: every channel plane starts on a
+// 16-byte boundary (H * W a multiple of 8, aligned pointers); else the
+// activations are read 2 bytes at a time and the outputs stored one by one.
+template <bool F16, int PD, bool PACKED, bool ALIGNED>
 __global__ __launch_bounds__(PW_NT, 1) void pointwise_conv(PwArgs a) {
   __shared__ __align__(16) unsigned char lds[2 * PW_BUF];
   constexpr uint32_t OOB = 0x80000000u;  // beyond every resource's size
@@ -109,62 +125,108 @@ __global__ __launch_bounds__(PW_NT, 1) void pointwise_conv(PwArgs a) {
   const int t = b % a.To;
   const int n = b / a.To;
   const int px0 = pt * PW_PX;
-  const int f = t * a.st - a.p_l;
-  const bool fok = f >= 0 && f < a.Z;
+  // active taps (Eq. 4): source frame t s_t + k d_t - p_l inside Z; the
+  // frame grows with k, so they form one range [k_lo, k_lo + ntap)
+  int k_lo = 0;
+  while (k_lo < a.Kt && t * a.st + k_lo * a.dt - a.p_l < 0) ++k_lo;
+  int k_hi = a.Kt - 1;
+  while (k_hi >= 0 && t * a.st + k_hi * a.dt - a.p_l >= a.Z) --k_hi;
+  const int ntap = k_hi >= k_lo ? k_hi - k_lo + 1 : 0;
+  const int nst = ntap * a.chunks;  // stages: tap outer, chunk inner
 
-  // source frame plane of channel 0 (pixel px0) and the channel-plane stride
-  const uint16_t* src;
-  int64_t cstride;
-  if (f < a.Tc) {
-    cstride = static_cast<int64_t>(a.Tc) * a.hw;
-    src = a.cache + static_cast<int64_t>(n) * a.Ci * cstride + static_cast<int64_t>(f) * a.hw + px0;
-  } else {
-    cstride = static_cast<int64_t>(a.T) * a.hw;
-    src = a.x + static_cast<int64_t>(n) * a.Ci * cstride + static_cast<int64_t>(f - a.Tc) * a.hw + px0;
-  }
-  const uint32_t cs = static_cast<uint32_t>(cstride * 2);
-  // chunk c's resource starts at channel 32c and ends after the last real
-  // channel's row of this frame: channels past Ci load as 0; a frame outside
-  // Z has an empty resource (the output is the bias alone)
-  auto chunk_rsrc = [&](int c) {
-    const int c0 = c * PW_K;
+  // the channel-plane strides of the cache and of the new chunk
+  const int64_t cs_c = static_cast<int64_t>(a.Tc) * a.hw, cs_x = static_cast<int64_t>(a.T) * a.hw;
+  // Stage s's resource starts at channel 32 c of its source frame (pixel
+  // px0) and ends after the last real channel's row of that frame: channels
+  // past Ci load as 0; a stage past the last has an empty resource.
+  struct StageSrc {
+    __amdgpu_buffer_rsrc_t rs;
+    uint32_t cs;
+  };
+  auto stage_src = [&](int st_) {
+    const bool real = st_ < nst;
+    const int k = k_lo + (real ? st_ / a.chunks : 0), c0 = (real ? st_ % a.chunks : 0) * PW_K;
+    const int f = real ? t * a.st + k * a.dt - a.p_l : 0;
+    const bool in_cache = f < a.Tc;
+    const int64_t cstride = in_cache ? cs_c : cs_x;
+    const uint16_t* base = in_cache ? a.cache : a.x;
+    const int64_t off = static_cast<int64_t>(in_cache ? f : f - a.Tc) * a.hw +
+                        static_cast<int64_t>(n) * a.Ci * cstride + px0 + c0 * cstride;
     int64_t bytes = ((a.Ci - 1 - c0) * cstride + a.hw - px0) * 2;
-    if (!fok || bytes < 0) bytes = 0;
+    if (!real || bytes < 0) bytes = 0;
     if (bytes > 0x7fffffff) bytes = 0x7fffffff;
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(src + (fok ? c0 * cstride : 0)), 0,
+    StageSrc r;
+    r.rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(real ? base + off : base), 0,
                                              static_cast<int>(bytes), 0x00020000);
+    r.cs = static_cast<uint32_t>(cstride * 2);
+    return r;
   };
 
   // staging: thread -> activation channel row tid / 16, pixels 8 (tid % 16)
-  // .. + 7 and 128 + 8 (tid % 16) .. + 7 (16 lanes read 256 contiguous bytes);
-  // weight pieces tid + 512 i -> row piece / 4, channels 8 (piece % 4) .. + 7
+  // .. + 7 and 128 + 8 (tid % 16) .. + 7 (16 lanes read 256 contiguous bytes)
   const int sch = tid >> 4, spx = (tid & 15) * 8;
-  const uint32_t soff = static_cast<uint32_t>(sch) * cs + static_cast<uint32_t>(spx) * 2u;
   const int slds = sch * PW_PITCH + spx * 2;
-  // rows past Co and channels past Ci are out-of-range offsets (zeros)
+  // Weights.  Unpacked: pieces tid + 512 i -> row piece / 4, channels
+  // 8 (piece % 4) .. + 7; rows past Co and channels past Ci are out-of-range
+  // offsets (zeros).  Packed: piece q = 16-byte lane slot q % 64 of output
+  // fragment q / 64 of the stage's (tap, chunk), fragments past the last
+  // clamped to it (they feed accumulators that are never stored); stored in
+  // LDS as whole fragments, 1 KiB each.
   const __amdgpu_buffer_rsrc_t wrs = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<uint16_t*>(a.w), 0, static_cast<int>(static_cast<int64_t>(a.Co) * a.Ci * 2), 0x00020000);
+      const_cast<uint16_t*>(a.w), 0, static_cast<int>(a.w_bytes), 0x00020000);
   int wrow[PW_WPT], wq[PW_WPT];
+  uint32_t wp_off[PW_WPT];
+  bool wp_ok[PW_WPT];
 #pragma unroll
   for (int i = 0; i < PW_WPT; ++i) {
     const int piece = tid + PW_NT * i;
     wrow[i] = piece >> 2;
     wq[i] = (piece & 3) * 8;
+    const int frag = min(ctile * (PW_CO / 16) + piece / 64, a.cofrags - 1);
+    wp_ok[i] = piece < (PW_CO / 16) * 64;
+    wp_off[i] = static_cast<uint32_t>(frag) * 1024u + static_cast<uint32_t>(piece % 64) * 16u;
   }
   struct Chunk {
     u32x4 x[2];
     u32x4 w[PW_WPT];
   };
-  auto load_chunk = [&](int c, Chunk& ck) {
-    const __amdgpu_buffer_rsrc_t rs = chunk_rsrc(c);
-    ck.x[0] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, soff, 0, 0));
-    ck.x[1] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, soff + 256u, 0, 0));
+  auto load_chunk = [&](int st_, Chunk& ck) {
+    const StageSrc sr = stage_src(st_);
+    const uint32_t soff = static_cast<uint32_t>(sch) * sr.cs + static_cast<uint32_t>(spx) * 2u;
+    if constexpr (ALIGNED) {
+      ck.x[0] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(sr.rs, soff, 0, 0));
+      ck.x[1] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(sr.rs, soff + 256u, 0, 0));
+    } else {
 #pragma unroll
-    for (int i = 0; i < PW_WPT; ++i) {
-      const int co = ctile * PW_CO + wrow[i], ci = c * PW_K + wq[i];
-      const bool ok = (wrow[i] < PW_CO) & (co < a.Co) & (ci < a.Ci);
-      ck.w[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
-                                              wrs, ok ? static_cast<uint32_t>(co * a.Ci + ci) * 2u : OOB, 0, 0));
+      for (int h = 0; h < 2; ++h) {
+        uint32_t wd[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const uint32_t o = soff + 256u * h + 4u * e;
+          const uint32_t lo = __builtin_amdgcn_raw_buffer_load_b16(sr.rs, o, 0, 0);
+          const uint32_t hi = __builtin_amdgcn_raw_buffer_load_b16(sr.rs, o + 2u, 0, 0);
+          wd[e] = (lo & 0xffffu) | (hi << 16);
+        }
+        ck.x[h] = u32x4{wd[0], wd[1], wd[2], wd[3]};
+      }
+    }
+    if constexpr (PACKED) {
+      // stage (tap k, chunk c): fragment row (k * chunks + c) of the packing
+      const int k = k_lo + (ntap > 0 ? st_ / a.chunks : 0), c = ntap > 0 ? st_ % a.chunks : 0;
+      const uint32_t row = static_cast<uint32_t>((k * a.chunks + c) * a.cofrags) * 1024u;
+#pragma unroll
+      for (int i = 0; i < PW_WPT; ++i)
+        ck.w[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                                                wrs, wp_ok[i] && st_ < nst ? row + wp_off[i] : OOB, 0, 0));
+    } else {
+      const int c = st_;
+#pragma unroll
+      for (int i = 0; i < PW_WPT; ++i) {
+        const int co = ctile * PW_CO + wrow[i], ci = c * PW_K + wq[i];
+        const bool ok = (wrow[i] < PW_CO) & (co < a.Co) & (ci < a.Ci);
+        ck.w[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                                                wrs, ok ? static_cast<uint32_t>(co * a.Ci + ci) * 2u : OOB, 0, 0));
+      }
     }
   };
   auto store_chunk = [&](const Chunk& ck, int buf) {
@@ -172,9 +234,15 @@ __global__ __launch_bounds__(PW_NT, 1) void pointwise_conv(PwArgs a) {
     *reinterpret_cast<u32x4*>(base + slds) = ck.x[0];
     *reinterpret_cast<u32x4*>(base + slds + 256) = ck.x[1];
 #pragma unroll
-    for (int i = 0; i < PW_WPT; ++i)
-      if (wrow[i] < PW_CO)
-        *reinterpret_cast<u32x4*>(base + PW_WOFF + wrow[i] * PW_WPITCH + wq[i] * 2) = ck.w[i];
+    for (int i = 0; i < PW_WPT; ++i) {
+      if constexpr (PACKED) {
+        const int piece = tid + PW_NT * i;
+        if (wp_ok[i]) *reinterpret_cast<u32x4*>(base + PW_WOFF + piece * 16) = ck.w[i];
+      } else {
+        if (wrow[i] < PW_CO)
+          *reinterpret_cast<u32x4*>(base + PW_WOFF + wrow[i] * PW_WPITCH + wq[i] * 2) = ck.w[i];
+      }
+    }
   };
 
   // transposing operand read: within each 16-lane block (channel group
@@ -190,10 +258,13 @@ __global__ __launch_bounds__(PW_NT, 1) void pointwise_conv(PwArgs a) {
     return i16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
   };
   // weight operand: lane l holds w[co = frag * 16 + l % 16][ci = 8 (l / 16) .. + 7]
+  // (unpacked rows of PW_WPITCH bytes, or the packed fragment's lane slot)
   const int cof0 = ctile * PW_CO + wco * 16 * PW_WCO + (lane & 15);
-  const int rb = PW_WOFF + (wco * 16 * PW_WCO + j) * PW_WPITCH + 16 * g;
+  const int rb = PACKED ? PW_WOFF + wco * PW_WCO * 1024 + lane * 16
+                        : PW_WOFF + (wco * 16 * PW_WCO + j) * PW_WPITCH + 16 * g;
   auto read_b = [&](int buf, int cf) {
-    return *reinterpret_cast<const u32x4*>(lds + buf * PW_BUF + rb + cf * 16 * PW_WPITCH);
+    return *reinterpret_cast<const u32x4*>(lds + buf * PW_BUF + rb +
+                                           cf * (PACKED ? 1024 : 16 * PW_WPITCH));
   };
 
   f32x4 acc[PW_WCO][PW_NPF];
@@ -205,7 +276,7 @@ __global__ __launch_bounds__(PW_NT, 1) void pointwise_conv(PwArgs a) {
   Chunk ring[PD];
 #pragma unroll
   for (int u = 0; u < PD; ++u) load_chunk(u, ring[u]);
-  const int padded = (a.chunks + PD - 1) / PD * PD;
+  const int padded = (nst + PD - 1) / PD * PD;
   for (int c0 = 0; c0 < padded; c0 += PD) {
 #pragma unroll
     for (int u = 0; u < PD; ++u) {
@@ -243,7 +314,7 @@ __global__ __launch_bounds__(PW_NT, 1) void pointwise_conv(PwArgs a) {
       uint16_t v[4];
 #pragma unroll
       for (int r = 0; r < 4; ++r) v[r] = F16 ? to_f16(acc[cf][pf][r] + bb) : to_bf16(acc[cf][pf][r] + bb);
-      if (p + 4 <= a.hw) {
+      if (ALIGNED && p + 4 <= a.hw) {
         *reinterpret_cast<uint2*>(yrow + p) = make_uint2(v[0] | (static_cast<uint32_t>(v[1]) << 16),
                                                         v[2] | (static_cast<uint32_t>(v[3]) << 16));
       } else {
@@ -277,13 +348,54 @@ bool pointwise_eligible(const Geo& g, const void* x, const void* cache, const vo
   return true;
 }
 
-hipError_t launch_pointwise(const Geo& g, const void* x, const void* cache, const void* w,
-                            const void* bias, void* y, hipStream_t s) {
+namespace {
+
+// one launch of pointwise_conv: the ring depth that pads the largest stage
+// count of any output frame least (4, 3 or 2), the template instance by
+// element type, weight layout and alignment
+template <bool PACKED>
+hipError_t launch_pw(const Geo& g, PwArgs a, bool f16, bool al, hipStream_t s) {
+  const c3c_conv_desc& d = g.d;
+  a.px_tiles = static_cast<int>((a.hw + PW_PX - 1) / PW_PX);
+  a.co_tiles = static_cast<int>((d.Co + PW_CO - 1) / PW_CO);
+  const int64_t blocks = static_cast<int64_t>(a.px_tiles) * a.co_tiles * g.To * d.N;
+  if (blocks == 0) return hipSuccess;
+  if (blocks > 0x7fffffff) return hipErrorInvalidConfiguration;
+  int ntap = 0;
+  for (int64_t t = 0; t < g.To; ++t) {
+    int nt = 0;
+    for (int64_t k = 0; k < d.Kt; ++k) {
+      const int64_t f = t * d.stride_t + k * d.dil_t - g.p_l;
+      nt += f >= 0 && f < g.Z;
+    }
+    ntap = nt > ntap ? nt : ntap;
+  }
+  const int nst = ntap * a.chunks;
+  int pd = 4;
+  for (int cand : {3, 2})
+    if ((nst + cand - 1) / cand * cand < (nst + pd - 1) / pd * pd) pd = cand;
+  const dim3 grid(static_cast<unsigned>(blocks)), block(PW_NT);
+#define C3C_PW(F, P, A)                                                                        \
+  if (f16 == F && pd == P && al == A) {                                                         \
+    hipLaunchKernelGGL((pointwise_conv<F, P, PACKED, A>), grid, block, 0, s, a);               \
+    return hipGetLastError();                                                                  \
+  }
+  if constexpr (PACKED) {  // fast route: bf16, any alignment
+    C3C_PW(false, 2, true) C3C_PW(false, 3, true) C3C_PW(false, 4, true)
+    C3C_PW(false, 2, false) C3C_PW(false, 3, false) C3C_PW(false, 4, false)
+  } else {  // fallback: bf16 / fp16, aligned (pointwise_eligible)
+    C3C_PW(false, 2, true) C3C_PW(false, 3, true) C3C_PW(false, 4, true)
+    C3C_PW(true, 2, true) C3C_PW(true, 3, true) C3C_PW(true, 4, true)
+  }
+#undef C3C_PW
+  return hipErrorInvalidValue;
+}
+
+PwArgs common_args(const Geo& g, const void* x, const void* cache, const void* bias, void* y) {
   const c3c_conv_desc& d = g.d;
   PwArgs a;
   a.x = static_cast<const uint16_t*>(x);
   a.cache = static_cast<const uint16_t*>(cache);
-  a.w = static_cast<const uint16_t*>(w);
   a.bias = static_cast<const uint16_t*>(bias);
   a.y = static_cast<uint16_t*>(y);
   a.hw = d.H * d.W;
@@ -295,31 +407,41 @@ hipError_t launch_pointwise(const Geo& g, const void* x, const void* cache, cons
   a.To = static_cast<int>(g.To);
   a.Z = static_cast<int>(g.Z);
   a.st = static_cast<int>(d.stride_t);
+  a.dt = static_cast<int>(d.dil_t);
   a.p_l = static_cast<int>(g.p_l);
+  a.Kt = static_cast<int>(d.Kt);
   a.chunks = static_cast<int>((d.Ci + PW_K - 1) / PW_K);
-  a.px_tiles = static_cast<int>((a.hw + PW_PX - 1) / PW_PX);
-  a.co_tiles = static_cast<int>((d.Co + PW_CO - 1) / PW_CO);
   a.has_bias = d.has_bias ? 1 : 0;
-  const int64_t blocks = static_cast<int64_t>(a.px_tiles) * a.co_tiles * g.To * d.N;
-  if (blocks == 0) return hipSuccess;
-  if (blocks > 0x7fffffff) return hipErrorInvalidConfiguration;
-  // ring depth: the one of 4, 3, 2 that pads the chunk count least
-  int pd = 4;
-  for (int cand : {3, 2})
-    if ((a.chunks + cand - 1) / cand * cand < (a.chunks + pd - 1) / pd * pd) pd = cand;
-  const dim3 grid(static_cast<unsigned>(blocks)), block(PW_NT);
-  const bool f16 = d.dtype == C3C_DTYPE_F16;
-  if (pd == 2) {
-    if (f16) hipLaunchKernelGGL((pointwise_conv<true, 2>), grid, block, 0, s, a);
-    else hipLaunchKernelGGL((pointwise_conv<false, 2>), grid, block, 0, s, a);
-  } else if (pd == 4) {
-    if (f16) hipLaunchKernelGGL((pointwise_conv<true, 4>), grid, block, 0, s, a);
-    else hipLaunchKernelGGL((pointwise_conv<false, 4>), grid, block, 0, s, a);
-  } else {
-    if (f16) hipLaunchKernelGGL((pointwise_conv<true, 3>), grid, block, 0, s, a);
-    else hipLaunchKernelGGL((pointwise_conv<false, 3>), grid, block, 0, s, a);
-  }
-  return hipGetLastError();
+  return a;
+}
+
+}  // namespace
+
+hipError_t launch_pointwise(const Geo& g, const void* x, const void* cache, const void* w,
+                            const void* bias, void* y, hipStream_t s) {
+  PwArgs a = common_args(g, x, cache, bias, y);
+  a.w = static_cast<const uint16_t*>(w);
+  a.w_bytes = static_cast<uint32_t>(g.d.Co * g.d.Ci * 2);
+  a.cofrags = 0;
+  return launch_pw<false>(g, a, g.d.dtype == C3C_DTYPE_F16, true, s);
+}
+
+hipError_t launch_fast_tap1x1(const Geo& g, const void* x, const void* cache, const void* wpack,
+                              const void* bias, void* y, hipStream_t s) {
+  const c3c_conv_desc& d = g.d;
+  const PackDims p = pack_dims(d);
+  // 32-bit buffer offsets: one 32-channel chunk of a source frame and the
+  // packed weights must each span less than 2 GiB
+  const int64_t frames = d.T > d.Tc ? d.T : d.Tc;
+  if (static_cast<int64_t>(PW_K) * frames * d.H * d.W * 2 >= 0x7fffffff || p.elems() * 2 >= 0x7fffffff)
+    return hipErrorInvalidValue;
+  PwArgs a = common_args(g, x, cache, bias, y);
+  a.w = static_cast<const uint16_t*>(wpack);
+  a.w_bytes = static_cast<uint32_t>(p.elems() * 2);
+  a.cofrags = static_cast<int>(p.cofrags);
+  const bool al = (d.H * d.W) % 8 == 0 && aligned(x, 16) && (cache == nullptr || aligned(cache, 16)) &&
+                  aligned(y, 8);
+  return launch_pw<true>(g, a, false, al, s);
 }
 
 }  // namespace c3c

@@ -129,4 +129,15 @@ WORKLOADS = {
                                ("shortcut_1x1x1_320to160_352x640",
                                 spec(N=1, Ci=320, Co=160, T=4, Tc=0, H=352, W=640,
                                      Kt=1, Kh=1, Kw=1))]),
+    # 6: temporal convolutions (kernel 3x1x1) of the decoder's temporal
+    # upsampling (channels doubled, then split into two frames by the
+    # decoder) and of an encoder's stride-2 temporal downsampling
+    "temporal": dict(id=6, dtype="bf16", chunks=5,
+                     layers=[("tconv_up_384to768_60x104",
+                              spec(N=1, Ci=384, Co=768, T=1, Tc=2, H=60, W=104, Kh=1, Kw=1)),
+                             ("tconv_up_384to768_120x208",
+                              spec(N=1, Ci=384, Co=768, T=2, Tc=2, H=120, W=208, Kh=1, Kw=1)),
+                             ("tconv_down_s2_384_120x208",
+                              spec(N=1, Ci=384, Co=384, T=8, Tc=1, H=120, W=208, Kh=1, Kw=1,
+                                   s_t=2, p_base=1))]),
 }

@@ -85,6 +85,17 @@ FAST_CASES = [
     ("f32", dict(N=1, Ci=32, Co=32, T=2, Tc=2, H=32, W=32)),
     ("f32", dict(N=2, Ci=7, Co=45, T=3, Tc=1, H=13, W=34)),
     ("f32", dict(N=1, Ci=33, Co=70, T=1, Tc=2, H=10, W=66)),
+    # 1x1 spatial kernels (temporal convolutions): per-frame matrix products
+    ("bf16", dict(N=1, Ci=96, Co=192, T=4, Tc=2, H=16, W=40, Kh=1, Kw=1)),
+    ("bf16", dict(N=2, Ci=40, Co=200, T=3, Tc=2, H=9, W=24, Kh=1, Kw=1)),    # chunk tail, 2 co tiles
+    ("bf16", dict(N=1, Ci=33, Co=17, T=5, Tc=2, H=5, W=7, Kh=1, Kw=1)),      # H*W = 35: unaligned
+    ("bf16", dict(N=1, Ci=64, Co=64, T=6, Tc=0, H=8, W=16, Kh=1, Kw=1, s_t=2)),  # stride 2
+    ("bf16", dict(N=1, Ci=32, Co=48, T=4, Tc=4, H=8, W=8, Kh=1, Kw=1, d_t=2, p_base=4)),
+    ("bf16", dict(N=1, Ci=16, Co=32, T=2, Tc=0, H=4, W=64, Kt=2, Kh=1, Kw=1)),
+    ("bf16", dict(N=1, Ci=24, Co=40, T=3, Tc=2, H=6, W=20, Kh=1, Kw=1, p_r=1)),
+    ("bf16", dict(N=1, Ci=300, Co=70, T=5, Tc=1, H=3, W=37, Kh=1, Kw=1, s_t=3, p_base=2)),
+    ("f32", dict(N=1, Ci=20, Co=40, T=3, Tc=2, H=10, W=12, Kh=1, Kw=1)),
+    ("f32", dict(N=1, Ci=8, Co=8, T=5, Tc=0, H=6, W=6, Kh=1, Kw=1, s_t=2)),
 ]
 
 

@@ -100,3 +100,12 @@ def test_stack_720p():
     shapes = ctx.fallback_shapes()
     assert len(shapes) == 1 and shapes[0][0] == "kt1" and shapes[0][2] == 5
     assert shapes[0][1]["Kt"] == 1 and shapes[0][1]["Ci"] == 320 and shapes[0][1]["Co"] == 160
+
+
+def test_temporal_convs():
+    """Temporal convolutions (kernel 3x1x1) on the fast route: the 1x1-spatial
+    kernel, unit stride with a 2-frame cache and stride 2 with a 1-frame
+    cache, streamed over 5 chunks."""
+    ctx = _stream("temporal", check_chunks=[0, 1, -1])
+    c = ctx.counters()
+    assert (c["calls"], c["fast"], c["fallback"]) == (15, 15, 0)

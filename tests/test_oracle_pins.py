@@ -438,6 +438,19 @@ ROUTE_TABLE = [
     (dict(Kt=2, p_base=1, Tc=1), "bf16", False, "none"),
     (dict(T=0, Tc=0, Kt=1, Kh=3, p_base=2), "bf16", False, "no_tap"),  # |Z| = 0
     (dict(T=1, Tc=0, Kt=2, d_t=2, p_base=1, p_r=1), "bf16", False, "no_tap"),  # straddle
+    # the 1x1 spatial form (temporal convolutions), at any temporal stride
+    (dict(Kh=1, Kw=1, p_h=0, p_w=0), "bf16", False, "none"),
+    (dict(Kh=1, Kw=1, p_h=0, p_w=0), "f32", False, "none"),
+    (dict(Kh=1, Kw=1, p_h=0, p_w=0, T=6, Tc=0, s_t=2), "bf16", False, "none"),
+    (dict(Kh=1, Kw=1, p_h=0, p_w=0, T=6, Tc=0, s_t=3), "f32", False, "none"),
+    (dict(Kh=1, Kw=1, p_h=0, p_w=0), "f16", False, "dtype"),
+    (dict(Kh=1, Kw=1, p_h=0, p_w=0, s_h=2), "bf16", False, "spatial"),
+    (dict(Kh=1, Kw=1, p_h=0, p_w=0, d_w=2), "bf16", False, "spatial"),
+    (dict(Kh=1, Kw=3, p_h=0, p_w=1), "bf16", False, "spatial"),
+    (dict(Kh=1, Kw=1, p_h=0, p_w=0, s_t=2, s_w=2), "bf16", False, "stride_t"),
+    (dict(Kt=1, Kh=1, Kw=1, p_h=0, p_w=0, p_base=0, Tc=0, s_t=2), "bf16", False, "kt1"),
+    (dict(Kh=1, Kw=1, p_h=0, p_w=0, T=1, Tc=0, Kt=2, d_t=2, p_base=1, p_r=1, s_t=2),
+     "bf16", False, "no_tap"),
 ]
 
 
@@ -448,6 +461,30 @@ def test_route_rule_table(over, dtype, forced, reason):
     r, why = oracle.route(sp, dtype, forced)
     assert why == reason
     assert r == ("fast" if reason == "none" else "fallback")
+
+
+def test_no_tap_clause_matches_enumeration_at_any_stride():
+    # the 1x1 spatial form passes the stride clause at any temporal stride, so
+    # the "no active tap" clause is reached with s_t > 1 too: it must fire
+    # exactly when no (output frame, tap) pair t s_t + k d_t - p_l lands in Z
+    rng = np.random.default_rng(62)
+    seen = fired = 0
+    for _ in range(3000):
+        sp = _random_spec(rng)
+        sp.update(Kh=1, Kw=1, p_h=0, p_w=0, s_h=1, s_w=1, d_h=1, d_w=1, groups=1,
+                  s_t=int(rng.integers(2, 4)))
+        sp["p_r"] = abs(sp["p_r"])
+        To, _, _, _ = oracle.output_dims(sp)
+        if To < 1:
+            continue
+        _, why = oracle.route(sp, "bf16")
+        p_l = sp["p_base"] - sp["Tc"]
+        hit = any(0 <= t * sp["s_t"] + k * sp["d_t"] - p_l < sp["Tc"] + sp["T"]
+                  for t in range(To) for k in range(sp["Kt"]))
+        assert (why == "no_tap") == (not hit), sp
+        seen += 1
+        fired += not hit
+    assert seen > 1000 and fired > 0
 
 
 def test_no_tap_clause_matches_enumeration():
