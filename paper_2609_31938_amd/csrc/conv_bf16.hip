@@ -100,7 +100,10 @@ __device__ inline void transpose8x8(const u32x4 (&v)[8], u32x4 (&o)[8]) {
 // buffers: with 3, the barrier that publishes the next stage's tile sits
 // inside the current stage, so the first operand reads of the next stage
 // overlap the current stage's last matrix-core step.
-template <int WCO, int WR, int WCF, int WAVES_CO, int WAVES_PX, int NBUF, bool ALIGNED>
+// SPLIT: the split-K instance (a stage range per workgroup, fp32 partial
+// sums out); a separate instance so that the unsplit kernel's register
+// allocation is not shaped by the split epilogue.
+template <int WCO, int WR, int WCF, int WAVES_CO, int WAVES_PX, int NBUF, bool ALIGNED, bool SPLIT>
 __global__ __launch_bounds__(64 * WAVES_CO * WAVES_PX, 1) void conv3d_bf16(Args a) {
   constexpr int NT = 64 * WAVES_CO * WAVES_PX;
   constexpr int BH = WR * WAVES_PX, BW = 16 * WCF;
@@ -142,8 +145,8 @@ __global__ __launch_bounds__(64 * WAVES_CO * WAVES_PX, 1) void conv3d_bf16(Args 
     L /= a.tiles_h;
     n = L % a.N;
     L /= a.N;
-    ct = L % a.tiles_co;
-    sp = L / a.tiles_co;
+    ct = SPLIT ? L % a.tiles_co : L;
+    sp = SPLIT ? L / a.tiles_co : 0;
   }
   const int h0 = th * BH, w0 = tw * BW;
 
@@ -158,7 +161,8 @@ __global__ __launch_bounds__(64 * WAVES_CO * WAVES_PX, 1) void conv3d_bf16(Args 
   const int ntap = k_hi >= k_lo ? k_hi - k_lo + 1 : 0;
   const int nst = ntap * a.chunks;
   // this workgroup's share of the stages (all of them unless split-K)
-  const int s_lo = (sp * nst) / a.splits, s_hi = ((sp + 1) * nst) / a.splits;
+  const int s_lo = SPLIT ? (sp * nst) / a.splits : 0;
+  const int s_hi = SPLIT ? ((sp + 1) * nst) / a.splits : nst;
   const int cnt = s_hi - s_lo;
   constexpr uint32_t OOB = 0x80000000u;  // beyond every resource's size
 
@@ -368,7 +372,7 @@ __global__ __launch_bounds__(64 * WAVES_CO * WAVES_PX, 1) void conv3d_bf16(Args 
 
   u32x4 av[NPF];
   // (tap index, chunk) of the next stage, advanced incrementally
-  int nk = ntap > 0 ? s_lo % ntap : 0, nc = ntap > 0 ? s_lo / ntap : 0;
+  int nk = SPLIT && ntap > 0 ? s_lo % ntap : 0, nc = SPLIT && ntap > 0 ? s_lo / ntap : 0;
   auto advance = [&]() {
     if (++nk == ntap) {
       nk = 0;
@@ -461,7 +465,7 @@ __global__ __launch_bounds__(64 * WAVES_CO * WAVES_PX, 1) void conv3d_bf16(Args 
   // store per fragment.  Under split-K the fp32 sums go to the partial
   // buffer instead (one 16-byte store per fragment), without the bias.
   const int64_t plane = static_cast<int64_t>(a.To) * a.hw;
-  if (a.splits > 1) {
+  if constexpr (SPLIT) {
     float* pbase = a.part + (static_cast<int64_t>(sp) * a.N + n) * a.Co * plane +
                    static_cast<int64_t>(o) * a.hw;
 #pragma unroll
@@ -573,11 +577,16 @@ hipError_t run(const Geo& g, Args a, const Plan& p, bool aligned, hipStream_t s)
   if (blocks > 0x7fffffff) return hipErrorInvalidConfiguration;
   a.nblocks = static_cast<int>(blocks);
   const dim3 grid(static_cast<unsigned>(blocks)), block(64 * WAVES_CO * WAVES_PX);
-  if (aligned)
-    hipLaunchKernelGGL((conv3d_bf16<WCO, WR, WCF, WAVES_CO, WAVES_PX, NBUF, true>), grid, block, 0, s, a);
+  const bool split = a.splits > 1;
+  if (aligned && !split)
+    hipLaunchKernelGGL((conv3d_bf16<WCO, WR, WCF, WAVES_CO, WAVES_PX, NBUF, true, false>), grid, block, 0, s, a);
+  else if (!split)
+    hipLaunchKernelGGL((conv3d_bf16<WCO, WR, WCF, WAVES_CO, WAVES_PX, NBUF, false, false>), grid, block, 0, s, a);
+  else if (aligned)
+    hipLaunchKernelGGL((conv3d_bf16<WCO, WR, WCF, WAVES_CO, WAVES_PX, NBUF, true, true>), grid, block, 0, s, a);
   else
-    hipLaunchKernelGGL((conv3d_bf16<WCO, WR, WCF, WAVES_CO, WAVES_PX, NBUF, false>), grid, block, 0, s, a);
-  if (a.splits == 1) return hipGetLastError();
+    hipLaunchKernelGGL((conv3d_bf16<WCO, WR, WCF, WAVES_CO, WAVES_PX, NBUF, false, true>), grid, block, 0, s, a);
+  if (!split) return hipGetLastError();
   const int64_t plane = static_cast<int64_t>(a.To) * a.hw;
   const int64_t total = static_cast<int64_t>(a.N) * a.Co * plane;
   const bool vec4 = plane % 4 == 0 && (reinterpret_cast<uintptr_t>(a.y) & 7u) == 0;
