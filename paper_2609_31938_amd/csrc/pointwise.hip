@@ -27,6 +27,8 @@
 // past the end of a frame plane are loaded (from the next plane, or as zeros
 // past the tensor) but only feed outputs that are never stored: a 1x1 kernel
 // maps each output pixel to the same input pixel.
+#include <atomic>
+
 #include "c3c_internal.h"
 
 namespace c3c {
@@ -41,21 +43,22 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
 constexpr int PW_K = 32;       // input channels per chunk (one matrix-core K step)
-constexpr int PW_PX = 256;     // pixels per workgroup
 constexpr int PW_NT = 512;     // threads per workgroup: 2 x 4 waves
 constexpr int PW_WCO = 5;      // 16-channel output fragments per wave
-constexpr int PW_NPF = 4;      // 16-pixel fragments per wave
 constexpr int PW_CO = 2 * 16 * PW_WCO;  // output channels per workgroup
+// pixels per workgroup: 4 waves along the pixels, NPF 16-pixel fragments
+// each (NPF = 4: 256 pixels; NPF = 8: 512)
+constexpr int pw_px(int npf) { return 4 * 16 * npf; }
 // LDS bytes per staged activation channel row: 256 px * 2 B + 32 B.  The pad
 // makes the row stride 8 banks mod 64, so the 4 channel rows x 4 pixel groups
 // that one 16-lane block of a transposing read touches fall in distinct banks.
-constexpr int PW_PITCH = PW_PX * 2 + 32;
+constexpr int pw_pitch(int npf) { return pw_px(npf) * 2 + 32; }
 // LDS bytes per staged weight row (32 channels of one output channel): 64 B
 // + 16 B, so that 8 consecutive rows read with 16-byte loads hit distinct
 // 4-bank groups.
 constexpr int PW_WPITCH = 80;
-constexpr int PW_WOFF = PW_K * PW_PITCH;            // weights after the activations
-constexpr int PW_BUF = PW_WOFF + PW_CO * PW_WPITCH;
+constexpr int pw_woff(int npf) { return PW_K * pw_pitch(npf); }  // weights after the activations
+constexpr int pw_buf(int npf) { return pw_woff(npf) + PW_CO * PW_WPITCH; }
 constexpr int PW_WPIECES = PW_CO * PW_K * 2 / 16;    // 16-byte pieces of a weight chunk
 constexpr int PW_WPT = (PW_WPIECES + PW_NT - 1) / PW_NT;  // per thread
 static_assert(PW_CO * PW_K * 2 <= PW_CO * PW_WPITCH, "packed weights fit the weight area");
@@ -101,8 +104,11 @@ __device__ inline f32x4 mma(i16x8 a, u32x4 b, f32x4 c) {
 // w[co][ci] (fallback, Kt = 1).  ALIGNED: every channel plane starts on a
 // 16-byte boundary (H * W a multiple of 8, aligned pointers); else the
 // activations are read 2 bytes at a time and the outputs stored one by one.
-template <bool F16, int PD, bool PACKED, bool ALIGNED>
+template <bool F16, int PD, bool PACKED, bool ALIGNED, int PW_NPF>
 __global__ __launch_bounds__(PW_NT, 1) void pointwise_conv(PwArgs a) {
+  constexpr int PW_PX = pw_px(PW_NPF), PW_PITCH = pw_pitch(PW_NPF);
+  constexpr int PW_WOFF = pw_woff(PW_NPF), PW_BUF = pw_buf(PW_NPF);
+  constexpr int SEG = PW_PX / 128;  // 16-byte row segments per thread per stage
   __shared__ __align__(16) unsigned char lds[2 * PW_BUF];
   constexpr uint32_t OOB = 0x80000000u;  // beyond every resource's size
   const int tid = threadIdx.x, lane = tid & 63;
@@ -162,8 +168,8 @@ __global__ __launch_bounds__(PW_NT, 1) void pointwise_conv(PwArgs a) {
     return r;
   };
 
-  // staging: thread -> activation channel row tid / 16, pixels 8 (tid % 16)
-  // .. + 7 and 128 + 8 (tid % 16) .. + 7 (16 lanes read 256 contiguous bytes)
+  // staging: thread -> activation channel row tid / 16, pixels
+  // 128 h + 8 (tid % 16) .. + 7 for h < SEG (16 lanes read 256 contiguous bytes)
   const int sch = tid >> 4, spx = (tid & 15) * 8;
   const int slds = sch * PW_PITCH + spx * 2;
   // Weights.  Unpacked: pieces tid + 512 i -> row piece / 4, channels
@@ -187,18 +193,19 @@ __global__ __launch_bounds__(PW_NT, 1) void pointwise_conv(PwArgs a) {
     wp_off[i] = static_cast<uint32_t>(frag) * 1024u + static_cast<uint32_t>(piece % 64) * 16u;
   }
   struct Chunk {
-    u32x4 x[2];
+    u32x4 x[SEG];
     u32x4 w[PW_WPT];
   };
   auto load_chunk = [&](int st_, Chunk& ck) {
     const StageSrc sr = stage_src(st_);
     const uint32_t soff = static_cast<uint32_t>(sch) * sr.cs + static_cast<uint32_t>(spx) * 2u;
     if constexpr (ALIGNED) {
-      ck.x[0] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(sr.rs, soff, 0, 0));
-      ck.x[1] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(sr.rs, soff + 256u, 0, 0));
+#pragma unroll
+      for (int h = 0; h < SEG; ++h)
+        ck.x[h] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(sr.rs, soff + 256u * h, 0, 0));
     } else {
 #pragma unroll
-      for (int h = 0; h < 2; ++h) {
+      for (int h = 0; h < SEG; ++h) {
         uint32_t wd[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
@@ -231,8 +238,8 @@ __global__ __launch_bounds__(PW_NT, 1) void pointwise_conv(PwArgs a) {
   };
   auto store_chunk = [&](const Chunk& ck, int buf) {
     unsigned char* base = lds + buf * PW_BUF;
-    *reinterpret_cast<u32x4*>(base + slds) = ck.x[0];
-    *reinterpret_cast<u32x4*>(base + slds + 256) = ck.x[1];
+#pragma unroll
+    for (int h = 0; h < SEG; ++h) *reinterpret_cast<u32x4*>(base + slds + 256 * h) = ck.x[h];
 #pragma unroll
     for (int i = 0; i < PW_WPT; ++i) {
       if constexpr (PACKED) {
@@ -353,11 +360,34 @@ namespace {
 // one launch of pointwise_conv: the ring depth that pads the largest stage
 // count of any output frame least (4, 3 or 2), the template instance by
 // element type, weight layout and alignment
+// compute units of the current device (queried once per device)
+int64_t pw_compute_units() {
+  static std::atomic<int> cache[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  int n = cache[dev].load(std::memory_order_relaxed);
+  if (n == 0) {
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+      n = 256;
+    cache[dev].store(n, std::memory_order_relaxed);
+  }
+  return n;
+}
+
 template <bool PACKED>
 hipError_t launch_pw(const Geo& g, PwArgs a, bool f16, bool al, hipStream_t s) {
   const c3c_conv_desc& d = g.d;
-  a.px_tiles = static_cast<int>((a.hw + PW_PX - 1) / PW_PX);
   a.co_tiles = static_cast<int>((d.Co + PW_CO - 1) / PW_CO);
+  // Fast route, aligned: 512-pixel workgroups (twice the products per
+  // staged weight chunk; 1.4x on a 384->768 120x208 temporal conv) unless
+  // that leaves fewer workgroups than half the compute units.  Otherwise
+  // 256-pixel ones: the unpacked-weight and unaligned instances would spill
+  // at 512 (with 8 waves a wave has 256 registers), and on the 1x1x1
+  // shortcut the wide tile measured no faster.
+  const int64_t tiles512 = (a.hw + pw_px(8) - 1) / pw_px(8);
+  const bool wide = PACKED && al && tiles512 * a.co_tiles * g.To * d.N * 2 >= pw_compute_units();
+  const int px = wide ? pw_px(8) : pw_px(4);
+  a.px_tiles = static_cast<int>((a.hw + px - 1) / px);
   const int64_t blocks = static_cast<int64_t>(a.px_tiles) * a.co_tiles * g.To * d.N;
   if (blocks == 0) return hipSuccess;
   if (blocks > 0x7fffffff) return hipErrorInvalidConfiguration;
@@ -371,21 +401,28 @@ hipError_t launch_pw(const Geo& g, PwArgs a, bool f16, bool al, hipStream_t s) {
     ntap = nt > ntap ? nt : ntap;
   }
   const int nst = ntap * a.chunks;
-  int pd = 4;
-  for (int cand : {3, 2})
-    if ((nst + cand - 1) / cand * cand < (nst + pd - 1) / pd * pd) pd = cand;
+  // ring depth: 2 for 512-pixel workgroups (their staging registers leave
+  // no room for more); for 256-pixel ones, the one of 4, 3, 2 that pads the
+  // stage count least
+  int pd = 2;
+  if (!wide) {
+    pd = 4;
+    for (int cand : {3, 2})
+      if ((nst + cand - 1) / cand * cand < (nst + pd - 1) / pd * pd) pd = cand;
+  }
   const dim3 grid(static_cast<unsigned>(blocks)), block(PW_NT);
-#define C3C_PW(F, P, A)                                                                        \
-  if (f16 == F && pd == P && al == A) {                                                         \
-    hipLaunchKernelGGL((pointwise_conv<F, P, PACKED, A>), grid, block, 0, s, a);               \
+#define C3C_PW(F, P, A, NPF)                                                                   \
+  if (f16 == F && pd == P && al == A && (NPF == 8) == wide) {                                   \
+    hipLaunchKernelGGL((pointwise_conv<F, P, PACKED, A, NPF>), grid, block, 0, s, a);          \
     return hipGetLastError();                                                                  \
   }
   if constexpr (PACKED) {  // fast route: bf16, any alignment
-    C3C_PW(false, 2, true) C3C_PW(false, 3, true) C3C_PW(false, 4, true)
-    C3C_PW(false, 2, false) C3C_PW(false, 3, false) C3C_PW(false, 4, false)
+    C3C_PW(false, 2, true, 4) C3C_PW(false, 3, true, 4) C3C_PW(false, 4, true, 4)
+    C3C_PW(false, 2, false, 4) C3C_PW(false, 3, false, 4) C3C_PW(false, 4, false, 4)
+    C3C_PW(false, 2, true, 8)
   } else {  // fallback: bf16 / fp16, aligned (pointwise_eligible)
-    C3C_PW(false, 2, true) C3C_PW(false, 3, true) C3C_PW(false, 4, true)
-    C3C_PW(true, 2, true) C3C_PW(true, 3, true) C3C_PW(true, 4, true)
+    C3C_PW(false, 2, true, 4) C3C_PW(false, 3, true, 4) C3C_PW(false, 4, true, 4)
+    C3C_PW(true, 2, true, 4) C3C_PW(true, 3, true, 4) C3C_PW(true, 4, true, 4)
   }
 #undef C3C_PW
   return hipErrorInvalidValue;
