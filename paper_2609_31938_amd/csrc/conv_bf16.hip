@@ -547,7 +547,7 @@ __global__ __launch_bounds__(256) void splitk_reduce(const float* __restrict__ p
 }
 
 // Tile configurations of the bf16 kernel (template arguments of run()).
-enum Cfg { CFG_C192, CFG_C96, CFG_C160_4X80, CFG_C160_10X32 };
+enum Cfg { CFG_C192, CFG_C96, CFG_C16, CFG_C160_4X80, CFG_C160_10X32 };
 
 // Launch plan of one bf16 fast call: tile configuration, workgroups of one
 // split, split-K factor, and the fp32 partial-sum bytes the split needs.
@@ -648,6 +648,12 @@ Plan plan_bf16(const Geo& g) {
   if (Co > 128 && Co % 192 == 0) {
     p.cfg = CFG_C192;
     set_tiles(g, 192, 4, 64, &p);
+  } else if (Co <= 16) {
+    // a head conv with a few output channels (e.g. 3, to RGB): one 16-channel
+    // fragment per wave, so the matrix cores do 1/6 of the 96-channel tile's
+    // work on the same staged activations
+    p.cfg = CFG_C16;
+    set_tiles(g, 16, 8, 64, &p);
   } else if (Co <= 96) {
     p.cfg = CFG_C96;
     set_tiles(g, 96, 8, 64, &p);
@@ -748,6 +754,7 @@ hipError_t launch_fast_bf16(const Geo& g, const void* x, const void* cache, cons
   switch (pl.cfg) {
     case CFG_C192: return run<6, 2, 4, 2, 2, 3>(g, a, pl, aligned, s);
     case CFG_C96: return run<6, 2, 4, 1, 4, 2>(g, a, pl, aligned, s);
+    case CFG_C16: return run<1, 2, 4, 1, 4, 2>(g, a, pl, aligned, s);
     case CFG_C160_4X80: return run<5, 2, 5, 2, 2, 3>(g, a, pl, aligned, s);
     default: return run<5, 5, 2, 2, 2, 3>(g, a, pl, aligned, s);
   }

@@ -129,6 +129,9 @@ WORKLOADS = {
                                ("shortcut_1x1x1_320to160_352x640",
                                 spec(N=1, Ci=320, Co=160, T=4, Tc=0, H=352, W=640,
                                      Kt=1, Kh=1, Kw=1))]),
+    # 7: the decoder's output head (to 3 channels, RGB) at full resolution
+    "head": dict(id=7, dtype="bf16", chunks=5,
+                 layers=[("head_96to3_480x832", _c(96, 3, 4, 480, 832))]),
     # 6: temporal convolutions (kernel 3x1x1) of the decoder's temporal
     # upsampling (channels doubled, then split into two frames by the
     # decoder) and of an encoder's stride-2 temporal downsampling

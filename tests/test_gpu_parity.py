@@ -85,6 +85,10 @@ FAST_CASES = [
     ("f32", dict(N=1, Ci=32, Co=32, T=2, Tc=2, H=32, W=32)),
     ("f32", dict(N=2, Ci=7, Co=45, T=3, Tc=1, H=13, W=34)),
     ("f32", dict(N=1, Ci=33, Co=70, T=1, Tc=2, H=10, W=66)),
+    # few output channels (a head conv to RGB): the 16-channel tile
+    ("bf16", dict(N=1, Ci=96, Co=3, T=4, Tc=2, H=20, W=72)),
+    ("bf16", dict(N=1, Ci=40, Co=16, T=2, Tc=2, H=9, W=35)),             # unaligned width
+    ("bf16", dict(N=2, Ci=33, Co=1, T=3, Tc=0, H=17, W=64)),
     # 1x1 spatial kernels (temporal convolutions): per-frame matrix products
     ("bf16", dict(N=1, Ci=96, Co=192, T=4, Tc=2, H=16, W=40, Kh=1, Kw=1)),
     ("bf16", dict(N=2, Ci=40, Co=200, T=3, Tc=2, H=9, W=24, Kh=1, Kw=1)),    # chunk tail, 2 co tiles

@@ -109,3 +109,11 @@ def test_temporal_convs():
     ctx = _stream("temporal", check_chunks=[0, 1, -1])
     c = ctx.counters()
     assert (c["calls"], c["fast"], c["fallback"]) == (15, 15, 0)
+
+
+def test_head_conv():
+    """The decoder's output head (96 -> 3 channels at 480x832) on the
+    16-channel tile, streamed over 5 chunks."""
+    ctx = _stream("head", check_chunks=[0, -1])
+    c = ctx.counters()
+    assert (c["calls"], c["fast"], c["fallback"]) == (5, 5, 0)
