@@ -59,6 +59,18 @@ int64_t fast_bf16_workspace_bytes(const Geo& g);
 bool pointwise_eligible(const Geo& g, const void* x, const void* cache, const void* w, const void* y);
 hipError_t launch_pointwise(const Geo& g, const void* x, const void* cache, const void* w,
                             const void* bias, void* y, hipStream_t s);
+// compute units of the current device (256 when no device is visible)
+int64_t device_compute_units();
+// output channels per workgroup of the two bf16 1x1 kernels of the fast route
+constexpr int64_t kTap1x1TileCo = 192;     // conv_tap1x1.hip
+constexpr int64_t kPointwiseTileCo = 160;  // pointwise.hip
+// fast route, bf16, 1x1 spatial kernel (conv_tap1x1.hip): 192 x 320 output
+// tiles on 4 waves; needs H * W a multiple of 8 and aligned pointers.  The
+// caller copies the cache.
+bool tap1x1_eligible(const Geo& g, const void* x, const void* cache, const void* y);
+int64_t tap1x1_blocks(const Geo& g);
+hipError_t launch_tap1x1(const Geo& g, const void* x, const void* cache, const void* wpack,
+                         const void* bias, void* y, hipStream_t s);
 // fast route, bf16, 1x1 spatial kernel (pointwise.hip): every active temporal
 // tap of a call as per-frame matrix products, reading the packed weights; any
 // temporal stride and dilation, any H * W and alignment.  The caller copies

@@ -617,8 +617,10 @@ bool cache_covered(const Geo& g) {
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
+}  // namespace
+
 // compute units of the current device (queried once per device)
-int64_t compute_units() {
+int64_t device_compute_units() {
   static std::atomic<int> cache[64];
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
@@ -631,6 +633,9 @@ int64_t compute_units() {
   return n;
 }
 
+namespace {
+
+int64_t compute_units() { return device_compute_units(); }
 
 // The tile configuration by output-channel count, and the split-K factor: a
 // call whose workgroups fill less than one round of the compute units splits

@@ -1,0 +1,313 @@
+// Fast route, bf16, 1x1 spatial kernel: temporal convolutions (kernel Kt x 1
+// x 1, any temporal stride and dilation) as per-frame matrix products on
+// gfx950 matrix cores, one wave per SIMD.
+//
+// Output frame t of batch element n is
+//   y[co][p] = b[co] + sum_{k active} sum_ci w[co][ci][k] z[ci][f_k][p],
+//   f_k = t * s_t + k * d_t - p_l,
+// over the frames f_k of [cache; x] that exist (Eq. 2 with the source time of
+// Eq. 1 and the stride of Eq. 3; Eq. 4 drops the others), bias once.
+//
+// Workgroup = 192 output channels x 320 consecutive pixels of one (n, t)
+// frame, 4 waves side by side along the output channels, each 48 channels x
+// all 320 pixels: 3 x 20 accumulator fragments of v_mfma_f32_16x16x32_bf16
+// (activations as the A operand, lane l holding 4 consecutive pixels of
+// channel l % 16).  Every wave needs different weights, so no weight byte is
+// fetched twice per workgroup; the activation tile is shared through LDS.
+// A stage is one active tap and one 32-channel chunk:
+//   * its activation tile [32 ch][320 px] is copied into LDS as it lies in
+//     memory (pixels contiguous) and read back with the transposing
+//     ds_read_b64_tr_b16, which gives each lane 8 consecutive channels of one
+//     pixel;
+//   * its weights are the packed fragments (tap, chunk, output fragment), one
+//     16-byte load per lane each, straight from L2 into registers.
+// Pipeline: during stage s the waves issue the weights of stage s + 1 and the
+// activation loads of stage s + 2, compute stage s, then write stage s + 1's
+// activations (loaded during stage s - 1) into the other LDS buffer, and one
+// barrier publishes it.  The stage loop is unrolled by two (register sets
+// alternate), the stage count padded to even with stages that read zeros.
+// Pixels past the end of a frame plane are loaded (the next plane, or zeros
+// past the tensor) but only feed outputs that are never stored.
+//
+// Requires H * W a multiple of 8 and 16-byte-aligned x / cache, 8-byte y.
+#include "c3c_internal.h"
+
+namespace c3c {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef short i16x8 __attribute__((ext_vector_type(8)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+
+constexpr int TK = 32;                 // input channels per stage (one matrix-core K step)
+constexpr int TPX = 320;               // pixels per workgroup
+constexpr int WCO = 3, NPF = TPX / 16; // fragments per wave: 48 channels x 320 pixels
+constexpr int TCO = 4 * WCO * 16;      // output channels per workgroup
+static_assert(TCO == kTap1x1TileCo, "the tile width the dispatcher compares");
+// LDS offset of staged channel row r: pitch 640 B + 32 B, and 128 B more
+// after every 8 rows.  A transposing read serves 32 lanes at a time from 64
+// four-byte banks; those lanes read 32 B from each of rows {0..3, 8..11}
+// (+4, +16 or +20 for the other halves of the fragment and wave), which
+// start at banks 0, 40, 16, 56 and 32, 8, 48, 24: eight disjoint 8-bank
+// groups.
+constexpr int TPITCH = TPX * 2 + 32;
+constexpr int row_off(int r) { return r * TPITCH + (r >> 3) * 128; }
+constexpr int TBUF = row_off(TK);
+constexpr int TSEG = TK * TPX / 8;     // 16-byte segments of a stage tile
+constexpr int TSPT = TSEG / 256;       // per thread
+static_assert(TSEG % 256 == 0, "the stage tile splits evenly over the threads");
+
+struct TapArgs {
+  const uint16_t* x;
+  const uint16_t* cache;
+  const u32x4* wpack;
+  const uint16_t* bias;
+  uint16_t* y;
+  int64_t hw;
+  int N, Ci, Co, T, Tc, To, Z, st, dt, p_l, Kt;
+  int chunks, cofrags, px_tiles, co_tiles, nblocks;
+  uint32_t wpack_bytes;
+  int has_bias;
+};
+
+__global__ __launch_bounds__(256, 1) void conv_tap1x1(TapArgs a) {
+  __shared__ __align__(16) unsigned char lds[2 * TBUF];
+  constexpr uint32_t OOB = 0x80000000u;  // beyond every resource's size
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wco = wave;  // output-channel slice of this wave
+
+  // workgroups numbered so that each of the 8 XCDs (which take workgroups
+  // round-robin) runs a contiguous range: the output-channel tiles of a pixel
+  // tile (which read the same activations) run close together
+  int b;
+  {
+    const int per = a.nblocks / 8, rem = a.nblocks % 8;
+    const int xcd = static_cast<int>(blockIdx.x) % 8, slot = static_cast<int>(blockIdx.x) / 8;
+    b = (xcd < rem ? xcd * (per + 1) : rem * (per + 1) + (xcd - rem) * per) + slot;
+  }
+  const int ctile = b % a.co_tiles;
+  b /= a.co_tiles;
+  const int pt = b % a.px_tiles;
+  b /= a.px_tiles;
+  const int t = b % a.To;
+  const int n = b / a.To;
+  const int px0 = pt * TPX;
+
+  // active taps (Eq. 4): one contiguous range [k_lo, k_lo + ntap)
+  int k_lo = 0;
+  while (k_lo < a.Kt && t * a.st + k_lo * a.dt - a.p_l < 0) ++k_lo;
+  int k_hi = a.Kt - 1;
+  while (k_hi >= 0 && t * a.st + k_hi * a.dt - a.p_l >= a.Z) --k_hi;
+  const int ntap = k_hi >= k_lo ? k_hi - k_lo + 1 : 0;
+  const int nst = ntap * a.chunks;  // tap outer, chunk inner
+  const int padded = (nst + 1) & ~1;
+
+  // activation stages are loaded in order: (ak, ac) is the tap and channel
+  // chunk of the next one.  Its source is a buffer resource from channel
+  // 32 ac of frame f_ak (pixel px0) to the end of the last real channel's
+  // row, empty past the last stage.
+  const int64_t cs_c = static_cast<int64_t>(a.Tc) * a.hw, cs_x = static_cast<int64_t>(a.T) * a.hw;
+  int ak = k_lo, ac = 0;
+  auto next_rsrc = [&](uint32_t& cs) {
+    const bool real = ak <= k_hi;
+    const int c0 = ac * TK;
+    const int f = t * a.st + ak * a.dt - a.p_l;
+    const bool in_cache = f < a.Tc;
+    const int64_t cstride = in_cache ? cs_c : cs_x;
+    const uint16_t* base = in_cache ? a.cache : a.x;
+    const int64_t off = static_cast<int64_t>(in_cache ? f : f - a.Tc) * a.hw +
+                        static_cast<int64_t>(n) * a.Ci * cstride + px0 + c0 * cstride;
+    int64_t bytes = ((a.Ci - 1 - c0) * cstride + a.hw - px0) * 2;
+    if (!real || bytes < 0) bytes = 0;
+    if (bytes > 0x7fffffff) bytes = 0x7fffffff;
+    cs = static_cast<uint32_t>(cstride * 2);
+    if (++ac == a.chunks) {
+      ac = 0;
+      ++ak;
+    }
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(real ? base + off : base), 0,
+                                             static_cast<int>(bytes), 0x00020000);
+  };
+
+  // staging: segment q = tid + 256 i of the tile -> channel row q / 40,
+  // pixels 8 (q % 40) .. + 7 (consecutive lanes read consecutive 16 bytes)
+  uint32_t s_row[TSPT], s_px[TSPT], s_lds[TSPT];
+#pragma unroll
+  for (int i = 0; i < TSPT; ++i) {
+    const int q = tid + 256 * i, r = q / (TPX / 8), c = q % (TPX / 8);
+    s_row[i] = static_cast<uint32_t>(r);
+    s_px[i] = static_cast<uint32_t>(c) * 16u;
+    s_lds[i] = static_cast<uint32_t>(row_off(r) + c * 16);
+  }
+  auto load_act = [&](u32x4 (&v)[TSPT]) {
+    uint32_t cs;
+    const __amdgpu_buffer_rsrc_t rs = next_rsrc(cs);
+#pragma unroll
+    for (int i = 0; i < TSPT; ++i)
+      v[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, s_row[i] * cs + s_px[i], 0, 0));
+  };
+  auto store_act = [&](const u32x4 (&v)[TSPT], int buf) {
+#pragma unroll
+    for (int i = 0; i < TSPT; ++i) *reinterpret_cast<u32x4*>(lds + buf * TBUF + s_lds[i]) = v[i];
+  };
+
+  // weights: fragment (tap k, chunk c, output fragment ctile 12 + wco 3 + cf),
+  // clamped to the last packed fragment (padding rows are never stored); an
+  // out-of-range offset (zeros) past the last stage
+  const __amdgpu_buffer_rsrc_t wrs = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<u32x4*>(a.wpack), 0, static_cast<int>(a.wpack_bytes), 0x00020000);
+  uint32_t w_off[WCO];
+#pragma unroll
+  for (int cf = 0; cf < WCO; ++cf)
+    w_off[cf] = static_cast<uint32_t>(min(ctile * (TCO / 16) + wco * WCO + cf, a.cofrags - 1)) * 1024u +
+                static_cast<uint32_t>(lane) * 16u;
+  auto load_w = [&](int s, u32x4 (&v)[WCO]) {
+    // stage s is tap k_lo + s / chunks, chunk s % chunks: packed row k_lo * chunks + s
+    const bool real = s < nst;
+    const uint32_t row = static_cast<uint32_t>((k_lo * a.chunks + s) * a.cofrags) * 1024u;
+#pragma unroll
+    for (int cf = 0; cf < WCO; ++cf)
+      v[cf] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                                            wrs, real ? row + w_off[cf] : OOB, 0, 0));
+  };
+
+  // transposing operand read: within each 16-lane block (channel group
+  // g = l / 16), lane j names channel 8g + 4h + j / 4 at pixel group
+  // 4 (j % 4) of the fragment; lane j receives channels 8g + 4h .. + 3 of
+  // the fragment's pixel j (h = 0, 1: the two halves)
+  const int j = lane & 15, g = lane >> 4;
+  const int ra = row_off(8 * g + (j >> 2)) + 4 * (j & 3) * 2;
+  auto read_a = [&](int buf, int pf) {
+    const unsigned char* p = lds + buf * TBUF + ra + pf * 32;
+    const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p));
+    const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p + 4 * TPITCH));
+    return i16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+  };
+
+  f32x4 acc[WCO][NPF];
+#pragma unroll
+  for (int cf = 0; cf < WCO; ++cf)
+#pragma unroll
+    for (int pf = 0; pf < NPF; ++pf) acc[cf][pf] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  // prologue: weights of stage 0, activations of stages 0 and 1 in flight,
+  // stage 0 into LDS buffer 0
+  u32x4 act0[TSPT], act1[TSPT];
+  u32x4 w0[WCO], w1[WCO];
+  load_w(0, w0);
+  load_act(act0);
+  load_act(act1);
+  store_act(act0, 0);
+  __syncthreads();
+
+  // one stage: weights of s + 1 and activations of s + 2 issued (their
+  // register sets were consumed in stage s - 1), the products of s, then
+  // s + 1's activations into the other buffer (last read in stage s - 1,
+  // before its barrier)
+  auto stage = [&](int s, int buf, const u32x4 (&w_cur)[WCO], u32x4 (&w_nxt)[WCO], u32x4 (&a_free)[TSPT],
+                   const u32x4 (&a_next)[TSPT]) {
+    load_w(s + 1, w_nxt);
+    load_act(a_free);
+    i16x8 av[NPF];
+#pragma unroll
+    for (int pf = 0; pf < NPF; ++pf) av[pf] = read_a(buf, pf);
+#pragma unroll
+    for (int pf = 0; pf < NPF; ++pf)
+#pragma unroll
+      for (int cf = 0; cf < WCO; ++cf)
+        acc[cf][pf] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+            __builtin_bit_cast(bf16x8, av[pf]), __builtin_bit_cast(bf16x8, w_cur[cf]), acc[cf][pf], 0, 0, 0);
+    store_act(a_next, buf ^ 1);
+    __syncthreads();
+  };
+  for (int s = 0; s < padded; s += 2) {
+    stage(s, 0, w0, w1, act0, act1);
+    stage(s + 1, 1, w1, w0, act1, act0);
+  }
+
+  // epilogue: lane l holds pixels 4 (l / 16) .. + 3 of output channel l % 16
+  // of each fragment; bias once, one round-to-nearest-even, NCTHW store
+  uint16_t* ybase = a.y + (static_cast<int64_t>(n) * a.Co * a.To + t) * a.hw;
+#pragma unroll
+  for (int cf = 0; cf < WCO; ++cf) {
+    const int co = ctile * TCO + wco * 16 * WCO + cf * 16 + (lane & 15);
+    if (co >= a.Co) continue;
+    const float bb = a.has_bias ? __uint_as_float(static_cast<uint32_t>(a.bias[co]) << 16) : 0.f;
+    uint16_t* yrow = ybase + static_cast<int64_t>(co) * a.To * a.hw;
+#pragma unroll
+    for (int pf = 0; pf < NPF; ++pf) {
+      const int p = px0 + pf * 16 + 4 * g;
+      if (p >= a.hw) continue;
+      const uint32_t v01 = __builtin_bit_cast(
+          uint32_t, __builtin_convertvector((f32x2{acc[cf][pf][0] + bb, acc[cf][pf][1] + bb}), bf16x2));
+      const uint32_t v23 = __builtin_bit_cast(
+          uint32_t, __builtin_convertvector((f32x2{acc[cf][pf][2] + bb, acc[cf][pf][3] + bb}), bf16x2));
+      // H * W is a multiple of 8, so 4 pixels from a multiple of 4 stay in the plane
+      *reinterpret_cast<uint2*>(yrow + p) = make_uint2(v01, v23);
+    }
+  }
+}
+
+bool aligned_to(const void* p, uintptr_t m) { return (reinterpret_cast<uintptr_t>(p) & (m - 1)) == 0; }
+
+}  // namespace
+
+bool tap1x1_eligible(const Geo& g, const void* x, const void* cache, const void* y) {
+  const c3c_conv_desc& d = g.d;
+  // buffer offsets are 32-bit: one 32-channel stage slab and the packed weights must fit
+  const int64_t frames = d.T > d.Tc ? d.T : d.Tc;
+  if (static_cast<int64_t>(TK) * frames * d.H * d.W * 2 >= 0x7fffffff ||
+      pack_dims(d).elems() * 2 >= 0x7fffffff)
+    return false;
+  return (d.H * d.W) % 8 == 0 && aligned_to(x, 16) && (cache == nullptr || aligned_to(cache, 16)) &&
+         aligned_to(y, 8);
+}
+
+int64_t tap1x1_blocks(const Geo& g) {
+  return (g.d.H * g.d.W + TPX - 1) / TPX * ((g.d.Co + TCO - 1) / TCO) * g.To * g.d.N;
+}
+
+hipError_t launch_tap1x1(const Geo& g, const void* x, const void* cache, const void* wpack,
+                         const void* bias, void* y, hipStream_t s) {
+  const c3c_conv_desc& d = g.d;
+  const PackDims p = pack_dims(d);
+  if (!tap1x1_eligible(g, x, cache, y)) return hipErrorInvalidValue;
+  TapArgs a;
+  a.x = static_cast<const uint16_t*>(x);
+  a.cache = static_cast<const uint16_t*>(cache);
+  a.wpack = static_cast<const u32x4*>(wpack);
+  a.bias = static_cast<const uint16_t*>(bias);
+  a.y = static_cast<uint16_t*>(y);
+  a.hw = d.H * d.W;
+  a.N = static_cast<int>(d.N);
+  a.Ci = static_cast<int>(d.Ci);
+  a.Co = static_cast<int>(d.Co);
+  a.T = static_cast<int>(d.T);
+  a.Tc = static_cast<int>(d.Tc);
+  a.To = static_cast<int>(g.To);
+  a.Z = static_cast<int>(g.Z);
+  a.st = static_cast<int>(d.stride_t);
+  a.dt = static_cast<int>(d.dil_t);
+  a.p_l = static_cast<int>(g.p_l);
+  a.Kt = static_cast<int>(d.Kt);
+  a.chunks = static_cast<int>(p.chunks);
+  a.cofrags = static_cast<int>(p.cofrags);
+  a.px_tiles = static_cast<int>((a.hw + TPX - 1) / TPX);
+  a.co_tiles = static_cast<int>((d.Co + TCO - 1) / TCO);
+  a.wpack_bytes = static_cast<uint32_t>(p.elems() * 2);
+  a.has_bias = d.has_bias ? 1 : 0;
+  const int64_t blocks = tap1x1_blocks(g);
+  if (blocks == 0) return hipSuccess;
+  if (blocks > 0x7fffffff) return hipErrorInvalidConfiguration;
+  a.nblocks = static_cast<int>(blocks);
+  hipLaunchKernelGGL(conv_tap1x1, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace c3c

@@ -27,8 +27,6 @@
 // past the end of a frame plane are loaded (from the next plane, or as zeros
 // past the tensor) but only feed outputs that are never stored: a 1x1 kernel
 // maps each output pixel to the same input pixel.
-#include <atomic>
-
 #include "c3c_internal.h"
 
 namespace c3c {
@@ -46,6 +44,7 @@ constexpr int PW_K = 32;       // input channels per chunk (one matrix-core K st
 constexpr int PW_NT = 512;     // threads per workgroup: 2 x 4 waves
 constexpr int PW_WCO = 5;      // 16-channel output fragments per wave
 constexpr int PW_CO = 2 * 16 * PW_WCO;  // output channels per workgroup
+static_assert(PW_CO == kPointwiseTileCo, "the tile width the dispatcher compares");
 // pixels per workgroup: 4 waves along the pixels, NPF 16-pixel fragments
 // each (NPF = 4: 256 pixels; NPF = 8: 512)
 constexpr int pw_px(int npf) { return 4 * 16 * npf; }
@@ -360,20 +359,6 @@ namespace {
 // one launch of pointwise_conv: the ring depth that pads the largest stage
 // count of any output frame least (4, 3 or 2), the template instance by
 // element type, weight layout and alignment
-// compute units of the current device (queried once per device)
-int64_t pw_compute_units() {
-  static std::atomic<int> cache[64];
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
-  int n = cache[dev].load(std::memory_order_relaxed);
-  if (n == 0) {
-    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
-      n = 256;
-    cache[dev].store(n, std::memory_order_relaxed);
-  }
-  return n;
-}
-
 template <bool PACKED>
 hipError_t launch_pw(const Geo& g, PwArgs a, bool f16, bool al, hipStream_t s) {
   const c3c_conv_desc& d = g.d;
@@ -385,7 +370,7 @@ hipError_t launch_pw(const Geo& g, PwArgs a, bool f16, bool al, hipStream_t s) {
   // at 512 (with 8 waves a wave has 256 registers), and on the 1x1x1
   // shortcut the wide tile measured no faster.
   const int64_t tiles512 = (a.hw + pw_px(8) - 1) / pw_px(8);
-  const bool wide = PACKED && al && tiles512 * a.co_tiles * g.To * d.N * 2 >= pw_compute_units();
+  const bool wide = PACKED && al && tiles512 * a.co_tiles * g.To * d.N * 2 >= device_compute_units();
   const int px = wide ? pw_px(8) : pw_px(4);
   a.px_tiles = static_cast<int>((a.hw + px - 1) / px);
   const int64_t blocks = static_cast<int64_t>(a.px_tiles) * a.co_tiles * g.To * d.N;
