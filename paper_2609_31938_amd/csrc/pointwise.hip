@@ -48,15 +48,19 @@ static_assert(PW_CO == kPointwiseTileCo, "the tile width the dispatcher compares
 // pixels per workgroup: 4 waves along the pixels, NPF 16-pixel fragments
 // each (NPF = 4: 256 pixels; NPF = 8: 512)
 constexpr int pw_px(int npf) { return 4 * 16 * npf; }
-// LDS bytes per staged activation channel row: 256 px * 2 B + 32 B.  The pad
-// makes the row stride 8 banks mod 64, so the 4 channel rows x 4 pixel groups
-// that one 16-lane block of a transposing read touches fall in distinct banks.
+// LDS bytes per staged activation channel row: pixels * 2 B + 32 B, and 128 B
+// more after every 8 rows.  A transposing read serves 32 lanes at a time from
+// 64 four-byte banks; those lanes read 32 B from each of rows {0..3, 8..11}
+// (+4, +16 or +20 for the other halves), which the row stride (8 banks mod
+// 64) and the 8-row skew (32 banks) put at banks 0, 8, 16, 24 and 32, 40,
+// 48, 56: eight disjoint 8-bank groups.
 constexpr int pw_pitch(int npf) { return pw_px(npf) * 2 + 32; }
+constexpr int pw_row(int npf, int r) { return r * pw_pitch(npf) + (r >> 3) * 128; }
 // LDS bytes per staged weight row (32 channels of one output channel): 64 B
 // + 16 B, so that 8 consecutive rows read with 16-byte loads hit distinct
 // 4-bank groups.
 constexpr int PW_WPITCH = 80;
-constexpr int pw_woff(int npf) { return PW_K * pw_pitch(npf); }  // weights after the activations
+constexpr int pw_woff(int npf) { return pw_row(npf, PW_K); }  // weights after the activations
 constexpr int pw_buf(int npf) { return pw_woff(npf) + PW_CO * PW_WPITCH; }
 constexpr int PW_WPIECES = PW_CO * PW_K * 2 / 16;    // 16-byte pieces of a weight chunk
 constexpr int PW_WPT = (PW_WPIECES + PW_NT - 1) / PW_NT;  // per thread
@@ -170,7 +174,7 @@ __global__ __launch_bounds__(PW_NT, 1) void pointwise_conv(PwArgs a) {
   // staging: thread -> activation channel row tid / 16, pixels
   // 128 h + 8 (tid % 16) .. + 7 for h < SEG (16 lanes read 256 contiguous bytes)
   const int sch = tid >> 4, spx = (tid & 15) * 8;
-  const int slds = sch * PW_PITCH + spx * 2;
+  const int slds = pw_row(PW_NPF, sch) + spx * 2;
   // Weights.  Unpacked: pieces tid + 512 i -> row piece / 4, channels
   // 8 (piece % 4) .. + 7; rows past Co and channels past Ci are out-of-range
   // offsets (zeros).  Packed: piece q = 16-byte lane slot q % 64 of output
@@ -256,7 +260,7 @@ __global__ __launch_bounds__(PW_NT, 1) void pointwise_conv(PwArgs a) {
   // 4 (j % 4) of the fragment; lane j receives channels 8g + 4h .. + 3 of
   // the fragment's pixel j
   const int j = lane & 15, g = lane >> 4;
-  const int ra = (8 * g + (j >> 2)) * PW_PITCH + (wpx * 16 * PW_NPF + 4 * (j & 3)) * 2;
+  const int ra = pw_row(PW_NPF, 8 * g + (j >> 2)) + (wpx * 16 * PW_NPF + 4 * (j & 3)) * 2;
   auto read_a = [&](int buf, int pf) {
     const unsigned char* p = lds + buf * PW_BUF + ra + pf * 32;
     const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p));
