@@ -10,6 +10,12 @@ plain zero-padded causal Conv3D over the cache-augmented input Z = [C; X]_T of
 the paper's Sec. 4 (Eq. 1-4), with the bias added exactly once and the cache
 replaced by the last min(p_base, |Z|) frames of Z.
 
+The fused residual-block form is the composition of plain parts: the new
+chunk goes through ``u = RNE_bf16(SiLU(x * scale[n, c] + shift[n, c]))`` (fp64,
+one rounding), the convolution runs on ``[C; u]`` (so the new cache holds
+activated frames), and a residual of the output's shape is added in fp64 after
+the bias (``conv3d_fused``).
+
 A call is described by a plain ``spec`` dict with the keys
 ``N Ci Co T Tc H W Kt Kh Kw s_t s_h s_w d_t d_h d_w p_base p_r p_h p_w groups
 has_bias``.  Element types are named ``"f64" "f32" "bf16" "f16"``; bf16 data is
@@ -66,6 +72,11 @@ def _load():
         lib.ora_flops.argtypes = [P(_Desc)]
         lib.ora_flops.restype = C.c_double
         lib.ora_num_threads.restype = C.c_int
+        lib.ora_round_bf16.argtypes = [C.c_double]
+        lib.ora_round_bf16.restype = C.c_uint16
+        lib.ora_silu.argtypes = [C.c_double]
+        lib.ora_silu.restype = C.c_double
+        lib.ora_prologue_bf16.argtypes = [i64, i64, i64, i64, vp, vp, vp, vp]
         _lib = lib
     return _lib
 
@@ -214,3 +225,55 @@ def cache_update(spec: dict, dtype: str, x, cache) -> np.ndarray:
     _check(lib.ora_cache_update(C.byref(_desc(spec)), _DTYPES[dtype], _ptr(x),
                                 _ptr(cache), _ptr(out)), "cache_update")
     return out
+
+
+# ---------------------------------------------------------------- fused form
+def round_bf16(v) -> np.ndarray:
+    """Nearest bf16 (ties to even) of each fp64 value, as uint16 bits."""
+    lib = _load()
+    v = np.ascontiguousarray(v, dtype=np.float64)
+    return np.array([lib.ora_round_bf16(float(e)) for e in v.ravel()], np.uint16).reshape(v.shape)
+
+
+def silu(v) -> np.ndarray:
+    """SiLU(v) = v / (1 + e^-v) in fp64, elementwise."""
+    lib = _load()
+    v = np.ascontiguousarray(v, dtype=np.float64)
+    return np.array([lib.ora_silu(float(e)) for e in v.ravel()], np.float64).reshape(v.shape)
+
+
+def prologue_bf16(spec: dict, x, scale, shift) -> np.ndarray:
+    """u = RNE_bf16(SiLU(x * scale[n, c] + shift[n, c])) over the new chunk x
+    (N, Ci, T, H, W) bf16 bits; scale / shift are fp32 (N, Ci)."""
+    lib = _load()
+    N, Ci, T, hw = spec["N"], spec["Ci"], spec["T"], spec["H"] * spec["W"]
+    x = _host(x, "bf16")
+    sc = np.ascontiguousarray(_host(scale, "f32")).reshape(-1)
+    sh = np.ascontiguousarray(_host(shift, "f32")).reshape(-1)
+    if x.size != N * Ci * T * hw or sc.size != N * Ci or sh.size != N * Ci:
+        raise ValueError("prologue arguments have the wrong number of elements")
+    u = np.empty((N, Ci, T, spec["H"], spec["W"]), np.uint16)
+    _check(lib.ora_prologue_bf16(N, Ci, T, hw, _ptr(x), _ptr(sc), _ptr(sh), _ptr(u)),
+           "prologue_bf16")
+    return u
+
+
+def _widen_bf16(a) -> np.ndarray:
+    a = _host(a, "bf16")
+    return (a.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+
+
+def conv3d_fused(spec: dict, x, cache, w, b, scale=None, shift=None, residual=None):
+    """The fused residual-block call, bf16: (y fp64 (N, Co, T_o, H_o, W_o),
+    cache' bf16 bits (N, Ci, L, H, W)).  scale and shift are given together or
+    not at all (then u = x); residual (bf16, y's shape) may be None."""
+    if (scale is None) != (shift is None):
+        raise ValueError("scale and shift go together")
+    u = prologue_bf16(spec, x, scale, shift) if scale is not None else _host(x, "bf16")
+    y = conv3d(spec, "bf16", u, cache, w, b)
+    if residual is not None:
+        r = _widen_bf16(residual)
+        if r.size != y.size:
+            raise ValueError("residual has the wrong number of elements")
+        y = y + r.reshape(y.shape)
+    return y, cache_update(spec, "bf16", u, cache)

@@ -31,6 +31,19 @@
  * also exported, written from the formulas, so that tests can compare them
  * with brute-force enumeration.
  *
+ * The fused residual-block form (the library's fused entry point) is defined
+ * by composition, each part plain: the new chunk first goes through the
+ * block's folded normalisation and activation,
+ *   u[n,c,t,p] = RNE_bf16( SiLU( x[n,c,t,p] * s[n,c] + t[n,c] ) ),
+ *   SiLU(v) = v / (1 + e^{-v}),
+ * evaluated in fp64 and rounded once to bf16 (the precision the unfused
+ * pipeline stores the activation in); then the convolution above runs on
+ * Z = [C; u] (so cache' holds activated frames, as the cache of the next
+ * convolution in an unfused pipeline would), and a residual tensor of the
+ * output's shape is added after the bias.  This file provides the rounding,
+ * SiLU and the prologue; the residual sum is one fp64 addition per output,
+ * done by the Python wrapper.
+ *
  * The route rule (which calls the lowered fast route accepts) is the written
  * guard of Alg. 1 plus this library's fast-kernel contract: K_t >= 2, and
  * one of two spatial forms, 3x3 / stride 1 / pad 1 / dilation 1 or 1x1 /
@@ -422,4 +435,54 @@ int ora_num_threads(void) {
 #else
   return 1;
 #endif
+}
+
+/* Nearest bf16 to v (ties to even), as raw bits.  bf16 keeps the fp32
+ * exponent range and 8 significant bits: for |v| >= 2^-126 the spacing of
+ * bf16 values around v is 2^(e-7) where 2^e <= |v| < 2^(e+1); below 2^-126
+ * it is the subnormal spacing 2^-133.  |v| / spacing rounded to an integer
+ * with ties to even (nearbyint in the default rounding mode) is the
+ * significand in units of the spacing; a result of 2^128 or more is
+ * infinity.  The rounded value is exact in fp32, whose top 16 bits are the
+ * answer. */
+uint16_t ora_round_bf16(double v) {
+  if (isnan(v)) return 0x7fc0;
+  uint16_t sign = signbit(v) ? 0x8000 : 0;
+  double a = fabs(v);
+  if (isinf(a)) return (uint16_t)(sign | 0x7f80);
+  if (a == 0.0) return sign;
+  double q;
+  if (a >= ldexp(1.0, -126)) {
+    int ex;
+    frexp(a, &ex); /* a = m 2^ex, 0.5 <= m < 1: leading bit at 2^(ex-1) */
+    q = ldexp(1.0, ex - 1 - 7);
+  } else {
+    q = ldexp(1.0, -133);
+  }
+  double r = nearbyint(a / q) * q;
+  if (r >= ldexp(1.0, 128)) return (uint16_t)(sign | 0x7f80);
+  float f = (float)r;
+  uint32_t u;
+  memcpy(&u, &f, sizeof u);
+  return (uint16_t)(sign | (u >> 16));
+}
+
+/* SiLU(v) = v * sigmoid(v) = v / (1 + e^{-v}), fp64. */
+double ora_silu(double v) { return v / (1.0 + exp(-v)); }
+
+/* The fused prologue over x [N][Ci][T][hw] (bf16 bits), with per-(n, c)
+ * fp32 scale s and shift t ([N][Ci]); u receives bf16 bits. */
+int ora_prologue_bf16(int64_t N, int64_t Ci, int64_t T, int64_t hw,
+                      const uint16_t* x, const float* s, const float* t,
+                      uint16_t* u) {
+  if (N < 0 || Ci < 0 || T < 0 || hw < 0) return -1;
+  if (N * Ci * T * hw == 0) return 0;
+  if (!x || !s || !t || !u) return -1;
+#pragma omp parallel for schedule(static)
+  for (int64_t nc = 0; nc < N * Ci; ++nc) {
+    double sc = (double)s[nc], sh = (double)t[nc];
+    for (int64_t i = nc * T * hw; i < (nc + 1) * T * hw; ++i)
+      u[i] = ora_round_bf16(ora_silu(widen(x, ORA_BF16, i) * sc + sh));
+  }
+  return 0;
 }

@@ -4,7 +4,9 @@ Each mutant below is a copy of the oracle's C source with one deliberate
 mistake (a dropped tap, a flipped sign in the source-frame index of Eq. 1,
 cache and chunk frames swapped, the bias added per tap, a transposed weight
 index, the wrong effective left pad of Eq. 3, the wrong cache rule, a wrong
-spatial pad sign, an off-by-one in Eq. 4, a missing route clause).  The copy
+spatial pad sign, an off-by-one in Eq. 4, a missing route clause; in the
+fused form's parts, bf16 ties rounded away from zero, one significand bit
+short, the sign of SiLU's exponent, the shift of the wrong channel).  The copy
 is compiled to a temporary library and the pin suite is run against it in a
 child process; every mutant must make the suite fail.  Nothing here touches
 the HIP library or the GPU.
@@ -39,7 +41,14 @@ MUTANTS = {
     "eq4_off_by_one": [("int64_t hi = Z - delta < To ? Z - delta : To;",
                         "int64_t hi = Z - delta - 1 < To ? Z - delta - 1 : To;")],
     "route_kt_clause_missing": [("else if (d->Kt < 2)", "else if (d->Kt < 1)")],
+    # the fused form's parts
+    "bf16_ties_away_from_zero": [("double r = nearbyint(a / q) * q;", "double r = round(a / q) * q;")],
+    "bf16_one_bit_short": [("q = ldexp(1.0, ex - 1 - 7);", "q = ldexp(1.0, ex - 1 - 6);")],
+    "silu_sign": [("return v / (1.0 + exp(-v));", "return v / (1.0 + exp(v));")],
+    "prologue_shift_of_next_channel": [("double sc = (double)s[nc], sh = (double)t[nc];",
+                                        "double sc = (double)s[nc], sh = (double)t[(nc + 1) % (N * Ci)];")],
 }
+PIN_FILES = ["test_oracle_pins.py", "test_oracle_fused_pins.py"]
 
 
 @pytest.mark.parametrize("name", sorted(MUTANTS))
@@ -55,6 +64,6 @@ def test_pins_catch_mutant(name, tmp_path):
                            "-ffp-contract=off", str(csrc), "-o", str(lib), "-lm"])
     env = dict(os.environ, C3C_ORACLE_LIB=str(lib), OMP_NUM_THREADS="2")
     r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
-                        os.path.join(ROOT, "tests", "test_oracle_pins.py")],
+                        *[os.path.join(ROOT, "tests", f) for f in PIN_FILES]],
                        cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
     assert r.returncode != 0, f"mutant {name} survived the pins:\n{r.stdout[-2000:]}"
