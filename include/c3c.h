@@ -247,6 +247,44 @@ int c3c_conv3d_causal_cached(c3c_ctx* ctx, const c3c_conv_desc* d,
                              const void* wpack, const void* bias, void* y,
                              void* cache_out, void* stream);
 
+/* ---------------------------------------------------------------- fused form */
+/* The same call with the neighbouring ops of a decoder residual block folded
+ * in (bf16 only).  Each part is optional:
+ *
+ *   prologue  the new chunk x is read as
+ *               u = RNE_bf16(SiLU(x * scale[n][ci] + shift[n][ci])),
+ *               SiLU(v) = v / (1 + e^-v), computed in fp32: a normalisation
+ *             whose statistics and affine the caller has folded into one
+ *             scale and shift per (batch element, input channel), then the
+ *             activation.  Zero padding applies to u (padded positions stay
+ *             0).  The cache holds activated frames: cache frames are read as
+ *             they are, and cache_out receives the last L frames of
+ *             [cache; u] -- what the cache of the convolution would hold in an
+ *             unfused pipeline.
+ *   epilogue  residual (y's layout and dtype) is added after the bias,
+ *             before the one rounding: y = RNE(conv + bias + residual).
+ *
+ * The paper's memory results (Sec. 6) and discussion (Sec. 7) name the
+ * temporary buffers around the lowering and point to buffer reuse and
+ * streamed accumulation; this form removes the activated-input tensor and
+ * the separate residual pass of an unfused block.
+ *
+ * scale, shift: device fp32 [N][Ci], both or neither (neither: u = x).
+ * residual: device, [N][Co][To][Ho][Wo] bf16, or NULL; it may be y itself
+ *   (in place) but may not otherwise overlap an output.
+ * Routing, counters, strict mode and the other arguments are those of
+ * c3c_conv3d_causal_cached.  With scale, shift and residual all NULL the
+ * call is exactly c3c_conv3d_causal_cached.
+ * EINVAL: as c3c_conv3d_causal_cached; dtype not bf16; exactly one of scale
+ * and shift NULL; scale, shift or residual overlapping an output (other than
+ * residual == y). */
+int c3c_conv3d_causal_cached_fused(c3c_ctx* ctx, const c3c_conv_desc* d,
+                                   const void* x, const void* cache,
+                                   const void* w, const void* wpack,
+                                   const void* bias, const float* scale,
+                                   const float* shift, const void* residual,
+                                   void* y, void* cache_out, void* stream);
+
 /* ---------------------------------------------------------------- counters */
 int c3c_counters_get(const c3c_ctx* ctx, c3c_counters* out);
 int c3c_counters_reset(c3c_ctx* ctx); /* also clears the shape histogram */

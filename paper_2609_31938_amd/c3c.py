@@ -72,6 +72,8 @@ lib.c3c_ctx_set_workspace.argtypes = [_vp, _vp, C.c_size_t]
 lib.c3c_weight_repack.argtypes = [_vp, _P(Desc), _vp, _vp, _vp]
 lib.c3c_weight_unpack.argtypes = [_P(Desc), _vp, _vp, _vp]
 lib.c3c_conv3d_causal_cached.argtypes = [_vp, _P(Desc), _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp]
+lib.c3c_conv3d_causal_cached_fused.argtypes = [_vp, _P(Desc), _vp, _vp, _vp, _vp, _vp, _vp, _vp,
+                                               _vp, _vp, _vp, _vp]
 lib.c3c_counters_get.argtypes = [_vp, _P(Counters)]
 lib.c3c_counters_reset.argtypes = [_vp]
 lib.c3c_fallback_shapes.argtypes = [_vp, _P(SigCount), C.c_int, _P(C.c_int)]
@@ -310,4 +312,34 @@ def conv3d_causal_cached(ctx, spec: dict, x, cache, w, wpack, bias, y=None, cach
         _ptr(bias, "bias", dtype, spec["Co"]) if spec["has_bias"] else None,
         _ptr(y, "y", dtype), _ptr(cache_out, "cache_out", dtype), _stream(stream))
     _raise(st, ctx, "c3c_conv3d_causal_cached")
+    return y, cache_out
+
+
+def conv3d_causal_cached_fused(ctx, spec: dict, x, cache, w, wpack, bias, scale=None, shift=None,
+                               residual=None, y=None, cache_out=None, stream=None):
+    """The fused residual-block form (bf16): the new chunk read as
+    RNE_bf16(SiLU(x * scale[n, ci] + shift[n, ci])) when scale / shift (fp32,
+    (N, Ci)) are given, residual (y's shape) added before the rounding.
+    ``residual`` may be ``y`` itself.  Returns (y, cache_out)."""
+    import torch
+    dtype = dtype_of(w)
+    To, Ho, Wo, L = output_dims(spec, dtype)
+    dev = w.device
+    if y is None:
+        y = torch.empty((spec["N"], spec["Co"], To, Ho, Wo), dtype=w.dtype, device=dev)
+    if cache_out is None:
+        cache_out = torch.empty((spec["N"], spec["Ci"], L, spec["H"], spec["W"]),
+                                dtype=w.dtype, device=dev)
+    hw = spec["H"] * spec["W"]
+    nc = spec["N"] * spec["Ci"]
+    st = lib.c3c_conv3d_causal_cached_fused(
+        ctx._h, C.byref(make_desc(spec, dtype)),
+        _ptr(x, "x", dtype, spec["N"] * spec["Ci"] * spec["T"] * hw),
+        _ptr(cache, "cache", dtype, spec["N"] * spec["Ci"] * spec["Tc"] * hw) if spec["Tc"] else None,
+        _ptr(w, "w", dtype), _ptr(wpack, "wpack", dtype),
+        _ptr(bias, "bias", dtype, spec["Co"]) if spec["has_bias"] else None,
+        _ptr(scale, "scale", "f32", nc), _ptr(shift, "shift", "f32", nc),
+        _ptr(residual, "residual", dtype, y.numel()),
+        _ptr(y, "y", dtype), _ptr(cache_out, "cache_out", dtype), _stream(stream))
+    _raise(st, ctx, "c3c_conv3d_causal_cached_fused")
     return y, cache_out

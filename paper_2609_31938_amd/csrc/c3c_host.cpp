@@ -312,9 +312,12 @@ int c3c_weight_unpack(const c3c_conv_desc* d, const void* wpack, void* w_out, vo
              : C3C_E_DEVICE;
 }
 
-int c3c_conv3d_causal_cached(c3c_ctx* ctx, const c3c_conv_desc* d, const void* x,
-                             const void* cache, const void* w, const void* wpack,
-                             const void* bias, void* y, void* cache_out, void* stream) {
+namespace {
+
+// One call, plain or fused (fu: the fused form's prologue / epilogue, or none).
+int run_call(c3c_ctx* ctx, const c3c_conv_desc* d, const void* x, const void* cache,
+             const void* w, const void* wpack, const void* bias, const Fuse& fu, void* y,
+             void* cache_out, void* stream) {
   if (!ctx) return C3C_E_INVAL;
   Geo g;
   const char* why = make_geo(d, &g);
@@ -346,6 +349,17 @@ int c3c_conv3d_causal_cached(c3c_ctx* ctx, const c3c_conv_desc* d, const void* x
       overlap(ctx->ws, wsb, w, wb) || overlap(ctx->ws, wsb, bias, bb) ||
       overlap(ctx->ws, wsb, y, yb) || overlap(ctx->ws, wsb, cache_out, ob))
     return fail(ctx, C3C_E_INVAL, "the context's workspace overlaps a tensor");
+  if (fu.any()) {
+    if (d->dtype != C3C_DTYPE_BF16) return fail(ctx, C3C_E_INVAL, "the fused form is bf16 only");
+    const int64_t sb = fu.pro() ? d->N * d->Ci * 4 : 0;
+    const int64_t rb = fu.residual ? yb : 0;
+    for (const void* p : {static_cast<const void*>(fu.scale), static_cast<const void*>(fu.shift)})
+      if (overlap(p, sb, y, yb) || overlap(p, sb, cache_out, ob) || overlap(p, sb, ctx->ws, wsb))
+        return fail(ctx, C3C_E_INVAL, "scale or shift overlaps an output");
+    if ((fu.residual != y && overlap(fu.residual, rb, y, yb)) || overlap(fu.residual, rb, cache_out, ob) ||
+        overlap(fu.residual, rb, ctx->ws, wsb))
+      return fail(ctx, C3C_E_INVAL, "residual overlaps an output other than y itself");
+  }
 
   const int reason = decide(g, ctx->mode);
   size_t pb = 0;
@@ -373,7 +387,7 @@ int c3c_conv3d_causal_cached(c3c_ctx* ctx, const c3c_conv_desc* d, const void* x
       e = hipErrorLaunchFailure;  // stands for a failure before any launch
     } else {
       e = launch_fast(g, x, cache, wpack, bias, y, cache_out, ctx->ws,
-                      static_cast<int64_t>(ctx->ws_bytes), s);
+                      static_cast<int64_t>(ctx->ws_bytes), s, fu);
     }
     if (e == hipSuccess) {
       ++ctx->ctr.fast;
@@ -395,10 +409,32 @@ int c3c_conv3d_causal_cached(c3c_ctx* ctx, const c3c_conv_desc* d, const void* x
   }
   ++ctx->ctr.fallback;
   record_shape(ctx, fb_reason, *d);
-  hipError_t e = launch_fallback(g, x, cache, w, bias, y, s);
-  if (e == hipSuccess) e = launch_cache_copy(g, x, cache, cache_out, s);
+  hipError_t e = launch_fallback(g, x, cache, w, bias, y, s, fu);
+  if (e == hipSuccess) e = launch_cache_copy(g, x, cache, cache_out, s, fu);
   if (e != hipSuccess) return fail(ctx, C3C_E_DEVICE, hipGetErrorString(e));
   return C3C_OK;
+}
+
+}  // namespace
+
+int c3c_conv3d_causal_cached(c3c_ctx* ctx, const c3c_conv_desc* d, const void* x,
+                             const void* cache, const void* w, const void* wpack,
+                             const void* bias, void* y, void* cache_out, void* stream) {
+  return run_call(ctx, d, x, cache, w, wpack, bias, Fuse{}, y, cache_out, stream);
+}
+
+int c3c_conv3d_causal_cached_fused(c3c_ctx* ctx, const c3c_conv_desc* d, const void* x,
+                                   const void* cache, const void* w, const void* wpack,
+                                   const void* bias, const float* scale, const float* shift,
+                                   const void* residual, void* y, void* cache_out,
+                                   void* stream) {
+  if (ctx && (scale == nullptr) != (shift == nullptr))
+    return fail(ctx, C3C_E_INVAL, "scale and shift are given together or not at all");
+  Fuse fu;
+  fu.scale = scale;
+  fu.shift = shift;
+  fu.residual = static_cast<const uint16_t*>(residual);
+  return run_call(ctx, d, x, cache, w, wpack, bias, fu, y, cache_out, stream);
 }
 
 int c3c_counters_get(const c3c_ctx* ctx, c3c_counters* out) {

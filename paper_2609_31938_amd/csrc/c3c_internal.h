@@ -39,26 +39,40 @@ struct PackDims {
 };
 PackDims pack_dims(const c3c_conv_desc& d);
 
+// The fused entry point's optional prologue and epilogue (bf16 calls only).
+// scale / shift ([N][Ci] fp32): new-chunk inputs are read as
+// RNE_bf16(SiLU(x * scale + shift)), padding stays 0, and frames copied into
+// the new cache from the chunk get the same transform.  residual (y's
+// layout) is added after the bias, before the one rounding.  Default: none.
+struct Fuse {
+  const float* scale = nullptr;
+  const float* shift = nullptr;
+  const uint16_t* residual = nullptr;
+  bool pro() const { return scale != nullptr; }
+  bool any() const { return scale != nullptr || residual != nullptr; }
+};
+
 hipError_t launch_repack(const Geo& g, const void* w, void* wpack, hipStream_t s);
 hipError_t launch_unpack(const Geo& g, const void* wpack, void* w, hipStream_t s);
 // ws / ws_bytes: the caller's split-K workspace (may be NULL / 0).
 hipError_t launch_fast(const Geo& g, const void* x, const void* cache, const void* wpack,
                        const void* bias, void* y, void* cache_out, void* ws, int64_t ws_bytes,
-                       hipStream_t s);
+                       hipStream_t s, const Fuse& fu = Fuse{});
 // bf16 fast kernel (conv_bf16.hip); writes cache_out itself when it can
 // (returns *cache_written = true), else the caller copies the cache.  Splits
 // the stages of a call too small to fill the device over several workgroups
 // when ws holds at least fast_bf16_workspace_bytes(g) bytes (16-byte aligned).
 hipError_t launch_fast_bf16(const Geo& g, const void* x, const void* cache, const void* wpack,
                             const void* bias, void* y, void* cache_out, void* ws,
-                            int64_t ws_bytes, bool* cache_written, hipStream_t s);
+                            int64_t ws_bytes, bool* cache_written, hipStream_t s,
+                            const Fuse& fu = Fuse{});
 // fp32 partial-sum bytes a bf16 fast call would split into (0: it runs unsplit)
 int64_t fast_bf16_workspace_bytes(const Geo& g);
 // fallback, pointwise case (pointwise.hip): 1x1x1, unit spatial stride, no
 // spatial padding, one group, bf16 / fp16, aligned buffers
 bool pointwise_eligible(const Geo& g, const void* x, const void* cache, const void* w, const void* y);
 hipError_t launch_pointwise(const Geo& g, const void* x, const void* cache, const void* w,
-                            const void* bias, void* y, hipStream_t s);
+                            const void* bias, void* y, hipStream_t s, const Fuse& fu = Fuse{});
 // compute units of the current device (256 when no device is visible)
 int64_t device_compute_units();
 // output channels per workgroup of the two bf16 1x1 kernels of the fast route
@@ -76,10 +90,10 @@ hipError_t launch_tap1x1(const Geo& g, const void* x, const void* cache, const v
 // temporal stride and dilation, any H * W and alignment.  The caller copies
 // the cache.
 hipError_t launch_fast_tap1x1(const Geo& g, const void* x, const void* cache, const void* wpack,
-                              const void* bias, void* y, hipStream_t s);
+                              const void* bias, void* y, hipStream_t s, const Fuse& fu = Fuse{});
 hipError_t launch_fallback(const Geo& g, const void* x, const void* cache, const void* w,
-                           const void* bias, void* y, hipStream_t s);
+                           const void* bias, void* y, hipStream_t s, const Fuse& fu = Fuse{});
 hipError_t launch_cache_copy(const Geo& g, const void* x, const void* cache, void* cache_out,
-                             hipStream_t s);
+                             hipStream_t s, const Fuse& fu = Fuse{});
 
 }  // namespace c3c

@@ -46,6 +46,7 @@
 #include <atomic>
 
 #include "c3c_internal.h"
+#include "fuse_dev.h"
 
 namespace c3c {
 namespace {
@@ -80,6 +81,11 @@ struct Args {
   // to part[sp][n][co][o][h][w]; splitk_reduce then adds them and the bias
   int splits;
   float* part;
+  // the fused form (FUSED instances; NULL when absent): per-(n, ci) scale and
+  // shift of the prologue, the residual added in the epilogue
+  const float* scale;
+  const float* shift;
+  const uint16_t* residual;
 };
 
 // 8 channel rows of 8 pixels (v[c] = pixels 0..7 of channel c) -> 8 pixel
@@ -103,7 +109,13 @@ __device__ inline void transpose8x8(const u32x4 (&v)[8], u32x4 (&o)[8]) {
 // SPLIT: the split-K instance (a stage range per workgroup, fp32 partial
 // sums out); a separate instance so that the unsplit kernel's register
 // allocation is not shaped by the split epilogue.
-template <int WCO, int WR, int WCF, int WAVES_CO, int WAVES_PX, int NBUF, bool ALIGNED, bool SPLIT>
+// FUSED: the fused form.  Each stage's scale / shift values load with its
+// activations; once the staged registers are complete (the top of step 7)
+// a stage whose frame comes from the new chunk gets the prologue, in place,
+// before both the LDS store and the cache store see the values; positions
+// outside the image keep their zero.  The residual joins the epilogue.
+template <int WCO, int WR, int WCF, int WAVES_CO, int WAVES_PX, int NBUF, bool ALIGNED, bool SPLIT,
+          bool FUSED = false>
 __global__ __launch_bounds__(64 * WAVES_CO * WAVES_PX, 1) void conv3d_bf16(Args a) {
   constexpr int NT = 64 * WAVES_CO * WAVES_PX;
   constexpr int BH = WR * WAVES_PX, BW = 16 * WCF;
@@ -237,11 +249,37 @@ __global__ __launch_bounds__(64 * WAVES_CO * WAVES_PX, 1) void conv3d_bf16(Args 
 
   u32x4 sv[TPT][8];
   uint16_t hv[HPT];
+  // FUSED: this thread's 8 task channels (8g + j, the same g for every task
+  // of a thread) and its halo channels, for the stage being loaded; batch
+  // element n's scale / shift with channels past Ci out of range (0)
+  float psc[8], psh[8], hsc[HPT], hsh[HPT];
+  bool ppro = false;
+  const __amdgpu_buffer_rsrc_t ssr = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<float*>(FUSED && a.scale ? a.scale + static_cast<int64_t>(n) * a.Ci : a.scale), 0,
+      FUSED && a.scale ? a.Ci * 4 : 0, 0x00020000);
+  const __amdgpu_buffer_rsrc_t shr = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<float*>(FUSED && a.shift ? a.shift + static_cast<int64_t>(n) * a.Ci : a.shift), 0,
+      FUSED && a.shift ? a.Ci * 4 : 0, 0x00020000);
 
   // part p of a stage's loads: channel rows 2p, 2p + 1 of every task for
   // p = 0..3, the halo columns for p = 4 (spread over five steps so that no
   // burst of loads sits in front of the weight loads that follow it)
   auto load_stage = [&](const Stage& st, int part) {
+    if (FUSED && part == 0) {
+      ppro = a.scale != nullptr && st.f >= a.Tc;
+      const uint32_t c8 = static_cast<uint32_t>(st.c0) + t_g8[0];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        psc[j] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(ssr, ppro ? (c8 + j) * 4u : OOB, 0, 0));
+        psh[j] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(shr, ppro ? (c8 + j) * 4u : OOB, 0, 0));
+      }
+#pragma unroll
+      for (int hh = 0; hh < HPT; ++hh) {
+        const uint32_t c = static_cast<uint32_t>(st.c0) + h_ch[hh];
+        hsc[hh] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(ssr, ppro ? c * 4u : OOB, 0, 0));
+        hsh[hh] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(shr, ppro ? c * 4u : OOB, 0, 0));
+      }
+    }
     if (part < 4)
 #pragma unroll
     for (int tt = 0; tt < TPT; ++tt) {
@@ -270,6 +308,31 @@ __global__ __launch_bounds__(64 * WAVES_CO * WAVES_PX, 1) void conv3d_bf16(Args 
     for (int hh = 0; hh < HPT; ++hh)
       hv[hh] = __builtin_amdgcn_raw_buffer_load_b16(
           st.rs, h_ok[hh] ? h_ch[hh] * st.cs + h_pix[hh] : OOB, 0, 0);
+  };
+
+  // FUSED: the prologue on the staged registers of a new-chunk stage (all
+  // selects, no branch).  A task is in the image when t_ok; without ALIGNED
+  // its pixels past W are padding too.
+  auto pro_stage = [&]() {
+    if constexpr (FUSED) {
+#pragma unroll
+      for (int tt = 0; tt < TPT; ++tt) {
+        const bool ok = ppro & t_ok[tt];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          if (ALIGNED) {
+            sv[tt][j] = fuse_seg8(sv[tt][j], psc[j], psh[j], ok);
+          } else {
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+              sv[tt][j][r] = fuse_pair(sv[tt][j][r], psc[j], psh[j], ok & (t_w[tt] + 2 * r < a.W),
+                                       ok & (t_w[tt] + 2 * r + 1 < a.W));
+          }
+        }
+      }
+#pragma unroll
+      for (int hh = 0; hh < HPT; ++hh) hv[hh] = fuse_one(hv[hh], hsc[hh], hsh[hh], ppro & h_ok[hh]);
+    }
   };
 
   // transpose the staged registers into LDS buffer `buf` (no branches:
@@ -384,6 +447,7 @@ __global__ __launch_bounds__(64 * WAVES_CO * WAVES_PX, 1) void conv3d_bf16(Args 
     load_w(cst.wbase, 0, wr[0]);
     load_w(cst.wbase, 1, wr[1]);
     for (int part = 0; part < 5; ++part) load_stage(cst, part);
+    pro_stage();
     if (cache_needed(cst, true)) cache_store(cst);
     store_stage(0);
     __syncthreads();
@@ -410,6 +474,7 @@ __global__ __launch_bounds__(64 * WAVES_CO * WAVES_PX, 1) void conv3d_bf16(Args 
     for (int ij = 0; ij < 9; ++ij) {
       // the cache write (rare, workgroup-uniform) is its own block ahead of
       // the scheduled region of step 7
+      if (FUSED && ij == 7) pro_stage();
       if (ij == 7 && cache_needed(nst_, s + 1 < cnt)) cache_store(nst_);
       // keep every LDS read inside its own step: re-reading is cheaper in
       // registers than keeping overlapping rows of neighbouring kh live
@@ -496,12 +561,26 @@ __global__ __launch_bounds__(64 * WAVES_CO * WAVES_PX, 1) void conv3d_bf16(Args 
     for (int pf = 0; pf < NPF; ++pf) {
       const int h = h0 + wpx * WR + pf / WCF, w = w0 + (pf % WCF) * 16 + 4 * (lane >> 4);
       if (co >= a.Co || h >= a.H || w >= a.W) continue;
+      uint16_t* dst = ybase + co * plane + static_cast<int64_t>(h) * a.W + w;
+      // FUSED: the residual at the same position, added before the rounding
+      f32x4 rr = {0.f, 0.f, 0.f, 0.f};
+      if (FUSED && a.residual) {
+        const uint16_t* rsrc = a.residual + (dst - a.y);
+        if (ALIGNED && w + 4 <= a.W) {
+          const uint2 r2 = *reinterpret_cast<const uint2*>(rsrc);
+          rr = f32x4{fuse_widen(r2.x & 0xffffu), fuse_widen(r2.x >> 16), fuse_widen(r2.y & 0xffffu),
+                     fuse_widen(r2.y >> 16)};
+        } else {
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            if (w + r < a.W) rr[r] = fuse_widen(rsrc[r]);
+        }
+      }
       // one round-to-nearest-even conversion per value (hardware, two at a time)
       const uint32_t v01 = __builtin_bit_cast(
-          uint32_t, __builtin_convertvector((f32x2{acc[cf][pf][0] + bb, acc[cf][pf][1] + bb}), bf16x2));
+          uint32_t, __builtin_convertvector((f32x2{acc[cf][pf][0] + bb + rr[0], acc[cf][pf][1] + bb + rr[1]}), bf16x2));
       const uint32_t v23 = __builtin_bit_cast(
-          uint32_t, __builtin_convertvector((f32x2{acc[cf][pf][2] + bb, acc[cf][pf][3] + bb}), bf16x2));
-      uint16_t* dst = ybase + co * plane + static_cast<int64_t>(h) * a.W + w;
+          uint32_t, __builtin_convertvector((f32x2{acc[cf][pf][2] + bb + rr[2], acc[cf][pf][3] + bb + rr[3]}), bf16x2));
       if (ALIGNED && w + 4 <= a.W) {
         *reinterpret_cast<uint2*>(dst) = make_uint2(v01, v23);
       } else {
@@ -522,7 +601,8 @@ __global__ __launch_bounds__(64 * WAVES_CO * WAVES_PX, 1) void conv3d_bf16(Args 
 template <bool VEC4>
 __global__ __launch_bounds__(256) void splitk_reduce(const float* __restrict__ part,
                                                      const uint16_t* __restrict__ bias,
-                                                     uint16_t* __restrict__ y, int64_t total,
+                                                     const uint16_t* residual,
+                                                     uint16_t* y, int64_t total,
                                                      int64_t plane, int Co, int splits,
                                                      int has_bias) {
   constexpr int V = VEC4 ? 4 : 1;
@@ -534,12 +614,18 @@ __global__ __launch_bounds__(256) void splitk_reduce(const float* __restrict__ p
       f32x4 v = *reinterpret_cast<const f32x4*>(part + i);
       for (int s = 1; s < splits; ++s)
         v += *reinterpret_cast<const f32x4*>(part + static_cast<int64_t>(s) * total + i);
+      if (residual) {  // the fused form's residual, after the split sums (y may be the residual)
+        const uint2 r2 = *reinterpret_cast<const uint2*>(residual + i);
+        v += f32x4{fuse_widen(r2.x & 0xffffu), fuse_widen(r2.x >> 16), fuse_widen(r2.y & 0xffffu),
+                   fuse_widen(r2.y >> 16)};
+      }
       const uint32_t v01 = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2{v[0] + bb, v[1] + bb}), bf16x2));
       const uint32_t v23 = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2{v[2] + bb, v[3] + bb}), bf16x2));
       *reinterpret_cast<uint2*>(y + i) = make_uint2(v01, v23);
     } else {
       float v = part[i];
       for (int s = 1; s < splits; ++s) v += part[static_cast<int64_t>(s) * total + i];
+      if (residual) v += fuse_widen(residual[i]);
       const uint32_t r = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2{v + bb, 0.f}), bf16x2));
       y[i] = static_cast<uint16_t>(r);
     }
@@ -568,7 +654,7 @@ void set_tiles(const Geo& g, int64_t bco, int64_t bh, int64_t bw, Plan* p) {
 }
 
 template <int WCO, int WR, int WCF, int WAVES_CO, int WAVES_PX, int NBUF>
-hipError_t run(const Geo& g, Args a, const Plan& p, bool aligned, hipStream_t s) {
+hipError_t run(const Geo& g, Args a, const Plan& p, bool aligned, bool fused, hipStream_t s) {
   a.tiles_co = static_cast<int>(p.tiles_co);
   a.tiles_w = static_cast<int>(p.tiles_w);
   a.tiles_h = static_cast<int>(p.tiles_h);
@@ -578,26 +664,26 @@ hipError_t run(const Geo& g, Args a, const Plan& p, bool aligned, hipStream_t s)
   a.nblocks = static_cast<int>(blocks);
   const dim3 grid(static_cast<unsigned>(blocks)), block(64 * WAVES_CO * WAVES_PX);
   const bool split = a.splits > 1;
-  if (aligned && !split)
-    hipLaunchKernelGGL((conv3d_bf16<WCO, WR, WCF, WAVES_CO, WAVES_PX, NBUF, true, false>), grid, block, 0, s, a);
-  else if (!split)
-    hipLaunchKernelGGL((conv3d_bf16<WCO, WR, WCF, WAVES_CO, WAVES_PX, NBUF, false, false>), grid, block, 0, s, a);
-  else if (aligned)
-    hipLaunchKernelGGL((conv3d_bf16<WCO, WR, WCF, WAVES_CO, WAVES_PX, NBUF, true, true>), grid, block, 0, s, a);
-  else
-    hipLaunchKernelGGL((conv3d_bf16<WCO, WR, WCF, WAVES_CO, WAVES_PX, NBUF, false, true>), grid, block, 0, s, a);
+#define C3C_BF16(AL, SP, FU)                                                                        \
+  if (aligned == AL && split == SP && fused == FU)                                                   \
+    hipLaunchKernelGGL((conv3d_bf16<WCO, WR, WCF, WAVES_CO, WAVES_PX, NBUF, AL, SP, FU>), grid, block, 0, s, a);
+  C3C_BF16(true, false, false) C3C_BF16(false, false, false) C3C_BF16(true, true, false)
+  C3C_BF16(false, true, false) C3C_BF16(true, false, true) C3C_BF16(false, false, true)
+  C3C_BF16(true, true, true) C3C_BF16(false, true, true)
+#undef C3C_BF16
   if (!split) return hipGetLastError();
   const int64_t plane = static_cast<int64_t>(a.To) * a.hw;
   const int64_t total = static_cast<int64_t>(a.N) * a.Co * plane;
   const bool vec4 = plane % 4 == 0 && (reinterpret_cast<uintptr_t>(a.y) & 7u) == 0;
   int64_t rb = (total / (vec4 ? 4 : 1) + 255) / 256;
   if (rb > 65536) rb = 65536;
-  if (vec4)
+  const uint16_t* res = fused ? a.residual : nullptr;
+  if (vec4 && (res == nullptr || (reinterpret_cast<uintptr_t>(res) & 7u) == 0))
     hipLaunchKernelGGL(splitk_reduce<true>, dim3(static_cast<unsigned>(rb)), dim3(256), 0, s, a.part,
-                       a.bias, a.y, total, plane, a.Co, a.splits, a.has_bias);
+                       a.bias, res, a.y, total, plane, a.Co, a.splits, a.has_bias);
   else
     hipLaunchKernelGGL(splitk_reduce<false>, dim3(static_cast<unsigned>(rb)), dim3(256), 0, s, a.part,
-                       a.bias, a.y, total, plane, a.Co, a.splits, a.has_bias);
+                       a.bias, res, a.y, total, plane, a.Co, a.splits, a.has_bias);
   return hipGetLastError();
 }
 
@@ -712,7 +798,7 @@ int64_t fast_bf16_workspace_bytes(const Geo& g) { return plan_bf16(g).part_bytes
 
 hipError_t launch_fast_bf16(const Geo& g, const void* x, const void* cache, const void* wpack,
                             const void* bias, void* y, void* cache_out, void* ws,
-                            int64_t ws_bytes, bool* cache_written, hipStream_t s) {
+                            int64_t ws_bytes, bool* cache_written, hipStream_t s, const Fuse& fu) {
   const PackDims p = pack_dims(g.d);
   Args a;
   a.x = static_cast<const uint16_t*>(x);
@@ -747,9 +833,14 @@ hipError_t launch_fast_bf16(const Geo& g, const void* x, const void* cache, cons
   a.has_bias = g.d.has_bias ? 1 : 0;
   a.write_cache = (g.L > 0 && cache_covered(g)) ? 1 : 0;
   *cache_written = a.write_cache != 0;
+  a.scale = fu.scale;
+  a.shift = fu.shift;
+  a.residual = fu.residual;
+  const bool fused = fu.any();
   const bool aligned = (g.d.W % 8 == 0) && (x == nullptr || aligned16(x)) &&
                        (cache == nullptr || aligned16(cache)) &&
-                       (cache_out == nullptr || aligned16(cache_out));
+                       (cache_out == nullptr || aligned16(cache_out)) &&
+                       (fu.residual == nullptr || (reinterpret_cast<uintptr_t>(fu.residual) & 7u) == 0);
   const Plan pl = plan_bf16(g);
   // split-K only with a large enough, 16-byte-aligned workspace; else unsplit
   const bool split = pl.splits > 1 && ws != nullptr && ws_bytes >= pl.part_bytes &&
@@ -757,11 +848,11 @@ hipError_t launch_fast_bf16(const Geo& g, const void* x, const void* cache, cons
   a.splits = split ? pl.splits : 1;
   a.part = split ? static_cast<float*>(ws) : nullptr;
   switch (pl.cfg) {
-    case CFG_C192: return run<6, 2, 4, 2, 2, 3>(g, a, pl, aligned, s);
-    case CFG_C96: return run<6, 2, 4, 1, 4, 2>(g, a, pl, aligned, s);
-    case CFG_C16: return run<1, 2, 4, 1, 4, 2>(g, a, pl, aligned, s);
-    case CFG_C160_4X80: return run<5, 2, 5, 2, 2, 3>(g, a, pl, aligned, s);
-    default: return run<5, 5, 2, 2, 2, 3>(g, a, pl, aligned, s);
+    case CFG_C192: return run<6, 2, 4, 2, 2, 3>(g, a, pl, aligned, fused, s);
+    case CFG_C96: return run<6, 2, 4, 1, 4, 2>(g, a, pl, aligned, fused, s);
+    case CFG_C16: return run<1, 2, 4, 1, 4, 2>(g, a, pl, aligned, fused, s);
+    case CFG_C160_4X80: return run<5, 2, 5, 2, 2, 3>(g, a, pl, aligned, fused, s);
+    default: return run<5, 5, 2, 2, 2, 3>(g, a, pl, aligned, fused, s);
   }
 }
 

@@ -7,6 +7,7 @@
 // right pad), and bf16 / fp16 / fp32 storage, accumulating in fp32.  Pointwise
 // (1x1x1) bf16 / fp16 calls go to the matrix-core kernel in pointwise.hip.
 #include "c3c_internal.h"
+#include "fuse_dev.h"
 
 #include <hip/hip_fp16.h>
 
@@ -38,6 +39,12 @@ struct FbArgs {
   int64_t p_l, ph, pw, groups;
   int64_t Z, To, Ho, Wo;
   int has_bias, is_f16;
+  // the fused form (bf16 only; NULL when absent): the prologue's per-(n, ci)
+  // scale and shift, applied to the new chunk's in-range values, and the
+  // residual added after the bias
+  const float* scale;
+  const float* shift;
+  const uint16_t* residual;
 };
 
 constexpr int FB_THREADS = 256;
@@ -142,11 +149,15 @@ __global__ __launch_bounds__(FB_THREADS) void fallback_conv3d(FbArgs a, const T*
                                               : x + ((n * a.Ci + cin) * a.T + (tz - a.Tc)) * hw;
         const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
             const_cast<T*>(plane), 0, fok ? plane_bytes : 0, 0x00020000);
+        // fused prologue on values of the new chunk (tz >= Tc); padding stays 0
+        const bool pro = a.scale != nullptr && fok && tz >= a.Tc;
+        const float psc = pro ? a.scale[n * a.Ci + cin] : 0.f, psh = pro ? a.shift[n * a.Ci + cin] : 0.f;
 #pragma unroll
         for (int q = 0; q < FB_PPT; ++q) {
           const int hz = hb[q] + i * dh, wz = wb[q] + j * dw;
           const bool ok = live[q] & (hz >= 0) & (hz < H) & (wz >= 0) & (wz < W);
           v[u][q] = Buf<T>::load(rs, ok ? static_cast<uint32_t>((hz * W + wz) * esz) : OOB, a.is_f16);
+          if (pro && ok) v[u][q] = fuse_value(v[u][q], psc, psh);
         }
         if (++j == Kw) {
           j = 0;
@@ -189,14 +200,16 @@ __global__ __launch_bounds__(FB_THREADS) void fallback_conv3d(FbArgs a, const T*
       const int64_t co = co0 + c;
       float v = acc[q][c];
       if (a.has_bias) v += load_f(bias, co, a.is_f16);  // bias added once, last
-      store_f(y, ((n * a.Co + co) * a.To + t) * hwo + p, v, a.is_f16);
+      const int64_t yi = ((n * a.Co + co) * a.To + t) * hwo + p;
+      if (a.residual) v += fuse_widen(a.residual[yi]);  // fused residual, before the rounding
+      store_f(y, yi, v, a.is_f16);
     }
   }
 }
 
 template <typename T>
 hipError_t launch_fb(const Geo& g, const void* x, const void* cache, const void* w,
-                     const void* bias, void* y, hipStream_t s) {
+                     const void* bias, void* y, hipStream_t s, const Fuse& fu) {
   const c3c_conv_desc& d = g.d;
   FbArgs a;
   a.N = d.N; a.Ci = d.Ci; a.Co = d.Co; a.T = d.T; a.Tc = d.Tc; a.H = d.H; a.W = d.W;
@@ -207,6 +220,9 @@ hipError_t launch_fb(const Geo& g, const void* x, const void* cache, const void*
   a.Z = g.Z; a.To = g.To; a.Ho = g.Ho; a.Wo = g.Wo;
   a.has_bias = d.has_bias ? 1 : 0;
   a.is_f16 = d.dtype == C3C_DTYPE_F16;
+  a.scale = fu.scale;
+  a.shift = fu.shift;
+  a.residual = fu.residual;
   const int64_t cog = d.Co / d.groups;
   const int64_t gx = (g.Ho * g.Wo + FB_THREADS * FB_PPT - 1) / (FB_THREADS * FB_PPT);
   const int64_t gy = d.groups * ((cog + FB_COB - 1) / FB_COB);
@@ -253,21 +269,70 @@ hipError_t launch_cc(const Geo& g, const void* x, const void* cache, void* out, 
   return hipGetLastError();
 }
 
+// The same copy for the fused form: planes that come from the new chunk get
+// the prologue (bf16), planes from the old cache are copied as they are.
+// VEC: 8 elements per step (16-byte units), else one.
+template <bool VEC>
+__global__ __launch_bounds__(256) void cache_copy_pro(const uint16_t* __restrict__ x,
+                                                      const uint16_t* __restrict__ cache,
+                                                      uint16_t* __restrict__ out,
+                                                      const float* __restrict__ scale,
+                                                      const float* __restrict__ shift, int64_t planes,
+                                                      int64_t hw, int64_t L, int64_t T, int64_t Tc,
+                                                      int64_t Z) {
+  const int64_t units = VEC ? hw / 8 : hw;
+  for (int64_t pl = blockIdx.y; pl < planes; pl += gridDim.y) {
+    const int64_t j = pl % L, nc = pl / L;  // nc = n * Ci + c
+    const int64_t f = Z - L + j;
+    const bool from_x = f >= Tc;
+    const uint16_t* src = from_x ? x + (nc * T + (f - Tc)) * hw : cache + (nc * Tc + f) * hw;
+    const float s = from_x ? scale[nc] : 0.f, t = from_x ? shift[nc] : 0.f;
+    uint16_t* dst = out + pl * hw;
+    for (int64_t u = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x; u < units;
+         u += static_cast<int64_t>(gridDim.x) * 256) {
+      if (VEC) {
+        const fuse_u32x4 v = reinterpret_cast<const fuse_u32x4*>(src)[u];
+        reinterpret_cast<fuse_u32x4*>(dst)[u] = from_x ? fuse_seg8(v, s, t, true) : v;
+      } else {
+        const uint16_t v = src[u];
+        dst[u] = from_x ? fuse_one(v, s, t, true) : v;
+      }
+    }
+  }
+}
+
 bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
 }  // namespace
 
 hipError_t launch_fallback(const Geo& g, const void* x, const void* cache, const void* w,
-                           const void* bias, void* y, hipStream_t s) {
+                           const void* bias, void* y, hipStream_t s, const Fuse& fu) {
   if (g.To == 0) return hipSuccess;
-  if (pointwise_eligible(g, x, cache, w, y)) return launch_pointwise(g, x, cache, w, bias, y, s);
-  if (g.d.dtype == C3C_DTYPE_F32) return launch_fb<float>(g, x, cache, w, bias, y, s);
-  return launch_fb<uint16_t>(g, x, cache, w, bias, y, s);
+  // the pointwise kernel's aligned epilogue also reads the residual 8 bytes at a time
+  if (pointwise_eligible(g, x, cache, w, y) &&
+      (fu.residual == nullptr || (reinterpret_cast<uintptr_t>(fu.residual) & 7) == 0))
+    return launch_pointwise(g, x, cache, w, bias, y, s, fu);
+  if (g.d.dtype == C3C_DTYPE_F32) return launch_fb<float>(g, x, cache, w, bias, y, s, fu);
+  return launch_fb<uint16_t>(g, x, cache, w, bias, y, s, fu);
 }
 
 hipError_t launch_cache_copy(const Geo& g, const void* x, const void* cache, void* cache_out,
-                             hipStream_t s) {
+                             hipStream_t s, const Fuse& fu) {
   if (g.L == 0) return hipSuccess;
+  if (fu.pro() && g.d.T > 0) {
+    const c3c_conv_desc& d = g.d;
+    const int64_t hw = d.H * d.W, planes = d.N * d.Ci * g.L;
+    const bool vec = hw % 8 == 0 && aligned(cache_out, 16) && aligned(x, 16) &&
+                     (cache == nullptr || aligned(cache, 16));
+    int64_t gx = ((vec ? hw / 8 : hw) + 255) / 256;
+    if (gx > 4096) gx = 4096;
+    const int64_t gy = planes < 65535 ? planes : 65535;
+    auto k = vec ? cache_copy_pro<true> : cache_copy_pro<false>;
+    hipLaunchKernelGGL(k, dim3(gx, gy), dim3(256), 0, s, static_cast<const uint16_t*>(x),
+                       static_cast<const uint16_t*>(cache), static_cast<uint16_t*>(cache_out),
+                       fu.scale, fu.shift, planes, hw, g.L, d.T, d.Tc, g.Z);
+    return hipGetLastError();
+  }
   const int64_t plane_bytes = g.d.H * g.d.W * g.elem;
   auto fits = [&](size_t a) {
     return plane_bytes % static_cast<int64_t>(a) == 0 && aligned(cache_out, a) &&

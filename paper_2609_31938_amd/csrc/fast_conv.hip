@@ -304,7 +304,7 @@ hipError_t launch_unpack(const Geo& g, const void* wpack, void* w, hipStream_t s
 
 hipError_t launch_fast(const Geo& g, const void* x, const void* cache, const void* wpack,
                        const void* bias, void* y, void* cache_out, void* ws, int64_t ws_bytes,
-                       hipStream_t s) {
+                       hipStream_t s, const Fuse& fu) {
   const PackDims p = pack_dims(g.d);
   FastArgs a;
   a.x = x; a.cache = cache; a.wpack = wpack; a.bias = bias; a.y = y;
@@ -323,24 +323,25 @@ hipError_t launch_fast(const Geo& g, const void* x, const void* cache, const voi
       // channels alike (measured: about 8% at Co = 768); the 4-wave kernel
       // (192-channel tiles) wins where it pads at least 10% fewer channels
       // (Co = 384: 384 against 480) and its 192 x 320 tiles still give every
-      // compute unit half a workgroup.
+      // compute unit half a workgroup.  The fused form (prologue / residual)
+      // is in the pointwise kernel only.
       const int64_t pad_tap = (g.d.Co + kTap1x1TileCo - 1) / kTap1x1TileCo * kTap1x1TileCo;
       const int64_t pad_pw = (g.d.Co + kPointwiseTileCo - 1) / kPointwiseTileCo * kPointwiseTileCo;
-      if (10 * pad_tap <= 9 * pad_pw && tap1x1_eligible(g, x, cache, y) &&
+      if (!fu.any() && 10 * pad_tap <= 9 * pad_pw && tap1x1_eligible(g, x, cache, y) &&
           2 * tap1x1_blocks(g) >= device_compute_units())
         e = launch_tap1x1(g, x, cache, wpack, bias, y, s);
       else
-        e = launch_fast_tap1x1(g, x, cache, wpack, bias, y, s);
+        e = launch_fast_tap1x1(g, x, cache, wpack, bias, y, s, fu);
     } else {
       bool written = false;
-      e = launch_fast_bf16(g, x, cache, wpack, bias, y, cache_out, ws, ws_bytes, &written, s);
+      e = launch_fast_bf16(g, x, cache, wpack, bias, y, cache_out, ws, ws_bytes, &written, s, fu);
       if (e != hipSuccess || written) return e;
     }
   } else {
     e = one ? run_fast<float, 1, 2, 1, 4, 4, 2, 1>(g, a, s) : run_fast<float, 1, 2, 1, 4, 4, 2, 3>(g, a, s);
   }
   if (e != hipSuccess) return e;
-  return launch_cache_copy(g, x, cache, cache_out, s);
+  return launch_cache_copy(g, x, cache, cache_out, s, fu);
 }
 
 }  // namespace c3c

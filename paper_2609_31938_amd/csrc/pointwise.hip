@@ -28,6 +28,7 @@
 // past the tensor) but only feed outputs that are never stored: a 1x1 kernel
 // maps each output pixel to the same input pixel.
 #include "c3c_internal.h"
+#include "fuse_dev.h"
 
 namespace c3c {
 namespace {
@@ -77,6 +78,10 @@ struct PwArgs {
   int chunks, px_tiles, co_tiles, cofrags;
   uint32_t w_bytes;
   int has_bias;
+  // the fused form (FUSED instances; NULL when absent)
+  const float* scale;
+  const float* shift;
+  const uint16_t* residual;
 };
 
 __device__ inline uint16_t to_bf16(float f) {
@@ -107,7 +112,11 @@ __device__ inline f32x4 mma(i16x8 a, u32x4 b, f32x4 c) {
 // w[co][ci] (fallback, Kt = 1).  ALIGNED: every channel plane starts on a
 // 16-byte boundary (H * W a multiple of 8, aligned pointers); else the
 // activations are read 2 bytes at a time and the outputs stored one by one.
-template <bool F16, int PD, bool PACKED, bool ALIGNED, int PW_NPF>
+// FUSED (bf16): the fused form's prologue on stages whose frame comes from
+// the new chunk (applied to the staged registers before they go to LDS; a
+// 1x1 kernel has no spatial padding, and pixels past the plane only feed
+// outputs that are never stored) and its residual in the epilogue.
+template <bool F16, int PD, bool PACKED, bool ALIGNED, int PW_NPF, bool FUSED = false>
 __global__ __launch_bounds__(PW_NT, 1) void pointwise_conv(PwArgs a) {
   constexpr int PW_PX = pw_px(PW_NPF), PW_PITCH = pw_pitch(PW_NPF);
   constexpr int PW_WOFF = pw_woff(PW_NPF), PW_BUF = pw_buf(PW_NPF);
@@ -198,9 +207,27 @@ __global__ __launch_bounds__(PW_NT, 1) void pointwise_conv(PwArgs a) {
   struct Chunk {
     u32x4 x[SEG];
     u32x4 w[PW_WPT];
+    float psc, psh;  // FUSED: this thread's channel's scale and shift
+    bool pro;        // FUSED: the stage's frame comes from the new chunk
   };
+  // FUSED: scale / shift of batch element n, channels past Ci read as 0
+  const __amdgpu_buffer_rsrc_t ssr = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<float*>(FUSED && a.scale ? a.scale + static_cast<int64_t>(n) * a.Ci : a.scale), 0,
+      FUSED && a.scale ? a.Ci * 4 : 0, 0x00020000);
+  const __amdgpu_buffer_rsrc_t shr = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<float*>(FUSED && a.shift ? a.shift + static_cast<int64_t>(n) * a.Ci : a.shift), 0,
+      FUSED && a.shift ? a.Ci * 4 : 0, 0x00020000);
   auto load_chunk = [&](int st_, Chunk& ck) {
     const StageSrc sr = stage_src(st_);
+    if constexpr (FUSED) {
+      // the prologue applies to the new chunk's frames only
+      const int k = k_lo + (ntap > 0 ? st_ / a.chunks : 0);
+      const bool from_x = st_ < nst && t * a.st + k * a.dt - a.p_l >= a.Tc;
+      const uint32_t co = static_cast<uint32_t>((ntap > 0 ? st_ % a.chunks : 0) * PW_K + sch) * 4u;
+      ck.pro = from_x && a.scale != nullptr;
+      ck.psc = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(ssr, from_x ? co : OOB, 0, 0));
+      ck.psh = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(shr, from_x ? co : OOB, 0, 0));
+    }
     const uint32_t soff = static_cast<uint32_t>(sch) * sr.cs + static_cast<uint32_t>(spx) * 2u;
     if constexpr (ALIGNED) {
 #pragma unroll
@@ -242,7 +269,11 @@ __global__ __launch_bounds__(PW_NT, 1) void pointwise_conv(PwArgs a) {
   auto store_chunk = [&](const Chunk& ck, int buf) {
     unsigned char* base = lds + buf * PW_BUF;
 #pragma unroll
-    for (int h = 0; h < SEG; ++h) *reinterpret_cast<u32x4*>(base + slds + 256 * h) = ck.x[h];
+    for (int h = 0; h < SEG; ++h) {
+      // FUSED: a cache frame (or no prologue) is kept as loaded
+      const u32x4 v = FUSED ? fuse_seg8(ck.x[h], ck.psc, ck.psh, ck.pro) : ck.x[h];
+      *reinterpret_cast<u32x4*>(base + slds + 256 * h) = v;
+    }
 #pragma unroll
     for (int i = 0; i < PW_WPT; ++i) {
       if constexpr (PACKED) {
@@ -321,9 +352,26 @@ __global__ __launch_bounds__(PW_NT, 1) void pointwise_conv(PwArgs a) {
 #pragma unroll
     for (int pf = 0; pf < PW_NPF; ++pf) {
       const int p = px0 + wpx * 16 * PW_NPF + pf * 16 + 4 * g;
+      float rr[4] = {0.f, 0.f, 0.f, 0.f};
+      if (FUSED && a.residual) {
+        // fused residual, added before the one rounding
+        const uint16_t* rrow = a.residual + (yrow - a.y);
+        if (ALIGNED && p + 4 <= a.hw) {
+          const uint2 r2 = *reinterpret_cast<const uint2*>(rrow + p);
+          rr[0] = fuse_widen(r2.x & 0xffffu);
+          rr[1] = fuse_widen(r2.x >> 16);
+          rr[2] = fuse_widen(r2.y & 0xffffu);
+          rr[3] = fuse_widen(r2.y >> 16);
+        } else {
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            if (p + r < a.hw) rr[r] = fuse_widen(rrow[p + r]);
+        }
+      }
       uint16_t v[4];
 #pragma unroll
-      for (int r = 0; r < 4; ++r) v[r] = F16 ? to_f16(acc[cf][pf][r] + bb) : to_bf16(acc[cf][pf][r] + bb);
+      for (int r = 0; r < 4; ++r)
+        v[r] = F16 ? to_f16(acc[cf][pf][r] + bb + rr[r]) : to_bf16(acc[cf][pf][r] + bb + rr[r]);
       if (ALIGNED && p + 4 <= a.hw) {
         *reinterpret_cast<uint2*>(yrow + p) = make_uint2(v[0] | (static_cast<uint32_t>(v[1]) << 16),
                                                         v[2] | (static_cast<uint32_t>(v[3]) << 16));
@@ -364,7 +412,7 @@ namespace {
 // count of any output frame least (4, 3 or 2), the template instance by
 // element type, weight layout and alignment
 template <bool PACKED>
-hipError_t launch_pw(const Geo& g, PwArgs a, bool f16, bool al, hipStream_t s) {
+hipError_t launch_pw(const Geo& g, PwArgs a, bool f16, bool al, hipStream_t s, bool fused) {
   const c3c_conv_desc& d = g.d;
   a.co_tiles = static_cast<int>((d.Co + PW_CO - 1) / PW_CO);
   // Fast route, aligned: 512-pixel workgroups (twice the products per
@@ -400,18 +448,22 @@ hipError_t launch_pw(const Geo& g, PwArgs a, bool f16, bool al, hipStream_t s) {
       if ((nst + cand - 1) / cand * cand < (nst + pd - 1) / pd * pd) pd = cand;
   }
   const dim3 grid(static_cast<unsigned>(blocks)), block(PW_NT);
-#define C3C_PW(F, P, A, NPF)                                                                   \
-  if (f16 == F && pd == P && al == A && (NPF == 8) == wide) {                                   \
-    hipLaunchKernelGGL((pointwise_conv<F, P, PACKED, A, NPF>), grid, block, 0, s, a);          \
+#define C3C_PW(F, P, A, NPF, FU)                                                               \
+  if (f16 == F && pd == P && al == A && (NPF == 8) == wide && fused == FU) {                    \
+    hipLaunchKernelGGL((pointwise_conv<F, P, PACKED, A, NPF, FU>), grid, block, 0, s, a);      \
     return hipGetLastError();                                                                  \
   }
   if constexpr (PACKED) {  // fast route: bf16, any alignment
-    C3C_PW(false, 2, true, 4) C3C_PW(false, 3, true, 4) C3C_PW(false, 4, true, 4)
-    C3C_PW(false, 2, false, 4) C3C_PW(false, 3, false, 4) C3C_PW(false, 4, false, 4)
-    C3C_PW(false, 2, true, 8)
+    C3C_PW(false, 2, true, 4, false) C3C_PW(false, 3, true, 4, false) C3C_PW(false, 4, true, 4, false)
+    C3C_PW(false, 2, false, 4, false) C3C_PW(false, 3, false, 4, false) C3C_PW(false, 4, false, 4, false)
+    C3C_PW(false, 2, true, 8, false)
+    C3C_PW(false, 2, true, 4, true) C3C_PW(false, 3, true, 4, true) C3C_PW(false, 4, true, 4, true)
+    C3C_PW(false, 2, false, 4, true) C3C_PW(false, 3, false, 4, true) C3C_PW(false, 4, false, 4, true)
+    C3C_PW(false, 2, true, 8, true)
   } else {  // fallback: bf16 / fp16, aligned (pointwise_eligible)
-    C3C_PW(false, 2, true, 4) C3C_PW(false, 3, true, 4) C3C_PW(false, 4, true, 4)
-    C3C_PW(true, 2, true, 4) C3C_PW(true, 3, true, 4) C3C_PW(true, 4, true, 4)
+    C3C_PW(false, 2, true, 4, false) C3C_PW(false, 3, true, 4, false) C3C_PW(false, 4, true, 4, false)
+    C3C_PW(true, 2, true, 4, false) C3C_PW(true, 3, true, 4, false) C3C_PW(true, 4, true, 4, false)
+    C3C_PW(false, 2, true, 4, true) C3C_PW(false, 3, true, 4, true) C3C_PW(false, 4, true, 4, true)
   }
 #undef C3C_PW
   return hipErrorInvalidValue;
@@ -438,22 +490,28 @@ PwArgs common_args(const Geo& g, const void* x, const void* cache, const void* b
   a.Kt = static_cast<int>(d.Kt);
   a.chunks = static_cast<int>((d.Ci + PW_K - 1) / PW_K);
   a.has_bias = d.has_bias ? 1 : 0;
+  a.scale = a.shift = nullptr;
+  a.residual = nullptr;
   return a;
 }
 
 }  // namespace
 
 hipError_t launch_pointwise(const Geo& g, const void* x, const void* cache, const void* w,
-                            const void* bias, void* y, hipStream_t s) {
+                            const void* bias, void* y, hipStream_t s, const Fuse& fu) {
   PwArgs a = common_args(g, x, cache, bias, y);
   a.w = static_cast<const uint16_t*>(w);
   a.w_bytes = static_cast<uint32_t>(g.d.Co * g.d.Ci * 2);
   a.cofrags = 0;
-  return launch_pw<false>(g, a, g.d.dtype == C3C_DTYPE_F16, true, s);
+  a.scale = fu.scale;
+  a.shift = fu.shift;
+  a.residual = fu.residual;
+  // launch_fallback checked the residual's 8-byte alignment
+  return launch_pw<false>(g, a, g.d.dtype == C3C_DTYPE_F16, true, s, fu.any());
 }
 
 hipError_t launch_fast_tap1x1(const Geo& g, const void* x, const void* cache, const void* wpack,
-                              const void* bias, void* y, hipStream_t s) {
+                              const void* bias, void* y, hipStream_t s, const Fuse& fu) {
   const c3c_conv_desc& d = g.d;
   const PackDims p = pack_dims(d);
   // 32-bit buffer offsets: one 32-channel chunk of a source frame and the
@@ -465,9 +523,12 @@ hipError_t launch_fast_tap1x1(const Geo& g, const void* x, const void* cache, co
   a.w = static_cast<const uint16_t*>(wpack);
   a.w_bytes = static_cast<uint32_t>(p.elems() * 2);
   a.cofrags = static_cast<int>(p.cofrags);
+  a.scale = fu.scale;
+  a.shift = fu.shift;
+  a.residual = fu.residual;
   const bool al = (d.H * d.W) % 8 == 0 && aligned(x, 16) && (cache == nullptr || aligned(cache, 16)) &&
-                  aligned(y, 8);
-  return launch_pw<true>(g, a, false, al, s);
+                  aligned(y, 8) && (fu.residual == nullptr || aligned(fu.residual, 8));
+  return launch_pw<true>(g, a, false, al, s, fu.any());
 }
 
 }  // namespace c3c

@@ -6,7 +6,10 @@ the convolution's arithmetic.
 
 Distributions (the decoder-layer stand-ins; no model weights are used):
   x ~ N(0, 1),  w ~ N(0, 1 / (Ci * Kt * Kh * Kw)),  b ~ N(0, 0.1)  (variance),
-drawn in fp32 and rounded to nearest-even into the call's dtype.  Each tensor
+drawn in fp32 and rounded to nearest-even into the call's dtype.  The fused
+form's extra operands: scale ~ 1 + N(0, 0.2^2) and shift ~ N(0, 0.5^2) per
+(batch element, input channel), fp32 (a folded normalisation's scale and
+shift), and a residual ~ N(0, 1) shaped like the output.  Each tensor
 has its own seed, derived from (workload, layer, tensor, chunk); weights and
 bias use chunk 0 so that a layer keeps its weights over a stream.
 """
@@ -18,6 +21,7 @@ import math
 import numpy as np
 
 TENSOR_X, TENSOR_W, TENSOR_B = 0, 1, 2
+TENSOR_SCALE, TENSOR_SHIFT, TENSOR_RES = 3, 4, 5
 
 
 def spec(N=1, Ci=1, Co=1, T=1, Tc=0, H=1, W=1, Kt=3, Kh=3, Kw=3,
@@ -79,6 +83,20 @@ def chunk_input(sp: dict, dtype: str, workload: int, layer: int, chunk: int,
     """x ~ N(0, 1) for one chunk, shaped (N, Ci, T, H, W)."""
     return randn((sp["N"], sp["Ci"], sp["T"], sp["H"], sp["W"]),
                  seed_of(workload, layer, TENSOR_X, chunk), 1.0, dtype, device)
+
+
+def affine_inputs(sp: dict, workload: int, layer: int, chunk: int, device="cpu"):
+    """(scale, shift), fp32 (N, Ci): 1 + N(0, 0.04) and N(0, 0.25)."""
+    shape = (sp["N"], sp["Ci"])
+    scale = randn(shape, seed_of(workload, layer, TENSOR_SCALE, chunk), 0.2, "f32", device)
+    scale.add_(1.0)
+    shift = randn(shape, seed_of(workload, layer, TENSOR_SHIFT, chunk), 0.5, "f32", device)
+    return scale, shift
+
+
+def residual_input(shape, dtype: str, workload: int, layer: int, chunk: int, device="cpu"):
+    """A residual ~ N(0, 1) of the given (output) shape."""
+    return randn(shape, seed_of(workload, layer, TENSOR_RES, chunk), 1.0, dtype, device)
 
 
 def zero_cache(sp: dict, dtype: str, device="cpu"):

@@ -33,7 +33,7 @@ def test_every_declared_symbol_is_exported():
         "c3c_weight_pack_bytes", "c3c_weight_repack", "c3c_weight_unpack",
         "c3c_conv3d_causal_cached", "c3c_counters_get", "c3c_counters_reset",
         "c3c_fallback_shapes", "c3c_strerror", "c3c_last_error",
-        "c3c_workspace_bytes", "c3c_ctx_set_workspace"])
+        "c3c_workspace_bytes", "c3c_ctx_set_workspace", "c3c_conv3d_causal_cached_fused"])
     for n in names:
         assert hasattr(c3c.lib, n), n
 
@@ -234,3 +234,46 @@ def test_workspace_overlapping_a_tensor_is_rejected():
         assert _call(ctx, sp) == c3c.E_INVAL, name
         assert "workspace" in ctx.last_error
     assert ctx.counters()["calls"] == 0
+
+
+# ---------------------------------------------------------------------------
+# the fused entry point: argument checks (fake addresses, no device work)
+# ---------------------------------------------------------------------------
+
+FAKE_FUSE = {"scale": 0x80000000, "shift": 0x90000000, "res": 0xa0000000}
+
+
+def _fcall(ctx, sp, dtype="bf16", **over):
+    p = dict(FAKE, **FAKE_FUSE)
+    p.update(over)
+    return c3c.lib.c3c_conv3d_causal_cached_fused(
+        ctx._h if ctx else None, C.byref(c3c.make_desc(sp, dtype)), p["x"], p["cache"], p["w"],
+        p["wpack"], p["b"], p["scale"], p["shift"], p["res"], p["y"], p["co"], None)
+
+
+@no_gpu
+def test_fused_call_argument_checks():
+    sp = spec(N=1, Ci=4, Co=4, T=2, Tc=2, H=8, W=8)
+    # strict + forced fallback: every valid call is rejected before device work
+    ctx = c3c.Context(c3c.MODE_STRICT | c3c.MODE_FORCE_FALLBACK)
+    assert _fcall(None, sp) == c3c.E_INVAL
+    assert _fcall(ctx, sp, shift=None) == c3c.E_INVAL
+    assert "together" in ctx.last_error
+    assert _fcall(ctx, sp, scale=None) == c3c.E_INVAL
+    assert _fcall(ctx, sp, dtype="f32") == c3c.E_INVAL
+    assert "bf16" in ctx.last_error
+    assert _fcall(ctx, sp, dtype="f32", scale=None, shift=None) == c3c.E_INVAL  # residual alone
+    assert _fcall(ctx, sp, scale=FAKE["y"]) == c3c.E_INVAL
+    assert _fcall(ctx, sp, shift=FAKE["co"] + 4) == c3c.E_INVAL
+    assert _fcall(ctx, sp, res=FAKE["y"] + 2) == c3c.E_INVAL   # partial overlap with y
+    assert _fcall(ctx, sp, res=FAKE["co"]) == c3c.E_INVAL
+    assert _fcall(ctx, sp, y=FAKE["x"]) == c3c.E_INVAL          # the plain call's checks hold
+    assert ctx.counters()["calls"] == 0
+    # valid: full form, in place (residual == y), prologue only, residual only, plain
+    assert _fcall(ctx, sp) == c3c.E_UNSUPPORTED
+    assert _fcall(ctx, sp, res=FAKE["y"]) == c3c.E_UNSUPPORTED
+    assert _fcall(ctx, sp, res=None) == c3c.E_UNSUPPORTED
+    assert _fcall(ctx, sp, scale=None, shift=None) == c3c.E_UNSUPPORTED
+    assert _fcall(ctx, sp, scale=None, shift=None, res=None) == c3c.E_UNSUPPORTED
+    c = ctx.counters()
+    assert c["calls"] == 5 and c["strict_rejects"] == 5
