@@ -51,6 +51,10 @@ def main():
     ap.add_argument("--layer", default=None,
                     help="time only this layer of the workload (for per-layer profiles); "
                          "the JSON line then covers that layer alone")
+    ap.add_argument("--fused-block", action="store_true",
+                    help="time the fused residual-block form on each layer of the workload "
+                         "against the plain call and against the unfused pipeline (prologue "
+                         "and residual add as separate torch ops) and exit")
     ap.add_argument("--gemm-reference", action="store_true",
                     help="time the vendor bf16 GEMM (torch.matmul) on square and "
                          "conv-shaped problems and exit: what the matrix cores reach "
@@ -69,6 +73,9 @@ def main():
         return
     if args.gemm_reference:
         gemm_reference()
+        return
+    if args.fused_block:
+        fused_block(args.workload, args.steps)
         return
 
     wl = inputs.WORKLOADS[args.workload]
@@ -231,6 +238,88 @@ def algorithmic_bytes(sp, dtype):
     n_w = sp["Co"] * (sp["Ci"] // sp["groups"]) * sp["Kt"] * sp["Kh"] * sp["Kw"]
     n_out = sp["N"] * sp["Co"] * To * Ho * Wo + sp["N"] * sp["Ci"] * L * hw
     return es * (n_in + n_w + sp["Co"] * sp["has_bias"] + n_out)
+
+
+def fused_block(workload, iters):
+    """Per layer: the plain call, the fused form (prologue + residual, and each
+    alone), and the unfused pipeline a PyTorch user would run (the prologue as
+    torch ops into a new tensor, the plain call, then y += residual), with the
+    HBM-bound floor of the two separate passes (read x, write u; read y and
+    the residual, write y) and the extra device memory each path allocates."""
+    import torch
+    from paper_2609_31938_amd import c3c, inputs
+    wl = inputs.WORKLOADS[workload]
+    dtype = wl["dtype"]
+    dev = torch.device("cuda", 0)
+    ctx = c3c.Context()
+    out = []
+
+    def timed(fn, n):
+        fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(n):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / n
+
+    for lid, (lname, sp) in enumerate(wl["layers"]):
+        w, b = inputs.layer_tensors(sp, dtype, wl["id"], lid, dev)
+        route, _ = c3c.route_query(None, sp, dtype)
+        wpack = c3c.weight_repack(ctx, sp, w) if route == "fast" else None
+        To, Ho, Wo, L = c3c.output_dims(sp, dtype)
+        x = inputs.chunk_input(sp, dtype, wl["id"], lid, 0, dev)
+        cin = torch.zeros((sp["N"], sp["Ci"], sp["Tc"], sp["H"], sp["W"]), dtype=w.dtype,
+                          device=dev) if sp["Tc"] else None
+        cout = torch.empty((sp["N"], sp["Ci"], L, sp["H"], sp["W"]), dtype=w.dtype,
+                           device=dev) if L else None
+        y = torch.empty((sp["N"], sp["Co"], To, Ho, Wo), dtype=w.dtype, device=dev)
+        scale, shift = inputs.affine_inputs(sp, wl["id"], lid, 0, dev)
+        r = inputs.residual_input(tuple(y.shape), dtype, wl["id"], lid, 0, dev)
+        s5, t5 = scale[:, :, None, None, None], shift[:, :, None, None, None]
+
+        def plain():
+            c3c.conv3d_causal_cached(ctx, sp, x, cin, w, wpack, b, y, cout)
+
+        def fused(pro=True, res=True):
+            c3c.conv3d_causal_cached_fused(ctx, sp, x, cin, w, wpack, b,
+                                           scale if pro else None, shift if pro else None,
+                                           r if res else None, y, cout)
+
+        def unfused():
+            u = torch.nn.functional.silu(x.float() * s5 + t5).to(w.dtype)
+            c3c.conv3d_causal_cached(ctx, sp, u, cin, w, wpack, b, y, cout)
+            y.add_(r)
+
+        torch.cuda.synchronize()
+        m0 = torch.cuda.memory_allocated()
+        torch.cuda.reset_peak_memory_stats()
+        unfused()
+        torch.cuda.synchronize()
+        extra_unfused = torch.cuda.max_memory_allocated() - m0
+        torch.cuda.reset_peak_memory_stats()
+        fused()
+        torch.cuda.synchronize()
+        extra_fused = torch.cuda.max_memory_allocated() - m0
+        n = max(2, iters)
+        t_plain = timed(plain, n)
+        t_fused = timed(fused, n)
+        t_pro = timed(lambda: fused(True, False), n)
+        t_res = timed(lambda: fused(False, True), n)
+        t_unf = timed(unfused, n)
+        xb, yb = x.numel() * 2, y.numel() * 2
+        floor_ms = (2 * xb + 3 * yb) / (PEAK_HBM_GBS * 1e9) * 1e3
+        out.append(dict(layer=lname, route=route, plain_ms=round(t_plain, 4),
+                        fused_ms=round(t_fused, 4), prologue_only_ms=round(t_pro, 4),
+                        residual_only_ms=round(t_res, 4), unfused_torch_ms=round(t_unf, 4),
+                        unfused_floor_ms=round(t_plain + floor_ms, 4),
+                        extra_bytes_unfused=int(extra_unfused), extra_bytes_fused=int(extra_fused)))
+        print(json.dumps(out[-1]), flush=True)
+        del x, y, r, cin, cout, w, b, wpack
+        torch.cuda.empty_cache()
+    print(json.dumps({"fused_block": workload, "layers": out}), flush=True)
 
 
 def copy_calibration():

@@ -81,7 +81,7 @@ struct Args {
   // to part[sp][n][co][o][h][w]; splitk_reduce then adds them and the bias
   int splits;
   float* part;
-  // the fused form (FUSED instances; NULL when absent): per-(n, ci) scale and
+  // the fused form (FU instances; NULL when absent): per-(n, ci) scale and
   // shift of the prologue, the residual added in the epilogue
   const float* scale;
   const float* shift;
@@ -109,15 +109,18 @@ __device__ inline void transpose8x8(const u32x4 (&v)[8], u32x4 (&o)[8]) {
 // SPLIT: the split-K instance (a stage range per workgroup, fp32 partial
 // sums out); a separate instance so that the unsplit kernel's register
 // allocation is not shaped by the split epilogue.
-// FUSED: the fused form.  Each stage's scale / shift values load with its
-// activations; once the staged registers are complete (the top of step 7)
-// a stage whose frame comes from the new chunk gets the prologue, in place,
-// before both the LDS store and the cache store see the values; positions
-// outside the image keep their zero.  The residual joins the epilogue.
+// FU: the fused form.  0: none.  1: the residual only.  2: the prologue
+// (and the residual when one is given).  With the prologue, each stage's
+// scale / shift values load with its activations, and a stage whose frame
+// comes from the new chunk gets the prologue on its staged registers, part
+// by part as they arrive, before both the LDS store and the cache store see
+// the values; positions outside the image keep their zero.  The residual
+// joins the epilogue.
 template <int WCO, int WR, int WCF, int WAVES_CO, int WAVES_PX, int NBUF, bool ALIGNED, bool SPLIT,
-          bool FUSED = false>
+          int FU = 0>
 __global__ __launch_bounds__(64 * WAVES_CO * WAVES_PX, 1) void conv3d_bf16(Args a) {
   constexpr int NT = 64 * WAVES_CO * WAVES_PX;
+  constexpr bool PRO = FU == 2, RES = FU >= 1;
   constexpr int BH = WR * WAVES_PX, BW = 16 * WCF;
   constexpr int TH = BH + 2, TW = BW + 2;
   constexpr int NCH = BW / 8;                   // 8-pixel segments per tile row
@@ -249,23 +252,23 @@ __global__ __launch_bounds__(64 * WAVES_CO * WAVES_PX, 1) void conv3d_bf16(Args 
 
   u32x4 sv[TPT][8];
   uint16_t hv[HPT];
-  // FUSED: this thread's 8 task channels (8g + j, the same g for every task
+  // PRO: this thread's 8 task channels (8g + j, the same g for every task
   // of a thread) and its halo channels, for the stage being loaded; batch
   // element n's scale / shift with channels past Ci out of range (0)
   float psc[8], psh[8], hsc[HPT], hsh[HPT];
   bool ppro = false;
   const __amdgpu_buffer_rsrc_t ssr = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<float*>(FUSED && a.scale ? a.scale + static_cast<int64_t>(n) * a.Ci : a.scale), 0,
-      FUSED && a.scale ? a.Ci * 4 : 0, 0x00020000);
+      const_cast<float*>(PRO && a.scale ? a.scale + static_cast<int64_t>(n) * a.Ci : a.scale), 0,
+      PRO && a.scale ? a.Ci * 4 : 0, 0x00020000);
   const __amdgpu_buffer_rsrc_t shr = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<float*>(FUSED && a.shift ? a.shift + static_cast<int64_t>(n) * a.Ci : a.shift), 0,
-      FUSED && a.shift ? a.Ci * 4 : 0, 0x00020000);
+      const_cast<float*>(PRO && a.shift ? a.shift + static_cast<int64_t>(n) * a.Ci : a.shift), 0,
+      PRO && a.shift ? a.Ci * 4 : 0, 0x00020000);
 
   // part p of a stage's loads: channel rows 2p, 2p + 1 of every task for
   // p = 0..3, the halo columns for p = 4 (spread over five steps so that no
   // burst of loads sits in front of the weight loads that follow it)
   auto load_stage = [&](const Stage& st, int part) {
-    if (FUSED && part == 0) {
+    if (PRO && part == 0) {
       ppro = a.scale != nullptr && st.f >= a.Tc;
       const uint32_t c8 = static_cast<uint32_t>(st.c0) + t_g8[0];
 #pragma unroll
@@ -310,28 +313,37 @@ __global__ __launch_bounds__(64 * WAVES_CO * WAVES_PX, 1) void conv3d_bf16(Args 
           st.rs, h_ok[hh] ? h_ch[hh] * st.cs + h_pix[hh] : OOB, 0, 0);
   };
 
-  // FUSED: the prologue on the staged registers of a new-chunk stage (all
-  // selects, no branch).  A task is in the image when t_ok; without ALIGNED
-  // its pixels past W are padding too.
-  auto pro_stage = [&]() {
-    if constexpr (FUSED) {
+  // PRO: the prologue on the staged registers of a new-chunk stage (a
+  // workgroup-uniform skip for cache frames, selects inside).  A task is in
+  // the image when t_ok; without ALIGNED its pixels past W are padding too.
+  // PRO: the prologue on the staged registers of part `part` of a stage
+  // (rows 2 part, 2 part + 1 of every task for part 0..3, the halo for part
+  // 4), applied a few steps after that part's loads were issued so that the
+  // VALU work interleaves with the matrix-core steps (branch-free: ppro is
+  // false for a cache frame, and a task is in the image when t_ok; without
+  // ALIGNED its pixels past W are padding too).
+  auto pro_part = [&](int part) {
+    if constexpr (PRO) {
+      if (part < 4) {
 #pragma unroll
-      for (int tt = 0; tt < TPT; ++tt) {
-        const bool ok = ppro & t_ok[tt];
+        for (int tt = 0; tt < TPT; ++tt) {
+          const bool ok = ppro & t_ok[tt];
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          if (ALIGNED) {
-            sv[tt][j] = fuse_seg8(sv[tt][j], psc[j], psh[j], ok);
-          } else {
+          for (int j = 2 * part; j < 2 * part + 2; ++j) {
+            if (ALIGNED) {
+              sv[tt][j] = fuse_seg8(sv[tt][j], psc[j], psh[j], ok);
+            } else {
 #pragma unroll
-            for (int r = 0; r < 4; ++r)
-              sv[tt][j][r] = fuse_pair(sv[tt][j][r], psc[j], psh[j], ok & (t_w[tt] + 2 * r < a.W),
-                                       ok & (t_w[tt] + 2 * r + 1 < a.W));
+              for (int r = 0; r < 4; ++r)
+                sv[tt][j][r] = fuse_pair(sv[tt][j][r], psc[j], psh[j], ok & (t_w[tt] + 2 * r < a.W),
+                                         ok & (t_w[tt] + 2 * r + 1 < a.W));
+            }
           }
         }
-      }
+      } else {
 #pragma unroll
-      for (int hh = 0; hh < HPT; ++hh) hv[hh] = fuse_one(hv[hh], hsc[hh], hsh[hh], ppro & h_ok[hh]);
+        for (int hh = 0; hh < HPT; ++hh) hv[hh] = fuse_one(hv[hh], hsc[hh], hsh[hh], ppro & h_ok[hh]);
+      }
     }
   };
 
@@ -447,7 +459,7 @@ __global__ __launch_bounds__(64 * WAVES_CO * WAVES_PX, 1) void conv3d_bf16(Args 
     load_w(cst.wbase, 0, wr[0]);
     load_w(cst.wbase, 1, wr[1]);
     for (int part = 0; part < 5; ++part) load_stage(cst, part);
-    pro_stage();
+    for (int part = 0; part < 5; ++part) pro_part(part);
     if (cache_needed(cst, true)) cache_store(cst);
     store_stage(0);
     __syncthreads();
@@ -474,7 +486,11 @@ __global__ __launch_bounds__(64 * WAVES_CO * WAVES_PX, 1) void conv3d_bf16(Args 
     for (int ij = 0; ij < 9; ++ij) {
       // the cache write (rare, workgroup-uniform) is its own block ahead of
       // the scheduled region of step 7
-      if (FUSED && ij == 7) pro_stage();
+      // PRO: the next stage's prologue, part p at step p + 3 (its loads were
+      // issued at step p), the halo at step 6; all before the cache and LDS
+      // stores of step 7
+      if (PRO && ij >= 3 && ij <= 6) pro_part(ij - 3);
+      if (PRO && ij == 6) pro_part(4);
       if (ij == 7 && cache_needed(nst_, s + 1 < cnt)) cache_store(nst_);
       // keep every LDS read inside its own step: re-reading is cheaper in
       // registers than keeping overlapping rows of neighbouring kh live
@@ -553,6 +569,33 @@ __global__ __launch_bounds__(64 * WAVES_CO * WAVES_PX, 1) void conv3d_bf16(Args 
     return;
   }
   uint16_t* ybase = a.y + (static_cast<int64_t>(n) * a.Co) * plane + static_cast<int64_t>(o) * a.hw;
+  // RES: every fragment's residual values, loaded as one batch before any
+  // store (branch-free: a position outside the output reads the residual's
+  // first element and is not used), so the block waits for memory once
+  uint2 rv[RES ? WCO : 1][RES ? NPF : 1];
+  if constexpr (RES) {
+    const bool has_r = a.residual != nullptr;
+#pragma unroll
+    for (int cf = 0; cf < WCO; ++cf) {
+      const int co = (cofrag0 + cf) * 16 + (lane & 15);
+#pragma unroll
+      for (int pf = 0; pf < NPF; ++pf) {
+        const int h = h0 + wpx * WR + pf / WCF, w = w0 + (pf % WCF) * 16 + 4 * (lane >> 4);
+        const bool ok = has_r & (co < a.Co) & (h < a.H) & (w < a.W);
+        const int64_t off = (static_cast<int64_t>(n) * a.Co + (ok ? co : 0)) * plane +
+                            static_cast<int64_t>(o) * a.hw + (ok ? static_cast<int64_t>(h) * a.W + w : 0);
+        const uint16_t* rsrc = has_r ? a.residual + off : a.y;
+        if (ALIGNED) {
+          rv[cf][pf] = *reinterpret_cast<const uint2*>(rsrc);
+        } else {
+          uint16_t e[4];
+#pragma unroll
+          for (int r = 0; r < 4; ++r) e[r] = rsrc[ok & (w + r < a.W) ? r : 0];
+          rv[cf][pf] = make_uint2(e[0] | (static_cast<uint32_t>(e[1]) << 16), e[2] | (static_cast<uint32_t>(e[3]) << 16));
+        }
+      }
+    }
+  }
 #pragma unroll
   for (int cf = 0; cf < WCO; ++cf) {
     const int co = (cofrag0 + cf) * 16 + (lane & 15);
@@ -562,19 +605,12 @@ __global__ __launch_bounds__(64 * WAVES_CO * WAVES_PX, 1) void conv3d_bf16(Args 
       const int h = h0 + wpx * WR + pf / WCF, w = w0 + (pf % WCF) * 16 + 4 * (lane >> 4);
       if (co >= a.Co || h >= a.H || w >= a.W) continue;
       uint16_t* dst = ybase + co * plane + static_cast<int64_t>(h) * a.W + w;
-      // FUSED: the residual at the same position, added before the rounding
+      // RES: the residual at the same position, added before the rounding
       f32x4 rr = {0.f, 0.f, 0.f, 0.f};
-      if (FUSED && a.residual) {
-        const uint16_t* rsrc = a.residual + (dst - a.y);
-        if (ALIGNED && w + 4 <= a.W) {
-          const uint2 r2 = *reinterpret_cast<const uint2*>(rsrc);
-          rr = f32x4{fuse_widen(r2.x & 0xffffu), fuse_widen(r2.x >> 16), fuse_widen(r2.y & 0xffffu),
-                     fuse_widen(r2.y >> 16)};
-        } else {
-#pragma unroll
-          for (int r = 0; r < 4; ++r)
-            if (w + r < a.W) rr[r] = fuse_widen(rsrc[r]);
-        }
+      if (RES && a.residual) {
+        const uint2 r2 = rv[RES ? cf : 0][RES ? pf : 0];
+        rr = f32x4{fuse_widen(r2.x & 0xffffu), fuse_widen(r2.x >> 16), fuse_widen(r2.y & 0xffffu),
+                   fuse_widen(r2.y >> 16)};
       }
       // one round-to-nearest-even conversion per value (hardware, two at a time)
       const uint32_t v01 = __builtin_bit_cast(
@@ -654,7 +690,7 @@ void set_tiles(const Geo& g, int64_t bco, int64_t bh, int64_t bw, Plan* p) {
 }
 
 template <int WCO, int WR, int WCF, int WAVES_CO, int WAVES_PX, int NBUF>
-hipError_t run(const Geo& g, Args a, const Plan& p, bool aligned, bool fused, hipStream_t s) {
+hipError_t run(const Geo& g, Args a, const Plan& p, bool aligned, int fused, hipStream_t s) {
   a.tiles_co = static_cast<int>(p.tiles_co);
   a.tiles_w = static_cast<int>(p.tiles_w);
   a.tiles_h = static_cast<int>(p.tiles_h);
@@ -667,9 +703,9 @@ hipError_t run(const Geo& g, Args a, const Plan& p, bool aligned, bool fused, hi
 #define C3C_BF16(AL, SP, FU)                                                                        \
   if (aligned == AL && split == SP && fused == FU)                                                   \
     hipLaunchKernelGGL((conv3d_bf16<WCO, WR, WCF, WAVES_CO, WAVES_PX, NBUF, AL, SP, FU>), grid, block, 0, s, a);
-  C3C_BF16(true, false, false) C3C_BF16(false, false, false) C3C_BF16(true, true, false)
-  C3C_BF16(false, true, false) C3C_BF16(true, false, true) C3C_BF16(false, false, true)
-  C3C_BF16(true, true, true) C3C_BF16(false, true, true)
+  C3C_BF16(true, false, 0) C3C_BF16(false, false, 0) C3C_BF16(true, true, 0) C3C_BF16(false, true, 0)
+  C3C_BF16(true, false, 1) C3C_BF16(false, false, 1) C3C_BF16(true, true, 1) C3C_BF16(false, true, 1)
+  C3C_BF16(true, false, 2) C3C_BF16(false, false, 2) C3C_BF16(true, true, 2) C3C_BF16(false, true, 2)
 #undef C3C_BF16
   if (!split) return hipGetLastError();
   const int64_t plane = static_cast<int64_t>(a.To) * a.hw;
@@ -677,7 +713,7 @@ hipError_t run(const Geo& g, Args a, const Plan& p, bool aligned, bool fused, hi
   const bool vec4 = plane % 4 == 0 && (reinterpret_cast<uintptr_t>(a.y) & 7u) == 0;
   int64_t rb = (total / (vec4 ? 4 : 1) + 255) / 256;
   if (rb > 65536) rb = 65536;
-  const uint16_t* res = fused ? a.residual : nullptr;
+  const uint16_t* res = fused != 0 ? a.residual : nullptr;
   if (vec4 && (res == nullptr || (reinterpret_cast<uintptr_t>(res) & 7u) == 0))
     hipLaunchKernelGGL(splitk_reduce<true>, dim3(static_cast<unsigned>(rb)), dim3(256), 0, s, a.part,
                        a.bias, res, a.y, total, plane, a.Co, a.splits, a.has_bias);
@@ -836,7 +872,8 @@ hipError_t launch_fast_bf16(const Geo& g, const void* x, const void* cache, cons
   a.scale = fu.scale;
   a.shift = fu.shift;
   a.residual = fu.residual;
-  const bool fused = fu.any();
+  // instance: 0 plain, 1 residual only, 2 prologue (+ residual)
+  const int fused = fu.pro() ? 2 : fu.residual ? 1 : 0;
   const bool aligned = (g.d.W % 8 == 0) && (x == nullptr || aligned16(x)) &&
                        (cache == nullptr || aligned16(cache)) &&
                        (cache_out == nullptr || aligned16(cache_out)) &&

@@ -78,7 +78,7 @@ struct PwArgs {
   int chunks, px_tiles, co_tiles, cofrags;
   uint32_t w_bytes;
   int has_bias;
-  // the fused form (FUSED instances; NULL when absent)
+  // the fused form (FU instances; NULL when absent)
   const float* scale;
   const float* shift;
   const uint16_t* residual;
@@ -112,13 +112,15 @@ __device__ inline f32x4 mma(i16x8 a, u32x4 b, f32x4 c) {
 // w[co][ci] (fallback, Kt = 1).  ALIGNED: every channel plane starts on a
 // 16-byte boundary (H * W a multiple of 8, aligned pointers); else the
 // activations are read 2 bytes at a time and the outputs stored one by one.
-// FUSED (bf16): the fused form's prologue on stages whose frame comes from
-// the new chunk (applied to the staged registers before they go to LDS; a
-// 1x1 kernel has no spatial padding, and pixels past the plane only feed
-// outputs that are never stored) and its residual in the epilogue.
-template <bool F16, int PD, bool PACKED, bool ALIGNED, int PW_NPF, bool FUSED = false>
+// FU (bf16): the fused form.  1: the residual, in the epilogue.  2: also
+// the prologue on stages whose frame comes from the new chunk (applied to
+// the staged registers before they go to LDS; a 1x1 kernel has no spatial
+// padding, and pixels past the plane only feed outputs that are never
+// stored).
+template <bool F16, int PD, bool PACKED, bool ALIGNED, int PW_NPF, int FU = 0>
 __global__ __launch_bounds__(PW_NT, 1) void pointwise_conv(PwArgs a) {
   constexpr int PW_PX = pw_px(PW_NPF), PW_PITCH = pw_pitch(PW_NPF);
+  constexpr bool PRO = FU == 2, RES = FU >= 1;
   constexpr int PW_WOFF = pw_woff(PW_NPF), PW_BUF = pw_buf(PW_NPF);
   constexpr int SEG = PW_PX / 128;  // 16-byte row segments per thread per stage
   __shared__ __align__(16) unsigned char lds[2 * PW_BUF];
@@ -207,19 +209,19 @@ __global__ __launch_bounds__(PW_NT, 1) void pointwise_conv(PwArgs a) {
   struct Chunk {
     u32x4 x[SEG];
     u32x4 w[PW_WPT];
-    float psc, psh;  // FUSED: this thread's channel's scale and shift
-    bool pro;        // FUSED: the stage's frame comes from the new chunk
+    float psc, psh;  // PRO: this thread's channel's scale and shift
+    bool pro;        // PRO: the stage's frame comes from the new chunk
   };
-  // FUSED: scale / shift of batch element n, channels past Ci read as 0
+  // PRO: scale / shift of batch element n, channels past Ci read as 0
   const __amdgpu_buffer_rsrc_t ssr = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<float*>(FUSED && a.scale ? a.scale + static_cast<int64_t>(n) * a.Ci : a.scale), 0,
-      FUSED && a.scale ? a.Ci * 4 : 0, 0x00020000);
+      const_cast<float*>(PRO && a.scale ? a.scale + static_cast<int64_t>(n) * a.Ci : a.scale), 0,
+      PRO && a.scale ? a.Ci * 4 : 0, 0x00020000);
   const __amdgpu_buffer_rsrc_t shr = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<float*>(FUSED && a.shift ? a.shift + static_cast<int64_t>(n) * a.Ci : a.shift), 0,
-      FUSED && a.shift ? a.Ci * 4 : 0, 0x00020000);
+      const_cast<float*>(PRO && a.shift ? a.shift + static_cast<int64_t>(n) * a.Ci : a.shift), 0,
+      PRO && a.shift ? a.Ci * 4 : 0, 0x00020000);
   auto load_chunk = [&](int st_, Chunk& ck) {
     const StageSrc sr = stage_src(st_);
-    if constexpr (FUSED) {
+    if constexpr (PRO) {
       // the prologue applies to the new chunk's frames only
       const int k = k_lo + (ntap > 0 ? st_ / a.chunks : 0);
       const bool from_x = st_ < nst && t * a.st + k * a.dt - a.p_l >= a.Tc;
@@ -270,8 +272,9 @@ __global__ __launch_bounds__(PW_NT, 1) void pointwise_conv(PwArgs a) {
     unsigned char* base = lds + buf * PW_BUF;
 #pragma unroll
     for (int h = 0; h < SEG; ++h) {
-      // FUSED: a cache frame (or no prologue) is kept as loaded
-      const u32x4 v = FUSED ? fuse_seg8(ck.x[h], ck.psc, ck.psh, ck.pro) : ck.x[h];
+      // PRO: the prologue on a new-chunk stage (a workgroup-uniform test)
+      u32x4 v = ck.x[h];
+      if (PRO && ck.pro) v = fuse_seg8(v, ck.psc, ck.psh, true);
       *reinterpret_cast<u32x4*>(base + slds + 256 * h) = v;
     }
 #pragma unroll
@@ -349,24 +352,36 @@ __global__ __launch_bounds__(PW_NT, 1) void pointwise_conv(PwArgs a) {
     if (co >= a.Co) continue;
     const float bb = a.has_bias ? from_b16(a.bias[co], F16) : 0.f;
     uint16_t* yrow = ybase + static_cast<int64_t>(co) * a.To * a.hw;
+    // RES: this fragment row's residual values, loaded as one batch before
+    // its stores (branch-free: a pixel past the plane reads the row's first
+    // element and is not used)
+    uint2 rv[RES ? PW_NPF : 1];
+    if constexpr (RES) {
+      const uint16_t* rrow = a.residual ? a.residual + (yrow - a.y) : yrow;
+#pragma unroll
+      for (int pf = 0; pf < PW_NPF; ++pf) {
+        const int p = px0 + wpx * 16 * PW_NPF + pf * 16 + 4 * g;
+        if (ALIGNED) {
+          rv[pf] = *reinterpret_cast<const uint2*>(rrow + (p + 4 <= a.hw ? p : 0));
+        } else {
+          uint16_t e[4];
+#pragma unroll
+          for (int r = 0; r < 4; ++r) e[r] = rrow[p + r < a.hw ? p + r : 0];
+          rv[pf] = make_uint2(e[0] | (static_cast<uint32_t>(e[1]) << 16), e[2] | (static_cast<uint32_t>(e[3]) << 16));
+        }
+      }
+    }
 #pragma unroll
     for (int pf = 0; pf < PW_NPF; ++pf) {
       const int p = px0 + wpx * 16 * PW_NPF + pf * 16 + 4 * g;
       float rr[4] = {0.f, 0.f, 0.f, 0.f};
-      if (FUSED && a.residual) {
+      if (RES && a.residual) {
         // fused residual, added before the one rounding
-        const uint16_t* rrow = a.residual + (yrow - a.y);
-        if (ALIGNED && p + 4 <= a.hw) {
-          const uint2 r2 = *reinterpret_cast<const uint2*>(rrow + p);
-          rr[0] = fuse_widen(r2.x & 0xffffu);
-          rr[1] = fuse_widen(r2.x >> 16);
-          rr[2] = fuse_widen(r2.y & 0xffffu);
-          rr[3] = fuse_widen(r2.y >> 16);
-        } else {
-#pragma unroll
-          for (int r = 0; r < 4; ++r)
-            if (p + r < a.hw) rr[r] = fuse_widen(rrow[p + r]);
-        }
+        const uint2 r2 = rv[RES ? pf : 0];
+        rr[0] = fuse_widen(r2.x & 0xffffu);
+        rr[1] = fuse_widen(r2.x >> 16);
+        rr[2] = fuse_widen(r2.y & 0xffffu);
+        rr[3] = fuse_widen(r2.y >> 16);
       }
       uint16_t v[4];
 #pragma unroll
@@ -412,7 +427,7 @@ namespace {
 // count of any output frame least (4, 3 or 2), the template instance by
 // element type, weight layout and alignment
 template <bool PACKED>
-hipError_t launch_pw(const Geo& g, PwArgs a, bool f16, bool al, hipStream_t s, bool fused) {
+hipError_t launch_pw(const Geo& g, PwArgs a, bool f16, bool al, hipStream_t s, int fused) {
   const c3c_conv_desc& d = g.d;
   a.co_tiles = static_cast<int>((d.Co + PW_CO - 1) / PW_CO);
   // Fast route, aligned: 512-pixel workgroups (twice the products per
@@ -454,16 +469,20 @@ hipError_t launch_pw(const Geo& g, PwArgs a, bool f16, bool al, hipStream_t s, b
     return hipGetLastError();                                                                  \
   }
   if constexpr (PACKED) {  // fast route: bf16, any alignment
-    C3C_PW(false, 2, true, 4, false) C3C_PW(false, 3, true, 4, false) C3C_PW(false, 4, true, 4, false)
-    C3C_PW(false, 2, false, 4, false) C3C_PW(false, 3, false, 4, false) C3C_PW(false, 4, false, 4, false)
-    C3C_PW(false, 2, true, 8, false)
-    C3C_PW(false, 2, true, 4, true) C3C_PW(false, 3, true, 4, true) C3C_PW(false, 4, true, 4, true)
-    C3C_PW(false, 2, false, 4, true) C3C_PW(false, 3, false, 4, true) C3C_PW(false, 4, false, 4, true)
-    C3C_PW(false, 2, true, 8, true)
+    C3C_PW(false, 2, true, 4, 0) C3C_PW(false, 3, true, 4, 0) C3C_PW(false, 4, true, 4, 0)
+    C3C_PW(false, 2, false, 4, 0) C3C_PW(false, 3, false, 4, 0) C3C_PW(false, 4, false, 4, 0)
+    C3C_PW(false, 2, true, 8, 0)
+    C3C_PW(false, 2, true, 4, 1) C3C_PW(false, 3, true, 4, 1) C3C_PW(false, 4, true, 4, 1)
+    C3C_PW(false, 2, false, 4, 1) C3C_PW(false, 3, false, 4, 1) C3C_PW(false, 4, false, 4, 1)
+    C3C_PW(false, 2, true, 8, 1)
+    C3C_PW(false, 2, true, 4, 2) C3C_PW(false, 3, true, 4, 2) C3C_PW(false, 4, true, 4, 2)
+    C3C_PW(false, 2, false, 4, 2) C3C_PW(false, 3, false, 4, 2) C3C_PW(false, 4, false, 4, 2)
+    C3C_PW(false, 2, true, 8, 2)
   } else {  // fallback: bf16 / fp16, aligned (pointwise_eligible)
-    C3C_PW(false, 2, true, 4, false) C3C_PW(false, 3, true, 4, false) C3C_PW(false, 4, true, 4, false)
-    C3C_PW(true, 2, true, 4, false) C3C_PW(true, 3, true, 4, false) C3C_PW(true, 4, true, 4, false)
-    C3C_PW(false, 2, true, 4, true) C3C_PW(false, 3, true, 4, true) C3C_PW(false, 4, true, 4, true)
+    C3C_PW(false, 2, true, 4, 0) C3C_PW(false, 3, true, 4, 0) C3C_PW(false, 4, true, 4, 0)
+    C3C_PW(true, 2, true, 4, 0) C3C_PW(true, 3, true, 4, 0) C3C_PW(true, 4, true, 4, 0)
+    C3C_PW(false, 2, true, 4, 1) C3C_PW(false, 3, true, 4, 1) C3C_PW(false, 4, true, 4, 1)
+    C3C_PW(false, 2, true, 4, 2) C3C_PW(false, 3, true, 4, 2) C3C_PW(false, 4, true, 4, 2)
   }
 #undef C3C_PW
   return hipErrorInvalidValue;
@@ -507,7 +526,7 @@ hipError_t launch_pointwise(const Geo& g, const void* x, const void* cache, cons
   a.shift = fu.shift;
   a.residual = fu.residual;
   // launch_fallback checked the residual's 8-byte alignment
-  return launch_pw<false>(g, a, g.d.dtype == C3C_DTYPE_F16, true, s, fu.any());
+  return launch_pw<false>(g, a, g.d.dtype == C3C_DTYPE_F16, true, s, fu.pro() ? 2 : fu.residual ? 1 : 0);
 }
 
 hipError_t launch_fast_tap1x1(const Geo& g, const void* x, const void* cache, const void* wpack,
@@ -528,7 +547,7 @@ hipError_t launch_fast_tap1x1(const Geo& g, const void* x, const void* cache, co
   a.residual = fu.residual;
   const bool al = (d.H * d.W) % 8 == 0 && aligned(x, 16) && (cache == nullptr || aligned(cache, 16)) &&
                   aligned(y, 8) && (fu.residual == nullptr || aligned(fu.residual, 8));
-  return launch_pw<true>(g, a, false, al, s, fu.any());
+  return launch_pw<true>(g, a, false, al, s, fu.pro() ? 2 : fu.residual ? 1 : 0);
 }
 
 }  // namespace c3c
