@@ -183,3 +183,47 @@ def test_fused_stream_matches_oracle_stream(kh):
         # carry the library's own cache forward; the oracle takes the same bits
         cache_d, cache_h = co, _bits(co)
     assert ctx.counters()["fast"] == 4
+
+
+# ---------------------------------------------------------------- memory
+def test_calls_allocate_no_device_memory():
+    """The library allocates nothing in a compute call (plain, fused, split-K
+    with the caller's workspace, fallback): after one warm-up call of each
+    kind (which loads its kernels' code), repeated calls leave the device's
+    free memory unchanged."""
+    ctx = c3c.Context()
+    cases = []
+    for over, mode, ws in [(dict(N=1, Ci=64, Co=160, T=2, Tc=2, H=24, W=80), 0, False),
+                           (dict(N=1, Ci=128, Co=128, T=1, Tc=2, H=16, W=32), 0, True),
+                           (dict(N=1, Ci=12, Co=20, T=3, Tc=2, H=10, W=13, Kh=5, Kw=3), 0, False)]:
+        sp = spec(**over)
+        w, b = layer(sp, "bf16", WID, 3)
+        x = chunk(sp, "bf16", WID, 3, 0)
+        cache = chunk(dict(sp, T=sp["Tc"]), "bf16", WID, 3, 1)
+        wpack = c3c.weight_repack(ctx, sp, w) if c3c.route_query(None, sp, "bf16")[0] == "fast" else None
+        To, Ho, Wo, L = c3c.output_dims(sp, "bf16")
+        y = torch.empty((sp["N"], sp["Co"], To, Ho, Wo), dtype=torch.bfloat16, device="cuda")
+        co = torch.empty((sp["N"], sp["Ci"], L, sp["H"], sp["W"]), dtype=torch.bfloat16, device="cuda")
+        scale, shift = inputs.affine_inputs(sp, WID, 3, 0, "cuda")
+        r = inputs.residual_input(tuple(y.shape), "bf16", WID, 3, 0, "cuda")
+        wsb = torch.empty(max(c3c.workspace_bytes(sp, "bf16"), 4) // 4, dtype=torch.float32,
+                          device="cuda") if ws else None
+        cases.append((sp, x, cache, w, wpack, b, y, co, scale, shift, r, wsb))
+
+    def all_calls():
+        for sp, x, cache, w, wpack, b, y, co, scale, shift, r, wsb in cases:
+            ctx.set_workspace(wsb)
+            c3c.conv3d_causal_cached(ctx, sp, x, cache, w, wpack, b, y, co)
+            c3c.conv3d_causal_cached_fused(ctx, sp, x, cache, w, wpack, b, scale, shift, r, y, co)
+            c3c.conv3d_causal_cached_fused(ctx, sp, x, cache, w, wpack, b, None, None, r, y, co)
+        ctx.set_workspace(None)
+
+    all_calls()
+    torch.cuda.synchronize()
+    free0, _ = torch.cuda.mem_get_info()
+    for _ in range(5):
+        all_calls()
+    torch.cuda.synchronize()
+    free1, _ = torch.cuda.mem_get_info()
+    say(f"free before {free0} after {free1}")
+    assert free1 == free0
