@@ -267,3 +267,28 @@ def test_tap1x1_kernel_matches_oracle(over):
     ctx, _, m = _case(sp, "bf16")
     assert ctx.counters()["fast"] == 1
     say(f"  rel={m['rel']:.3e} cos={m['cos']:.8f}")
+
+
+# ---------------------------------------------------------------- few output channels
+# The head kernel (Co <= 5, W a multiple of 8): the 9 spatial taps x Co as
+# matrix-core columns, then a 3x3 gather-sum.  Every Co it serves, ragged
+# rows (H not a multiple of the 6-row tile) and columns (W not a multiple of
+# 64), a channel-chunk tail, dilation, p_l < 0, no cache, N = 2, Kt = 2.
+HEAD_CASES = [
+    dict(N=1, Ci=96, Co=3, T=4, Tc=2, H=37, W=136),
+    dict(N=1, Ci=40, Co=1, T=2, Tc=2, H=20, W=72),
+    dict(N=2, Ci=64, Co=2, T=3, Tc=1, H=13, W=64),
+    dict(N=1, Ci=48, Co=4, T=2, Tc=3, H=19, W=80),
+    dict(N=1, Ci=32, Co=5, T=3, Tc=4, H=11, W=40, d_t=2),
+    dict(N=1, Ci=72, Co=3, T=3, Tc=0, H=25, W=200),
+    dict(N=1, Ci=24, Co=3, T=2, Tc=1, H=8, W=8, Kt=2),
+]
+
+
+@pytest.mark.parametrize("over", HEAD_CASES)
+def test_head_kernel_matches_oracle(over):
+    sp = spec(**over)
+    assert sp["Co"] <= 5 and sp["W"] % 8 == 0  # takes the head kernel
+    ctx, _, m = _case(sp, "bf16")
+    assert ctx.counters()["fast"] == 1
+    say(f"  rel={m['rel']:.3e} cos={m['cos']:.8f}")
