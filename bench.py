@@ -192,6 +192,11 @@ def main():
         roofline = {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS,
                     "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4), "traffic": None,
                     "kernel": f"fallback route, layer {dom['layer']}"}
+    # the matrix cores' sustained rate on this machine (outside the timed region):
+    # back-to-back bf16 products, one workgroup per compute unit
+    probe = mfma_probe_rate()
+    if roofline["bound"] == "mfma" and dtype == "bf16":
+        roofline["frac_of_probe"] = round(achieved / probe["tflops"], 4)
     shapes = sorted({(L_["sp"]["T"], L_["sp"]["Tc"]) for L_ in layers})
     frames = ", ".join(f"T={t} new + {tc} cached frames" for t, tc in shapes)
 
@@ -215,6 +220,7 @@ def main():
         "chunk_latency_ms": round(total_ms / args.steps, 4),
         "layers": per_layer,
         "roofline": roofline,
+        "mfma_probe": probe,
         "counters": counters,
         "wall_s": round(t_wall, 4),
     }
@@ -238,6 +244,31 @@ def algorithmic_bytes(sp, dtype):
     n_w = sp["Co"] * (sp["Ci"] // sp["groups"]) * sp["Kt"] * sp["Kh"] * sp["Kw"]
     n_out = sp["N"] * sp["Co"] * To * Ho * Wo + sp["N"] * sp["Ci"] * L * hw
     return es * (n_in + n_w + sp["Co"] * sp["has_bias"] + n_out)
+
+
+def mfma_probe_rate(iters=50000):
+    """TFLOP/s of the library's matrix-core probe (c3c_mfma_probe): four
+    workgroups of 4 waves per compute unit, 8 independent bf16 16x16x32
+    products back to back per wave, no memory traffic.  The published peak
+    times the clock the device holds under matrix-core load; the implied
+    clock is reported with it."""
+    import torch
+    from paper_2609_31938_amd import c3c
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    blocks = 4 * cus
+    c3c.mfma_probe(blocks, iters // 10)  # warm-up
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    out, fl = c3c.mfma_probe(blocks, iters)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1)
+    tf = fl / (ms * 1e-3) / 1e12
+    return {"tflops": round(tf, 1), "frac_of_published_peak": round(tf / PEAK_BF16_TFLOPS, 4),
+            "implied_clock_ghz": round(2.4 * tf / PEAK_BF16_TFLOPS, 3), "ms": round(ms, 3),
+            "launch": f"{blocks} workgroups x 4 waves, 8 chains, {iters} iterations",
+            "finite": bool(torch.isfinite(out).all().item())}
 
 
 def fused_block(workload, iters):

@@ -293,6 +293,18 @@ int c3c_counters_reset(c3c_ctx* ctx); /* also clears the shape histogram */
 int c3c_fallback_shapes(const c3c_ctx* ctx, c3c_sig_count* out, int cap,
                         int* n);
 
+/* ---------------------------------------------------------------- measurement */
+/* Not part of the paper's method: a reference rate for measuring the
+ * kernels.  Launches `blocks` workgroups of 4 waves; each wave runs `iters`
+ * iterations of 8 independent back-to-back bf16 matrix-core products
+ * (16x16x32) and reads no memory; with several workgroups per compute unit
+ * the launch runs at the matrix cores' peak at the clock the device sustains
+ * under that load.  Writes one float per thread to `out` (device memory,
+ * blocks * 256 floats, caller-owned); *flops receives the launch's FLOP
+ * count; the caller times the launch on `stream`.
+ * EINVAL: blocks or iters outside [1, 2^31), out or flops NULL. */
+int c3c_mfma_probe(int64_t blocks, int64_t iters, float* out, double* flops, void* stream);
+
 /* ---------------------------------------------------------------- messages */
 const char* c3c_strerror(int status);
 /* Message of the last failed call on ctx ("" if none); valid until the next

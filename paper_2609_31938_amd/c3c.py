@@ -75,6 +75,7 @@ lib.c3c_conv3d_causal_cached.argtypes = [_vp, _P(Desc), _vp, _vp, _vp, _vp, _vp,
 lib.c3c_conv3d_causal_cached_fused.argtypes = [_vp, _P(Desc), _vp, _vp, _vp, _vp, _vp, _vp, _vp,
                                                _vp, _vp, _vp, _vp]
 lib.c3c_counters_get.argtypes = [_vp, _P(Counters)]
+lib.c3c_mfma_probe.argtypes = [C.c_int64, C.c_int64, _vp, _P(C.c_double), _vp]
 lib.c3c_counters_reset.argtypes = [_vp]
 lib.c3c_fallback_shapes.argtypes = [_vp, _P(SigCount), C.c_int, _P(C.c_int)]
 lib.c3c_strerror.argtypes = [C.c_int]
@@ -343,3 +344,14 @@ def conv3d_causal_cached_fused(ctx, spec: dict, x, cache, w, wpack, bias, scale=
         _ptr(y, "y", dtype), _ptr(cache_out, "cache_out", dtype), _stream(stream))
     _raise(st, ctx, "c3c_conv3d_causal_cached_fused")
     return y, cache_out
+
+
+def mfma_probe(blocks: int, iters: int, stream=None):
+    """One launch of the matrix-core rate probe (c3c_mfma_probe), enqueued on
+    the stream; returns (out tensor, FLOP count).  The caller times it."""
+    import torch
+    out = torch.empty(blocks * 256, dtype=torch.float32, device="cuda")
+    fl = C.c_double()
+    st = lib.c3c_mfma_probe(blocks, iters, out.data_ptr(), C.byref(fl), _stream(stream))
+    _raise(st, None, "c3c_mfma_probe")
+    return out, fl.value

@@ -458,6 +458,15 @@ int c3c_fallback_shapes(const c3c_ctx* ctx, c3c_sig_count* out, int cap, int* n)
   return C3C_OK;
 }
 
+int c3c_mfma_probe(int64_t blocks, int64_t iters, float* out, double* flops, void* stream) {
+  if (blocks < 1 || blocks > 0x7fffffff || iters < 1 || iters > 0x7fffffff || !out || !flops)
+    return C3C_E_INVAL;
+  *flops = mfma_probe_flops(blocks, iters);
+  return launch_mfma_probe(blocks, iters, out, static_cast<hipStream_t>(stream)) == hipSuccess
+             ? C3C_OK
+             : C3C_E_DEVICE;
+}
+
 const char* c3c_strerror(int status) {
   switch (status) {
     case C3C_OK: return "ok";

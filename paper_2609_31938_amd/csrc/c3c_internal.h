@@ -53,6 +53,9 @@ struct Fuse {
 };
 
 hipError_t launch_repack(const Geo& g, const void* w, void* wpack, hipStream_t s);
+// measurement support (mfma_probe.hip): back-to-back bf16 matrix-core products
+hipError_t launch_mfma_probe(int64_t blocks, int64_t iters, float* out, hipStream_t s);
+double mfma_probe_flops(int64_t blocks, int64_t iters);
 hipError_t launch_unpack(const Geo& g, const void* wpack, void* w, hipStream_t s);
 // ws / ws_bytes: the caller's split-K workspace (may be NULL / 0).
 hipError_t launch_fast(const Geo& g, const void* x, const void* cache, const void* wpack,

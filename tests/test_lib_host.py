@@ -33,7 +33,8 @@ def test_every_declared_symbol_is_exported():
         "c3c_weight_pack_bytes", "c3c_weight_repack", "c3c_weight_unpack",
         "c3c_conv3d_causal_cached", "c3c_counters_get", "c3c_counters_reset",
         "c3c_fallback_shapes", "c3c_strerror", "c3c_last_error",
-        "c3c_workspace_bytes", "c3c_ctx_set_workspace", "c3c_conv3d_causal_cached_fused"])
+        "c3c_workspace_bytes", "c3c_ctx_set_workspace", "c3c_conv3d_causal_cached_fused",
+        "c3c_mfma_probe"])
     for n in names:
         assert hasattr(c3c.lib, n), n
 
@@ -277,3 +278,13 @@ def test_fused_call_argument_checks():
     assert _fcall(ctx, sp, scale=None, shift=None, res=None) == c3c.E_UNSUPPORTED
     c = ctx.counters()
     assert c["calls"] == 5 and c["strict_rejects"] == 5
+
+
+def test_mfma_probe_argument_checks():
+    fl = C.c_double()
+    f = c3c.lib.c3c_mfma_probe
+    assert f(0, 10, 0x10000000, C.byref(fl), None) == c3c.E_INVAL
+    assert f(4, 0, 0x10000000, C.byref(fl), None) == c3c.E_INVAL
+    assert f(4, 10, None, C.byref(fl), None) == c3c.E_INVAL
+    assert f(4, 10, 0x10000000, None, None) == c3c.E_INVAL
+    assert f(1 << 31, 10, 0x10000000, C.byref(fl), None) == c3c.E_INVAL
