@@ -87,8 +87,9 @@ typedef enum c3c_route { C3C_ROUTE_FAST = 0, C3C_ROUTE_FALLBACK = 1 } c3c_route;
  * is widened: a 1x1 spatial kernel (a temporal convolution) is accepted at
  * any temporal stride.  Clauses 8-9 state what the fast kernels are
  * specialised for: the 3x3 form (stride 1, pad 1, dilation 1) of the
- * decoder's main convolutions and the 1x1 form (stride 1, pad 0) of its
- * temporal convolutions. */
+ * decoder's main convolutions, also with a single temporal tap (a per-frame
+ * spatial convolution), and the 1x1 form (stride 1, pad 0) of its temporal
+ * convolutions, with at least two temporal taps. */
 typedef enum c3c_reason {
   C3C_REASON_NONE = 0,      /* routes fast                                   */
   C3C_REASON_FORCED = 1,    /* C3C_MODE_FORCE_FALLBACK                       */
@@ -98,7 +99,8 @@ typedef enum c3c_reason {
   C3C_REASON_PAD_RIGHT = 5, /* pad_t_right < 0                               */
   C3C_REASON_NO_OUTPUT = 6, /* To < 1                                        */
   C3C_REASON_NO_TAP = 7,    /* no (output frame, tap) pair reads a frame of Z */
-  C3C_REASON_KT1 = 8,       /* Kt < 2 (e.g. a 1x1x1 shortcut conv)           */
+  C3C_REASON_KT1 = 8,       /* Kt < 2 and the spatial kernel is not the 3x3
+                               form (e.g. a 1x1x1 shortcut conv)             */
   C3C_REASON_SPATIAL = 9,   /* spatial kernel is neither 3x3 (stride 1, pad 1,
                                dil 1) nor 1x1 (stride 1, pad 0)              */
   /* not a predicate clause: the call routed fast, the fast route failed and

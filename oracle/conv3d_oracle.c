@@ -49,7 +49,9 @@
  * one of two spatial forms, 3x3 / stride 1 / pad 1 / dilation 1 or 1x1 /
  * stride 1 / pad 0.  The guard's unit-temporal-stride clause is kept for the
  * 3x3 form; the 1x1 form (a temporal convolution, one matrix product per
- * output frame and tap) also accepts other temporal strides.
+ * output frame and tap) also accepts other temporal strides.  K_t >= 2 is
+ * asked of the 1x1 form only: a 3x3 call with one temporal tap is a
+ * per-frame spatial convolution and routes fast.
  */
 #include <math.h>
 #include <stdint.h>
@@ -185,7 +187,7 @@ int ora_route(const ora_desc* d, int dtype_ok, int force_fallback, int* route,
     }
     if (!any)
       r = ORA_NO_TAP;
-    else if (d->Kt < 2)
+    else if (d->Kt < 2 && !k3x3)
       r = ORA_KT1;
     else if (!k3x3 && !k1x1)
       r = ORA_SPATIAL;

@@ -130,7 +130,9 @@ bool spatial_1x1(const c3c_conv_desc& d) {
 }
 
 // The route predicate: the first failing clause is the reason.  Temporal
-// stride other than 1 is accepted for the 1x1 spatial form only.
+// stride other than 1 is accepted for the 1x1 spatial form only; a single
+// temporal tap (Kt = 1) for the 3x3 form only (a per-frame spatial
+// convolution), so that a 1x1x1 convolution stays on the fallback.
 int decide(const Geo& g, uint32_t mode) {
   const c3c_conv_desc& d = g.d;
   if (mode & C3C_MODE_FORCE_FALLBACK) return C3C_REASON_FORCED;
@@ -140,7 +142,7 @@ int decide(const Geo& g, uint32_t mode) {
   if (d.pad_t_right < 0) return C3C_REASON_PAD_RIGHT;
   if (g.To < 1) return C3C_REASON_NO_OUTPUT;
   if (!any_active_tap(g)) return C3C_REASON_NO_TAP;
-  if (d.Kt < 2) return C3C_REASON_KT1;
+  if (d.Kt < 2 && !spatial_3x3(d)) return C3C_REASON_KT1;
   if (!spatial_3x3(d) && !spatial_1x1(d)) return C3C_REASON_SPATIAL;
   return C3C_REASON_NONE;
 }

@@ -292,3 +292,25 @@ def test_head_kernel_matches_oracle(over):
     ctx, _, m = _case(sp, "bf16")
     assert ctx.counters()["fast"] == 1
     say(f"  rel={m['rel']:.3e} cos={m['cos']:.8f}")
+
+
+# ---------------------------------------------------------------- one temporal tap
+# A (1,3,3) call (a per-frame spatial convolution) routes fast: the 3x3
+# kernels with a single tap, every tile configuration, the head kernel, fp32,
+# and W not a multiple of 8.
+KT1_CASES = [
+    ("bf16", dict(N=1, Ci=64, Co=160, T=3, Tc=0, H=20, W=80)),
+    ("bf16", dict(N=2, Ci=40, Co=96, T=2, Tc=0, H=13, W=37)),
+    ("bf16", dict(N=1, Ci=48, Co=192, T=2, Tc=0, H=12, W=64)),
+    ("bf16", dict(N=1, Ci=96, Co=3, T=2, Tc=0, H=19, W=104)),
+    ("f32", dict(N=1, Ci=20, Co=36, T=2, Tc=0, H=9, W=21)),
+]
+
+
+@pytest.mark.parametrize("dtype,over", KT1_CASES)
+def test_single_temporal_tap_routes_fast(dtype, over):
+    sp = spec(Kt=1, p_base=0, **over)
+    assert c3c.route_query(None, sp, dtype) == ("fast", "none")
+    ctx, _, m = _case(sp, dtype)
+    assert ctx.counters()["fast"] == 1
+    say(f"  rel={m['rel']:.3e} cos={m['cos']:.8f}")

@@ -40,7 +40,7 @@ MUTANTS = {
                           "        int64_t hz = h * d->s_h + i * d->d_h + d->p_h;\n        if (hz < 0 || hz >= d->H) continue;\n        int64_t off;")],
     "eq4_off_by_one": [("int64_t hi = Z - delta < To ? Z - delta : To;",
                         "int64_t hi = Z - delta - 1 < To ? Z - delta - 1 : To;")],
-    "route_kt_clause_missing": [("else if (d->Kt < 2)", "else if (d->Kt < 1)")],
+    "route_kt_clause_missing": [("else if (d->Kt < 2 && !k3x3)", "else if (d->Kt < 1 && !k3x3)")],
     # the fused form's parts
     "bf16_ties_away_from_zero": [("double r = nearbyint(a / q) * q;", "double r = round(a / q) * q;")],
     "bf16_one_bit_short": [("q = ldexp(1.0, ex - 1 - 7);", "q = ldexp(1.0, ex - 1 - 6);")],

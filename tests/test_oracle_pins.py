@@ -427,7 +427,11 @@ ROUTE_TABLE = [
     (dict(p_r=-1), "bf16", False, "pad_right"),
     (dict(T=0, Tc=2), "bf16", False, "no_output"),
     (dict(Kt=1, Kh=1, Kw=1, p_base=0, Tc=0), "bf16", False, "kt1"),
-    (dict(Kt=1, p_base=0, Tc=0), "bf16", False, "kt1"),
+    (dict(Kt=1, p_base=0, Tc=0), "bf16", False, "none"),   # (1,3,3): per-frame spatial conv
+    (dict(Kt=1, p_base=0, Tc=0), "f32", False, "none"),
+    (dict(Kt=1, p_base=0, Tc=2), "bf16", False, "none"),   # p_l = -2: the cache is not read
+    (dict(Kt=1, p_base=0, Tc=0, T=4, s_t=2), "bf16", False, "stride_t"),
+    (dict(Kt=1, p_base=0, Tc=0, Kh=5, Kw=5, p_h=2, p_w=2), "bf16", False, "kt1"),
     (dict(Kh=1, Kw=1), "bf16", False, "spatial"),
     (dict(p_h=0, H=5), "bf16", False, "spatial"),
     (dict(d_h=2, p_h=2), "bf16", False, "spatial"),
