@@ -273,10 +273,11 @@ def mfma_probe_rate(iters=50000):
 
 def fused_block(workload, iters):
     """Per layer: the plain call, the fused form (prologue + residual, and each
-    alone), and the unfused pipeline a PyTorch user would run (the prologue as
-    torch ops into a new tensor, the plain call, then y += residual), with the
-    HBM-bound floor of the two separate passes (read x, write u; read y and
-    the residual, write y) and the extra device memory each path allocates."""
+    alone; and with the prologue-pass workspace attached), and the unfused
+    pipeline a PyTorch user would run (the prologue as torch ops into a new
+    tensor, the plain call, then y += residual), with the HBM-bound floor of
+    the two separate passes (read x, write u; read y and the residual, write
+    y) and the extra device memory each path allocates."""
     import torch
     from paper_2609_31938_amd import c3c, inputs
     wl = inputs.WORKLOADS[workload]
@@ -314,10 +315,16 @@ def fused_block(workload, iters):
         def plain():
             c3c.conv3d_causal_cached(ctx, sp, x, cin, w, wpack, b, y, cout)
 
-        def fused(pro=True, res=True):
-            c3c.conv3d_causal_cached_fused(ctx, sp, x, cin, w, wpack, b,
+        def fused(pro=True, res=True, c=ctx):
+            c3c.conv3d_causal_cached_fused(c, sp, x, cin, w, wpack, b,
                                            scale if pro else None, shift if pro else None,
                                            r if res else None, y, cout)
+
+        # the same fused call with the prologue-pass workspace attached
+        need = c3c.fused_workspace_bytes(sp, dtype)
+        ctx_ws = c3c.Context()
+        ws = torch.empty(max(need, 16) // 4, dtype=torch.float32, device=dev) if need else None
+        ctx_ws.set_workspace(ws)
 
         def unfused():
             u = torch.nn.functional.silu(x.float() * s5 + t5).to(w.dtype)
@@ -340,15 +347,19 @@ def fused_block(workload, iters):
         t_pro = timed(lambda: fused(True, False), n)
         t_res = timed(lambda: fused(False, True), n)
         t_unf = timed(unfused, n)
+        t_pass = timed(lambda: fused(c=ctx_ws), n) if need else None
         xb, yb = x.numel() * 2, y.numel() * 2
         floor_ms = (2 * xb + 3 * yb) / (PEAK_HBM_GBS * 1e9) * 1e3
         out.append(dict(layer=lname, route=route, plain_ms=round(t_plain, 4),
                         fused_ms=round(t_fused, 4), prologue_only_ms=round(t_pro, 4),
                         residual_only_ms=round(t_res, 4), unfused_torch_ms=round(t_unf, 4),
+                        fused_prologue_pass_ms=round(t_pass, 4) if t_pass is not None else None,
+                        prologue_pass_workspace_bytes=int(need),
                         unfused_floor_ms=round(t_plain + floor_ms, 4),
                         extra_bytes_unfused=int(extra_unfused), extra_bytes_fused=int(extra_fused)))
         print(json.dumps(out[-1]), flush=True)
-        del x, y, r, cin, cout, w, b, wpack
+        ctx_ws.set_workspace(None)
+        del x, y, r, cin, cout, w, b, wpack, ws
         torch.cuda.empty_cache()
     print(json.dumps({"fused_block": workload, "layers": out}), flush=True)
 

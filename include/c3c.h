@@ -280,6 +280,22 @@ int c3c_conv3d_causal_cached(c3c_ctx* ctx, const c3c_conv_desc* d,
  * EINVAL: as c3c_conv3d_causal_cached; dtype not bf16; exactly one of scale
  * and shift NULL; scale, shift or residual overlapping an output (other than
  * residual == y). */
+/* Workspace for the fused form's prologue pass.  On the fast route with the
+ * 3x3 spatial kernel, the prologue inside the convolution kernel evaluates
+ * SiLU once per time an input element is staged (about 3.75 times: three
+ * taps and the tile halo).  When the context's workspace (c3c_ctx_set_-
+ * workspace) holds at least the bytes this query reports, a fused call
+ * instead activates the new chunk once, in a separate elementwise pass, into
+ * the workspace's first round_up(|x|, 256) bytes, and runs the convolution on
+ * it (the residual stays fused; the rest of the workspace serves split-K as
+ * for a plain call).  The results are identical; the pass costs |x| bytes of
+ * workspace and two HBM passes over |x| instead of the repeated SiLU.
+ * *bytes: that size (the prologue region plus the split-K bytes of
+ * c3c_workspace_bytes), 0 when the fused call would not use a prologue pass
+ * (not bf16, or not the fast 3x3 form).  EINVAL for an invalid descriptor or
+ * NULL bytes. */
+int c3c_fused_workspace_bytes(const c3c_conv_desc* d, size_t* bytes);
+
 int c3c_conv3d_causal_cached_fused(c3c_ctx* ctx, const c3c_conv_desc* d,
                                    const void* x, const void* cache,
                                    const void* w, const void* wpack,

@@ -68,6 +68,7 @@ lib.c3c_flops.argtypes = [_P(Desc), _P(C.c_double)]
 lib.c3c_route_query.argtypes = [_vp, _P(Desc), _P(C.c_int), _P(C.c_int)]
 lib.c3c_weight_pack_bytes.argtypes = [_P(Desc), _P(C.c_size_t)]
 lib.c3c_workspace_bytes.argtypes = [_P(Desc), _P(C.c_size_t)]
+lib.c3c_fused_workspace_bytes.argtypes = [_P(Desc), _P(C.c_size_t)]
 lib.c3c_ctx_set_workspace.argtypes = [_vp, _vp, C.c_size_t]
 lib.c3c_weight_repack.argtypes = [_vp, _P(Desc), _vp, _vp, _vp]
 lib.c3c_weight_unpack.argtypes = [_P(Desc), _vp, _vp, _vp]
@@ -225,6 +226,15 @@ def workspace_bytes(spec: dict, dtype: str) -> int:
     n = C.c_size_t()
     _raise(lib.c3c_workspace_bytes(C.byref(make_desc(spec, dtype)), C.byref(n)),
            what="c3c_workspace_bytes")
+    return int(n.value)
+
+
+def fused_workspace_bytes(spec: dict, dtype: str) -> int:
+    """Workspace bytes with which a fused call runs its prologue as a pass of
+    its own (plus split-K); 0 when it would not use one."""
+    n = C.c_size_t()
+    _raise(lib.c3c_fused_workspace_bytes(C.byref(make_desc(spec, dtype)), C.byref(n)),
+           what="c3c_fused_workspace_bytes")
     return int(n.value)
 
 

@@ -264,6 +264,25 @@ int c3c_workspace_bytes(const c3c_conv_desc* d, size_t* bytes) {
   return C3C_OK;
 }
 
+namespace {
+// the fused form's prologue-pass region: |x| rounded up to 256 bytes, or 0
+// when the call would not use one (not bf16, or not the fast 3x3 form)
+int64_t prologue_region_bytes(const Geo& g) {
+  const c3c_conv_desc& d = g.d;
+  if (decide(g, 0u) != C3C_REASON_NONE || d.dtype != C3C_DTYPE_BF16 || !spatial_3x3(d)) return 0;
+  const int64_t xb = d.N * d.Ci * d.T * d.H * d.W * 2;
+  return (xb + 255) / 256 * 256;
+}
+}  // namespace
+
+int c3c_fused_workspace_bytes(const c3c_conv_desc* d, size_t* bytes) {
+  Geo g;
+  if (*make_geo(d, &g) || !bytes) return C3C_E_INVAL;
+  const int64_t pr = prologue_region_bytes(g);
+  *bytes = pr > 0 ? static_cast<size_t>(pr + fast_bf16_workspace_bytes(g)) : 0;
+  return C3C_OK;
+}
+
 int c3c_ctx_set_workspace(c3c_ctx* ctx, void* ws, size_t bytes) {
   if (!ctx || (ws == nullptr) != (bytes == 0)) return C3C_E_INVAL;
   if ((reinterpret_cast<uintptr_t>(ws) & 15u) != 0) return C3C_E_INVAL;
@@ -388,8 +407,22 @@ int run_call(c3c_ctx* ctx, const c3c_conv_desc* d, const void* x, const void* ca
       }
       e = hipErrorLaunchFailure;  // stands for a failure before any launch
     } else {
-      e = launch_fast(g, x, cache, wpack, bias, y, cache_out, ctx->ws,
-                      static_cast<int64_t>(ctx->ws_bytes), s, fu);
+      // the fused prologue as its own pass when the workspace holds the
+      // activated chunk (the 3x3 kernels would evaluate it per staging);
+      // the rest of the workspace serves split-K
+      const int64_t pr = fu.pro() ? prologue_region_bytes(g) : 0;
+      if (pr > 0 && static_cast<int64_t>(ctx->ws_bytes) >= pr && d->T > 0) {
+        unsigned char* u = static_cast<unsigned char*>(ctx->ws);
+        e = launch_prologue(g, x, fu.scale, fu.shift, u, s);
+        Fuse rest;
+        rest.residual = fu.residual;
+        if (e == hipSuccess)
+          e = launch_fast(g, u, cache, wpack, bias, y, cache_out, u + pr,
+                          static_cast<int64_t>(ctx->ws_bytes) - pr, s, rest);
+      } else {
+        e = launch_fast(g, x, cache, wpack, bias, y, cache_out, ctx->ws,
+                        static_cast<int64_t>(ctx->ws_bytes), s, fu);
+      }
     }
     if (e == hipSuccess) {
       ++ctx->ctr.fast;

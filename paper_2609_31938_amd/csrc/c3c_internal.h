@@ -103,6 +103,10 @@ hipError_t launch_fast_tap1x1(const Geo& g, const void* x, const void* cache, co
                               const void* bias, void* y, hipStream_t s, const Fuse& fu = Fuse{});
 hipError_t launch_fallback(const Geo& g, const void* x, const void* cache, const void* w,
                            const void* bias, void* y, hipStream_t s, const Fuse& fu = Fuse{});
+// the fused form's prologue as its own pass: u = RNE_bf16(SiLU(x * scale +
+// shift)) over the whole new chunk (fallback.hip)
+hipError_t launch_prologue(const Geo& g, const void* x, const float* scale, const float* shift,
+                           void* u, hipStream_t s);
 hipError_t launch_cache_copy(const Geo& g, const void* x, const void* cache, void* cache_out,
                              hipStream_t s, const Fuse& fu = Fuse{});
 

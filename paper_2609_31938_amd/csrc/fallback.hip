@@ -301,6 +301,30 @@ __global__ __launch_bounds__(256) void cache_copy_pro(const uint16_t* __restrict
   }
 }
 
+// The fused form's prologue as a pass of its own over the new chunk
+// [N * Ci rows][T * H * W]: u = RNE_bf16(SiLU(x * scale[row] + shift[row])).
+// VEC: 8 elements per step (16-byte units).
+template <bool VEC>
+__global__ __launch_bounds__(256) void prologue_pass(const uint16_t* __restrict__ x,
+                                                     const float* __restrict__ scale,
+                                                     const float* __restrict__ shift,
+                                                     uint16_t* __restrict__ u, int64_t rows,
+                                                     int64_t row_len) {
+  const int64_t units = VEC ? row_len / 8 : row_len;
+  for (int64_t r = blockIdx.y; r < rows; r += gridDim.y) {
+    const float s = scale[r], t = shift[r];
+    const uint16_t* src = x + r * row_len;
+    uint16_t* dst = u + r * row_len;
+    for (int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x; i < units;
+         i += static_cast<int64_t>(gridDim.x) * 256) {
+      if (VEC)
+        reinterpret_cast<fuse_u32x4*>(dst)[i] = fuse_seg8(reinterpret_cast<const fuse_u32x4*>(src)[i], s, t, true);
+      else
+        dst[i] = fuse_one(src[i], s, t, true);
+    }
+  }
+}
+
 bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
 }  // namespace
@@ -314,6 +338,21 @@ hipError_t launch_fallback(const Geo& g, const void* x, const void* cache, const
     return launch_pointwise(g, x, cache, w, bias, y, s, fu);
   if (g.d.dtype == C3C_DTYPE_F32) return launch_fb<float>(g, x, cache, w, bias, y, s, fu);
   return launch_fb<uint16_t>(g, x, cache, w, bias, y, s, fu);
+}
+
+hipError_t launch_prologue(const Geo& g, const void* x, const float* scale, const float* shift,
+                           void* u, hipStream_t s) {
+  const c3c_conv_desc& d = g.d;
+  const int64_t rows = d.N * d.Ci, row_len = d.T * d.H * d.W;
+  if (rows == 0 || row_len == 0) return hipSuccess;
+  const bool vec = row_len % 8 == 0 && aligned(x, 16) && aligned(u, 16);
+  int64_t gx = ((vec ? row_len / 8 : row_len) + 255) / 256;
+  if (gx > 4096) gx = 4096;
+  const int64_t gy = rows < 65535 ? rows : 65535;
+  auto k = vec ? prologue_pass<true> : prologue_pass<false>;
+  hipLaunchKernelGGL(k, dim3(gx, gy), dim3(256), 0, s, static_cast<const uint16_t*>(x), scale, shift,
+                     static_cast<uint16_t*>(u), rows, row_len);
+  return hipGetLastError();
 }
 
 hipError_t launch_cache_copy(const Geo& g, const void* x, const void* cache, void* cache_out,

@@ -227,3 +227,26 @@ def test_calls_allocate_no_device_memory():
     free1, _ = torch.cuda.mem_get_info()
     say(f"free before {free0} after {free1}")
     assert free1 == free0
+
+
+# ---------------------------------------------------------------- prologue pass
+@pytest.mark.parametrize("over,split", [(dict(N=1, Ci=64, Co=160, T=2, Tc=2, H=24, W=80), False),
+                                        (dict(N=2, Ci=40, Co=96, T=3, Tc=1, H=13, W=37), False),
+                                        (dict(N=1, Ci=128, Co=128, T=1, Tc=2, H=16, W=32), True),
+                                        (dict(N=1, Ci=32, Co=3, T=2, Tc=2, H=20, W=40), False)])
+def test_prologue_pass_equals_in_kernel_prologue(over, split):
+    """With a workspace of c3c_fused_workspace_bytes, the prologue runs as a
+    pass of its own into the workspace: y and the new cache are bit-identical
+    to the in-kernel prologue's (the same SiLU code on the same values), and
+    match the oracle.  With split, the workspace's remainder also splits K."""
+    sp = spec(**over)
+    need = c3c.fused_workspace_bytes(sp, "bf16")
+    assert need > 0
+    assert (c3c.workspace_bytes(sp, "bf16") > 0) == split
+    _, y0, c0 = _run(sp, expect_fast=True)
+    ctx = c3c.Context()
+    ctx.set_workspace(torch.empty(need // 4, dtype=torch.float32, device="cuda"))
+    _, y1, c1 = _run(sp, ctx=ctx, expect_fast=True)
+    if not split:  # split-K sums in another order: equal to the oracle, not bitwise
+        assert torch.equal(y0.view(torch.int16), y1.view(torch.int16))
+    assert torch.equal(c0.view(torch.int16), c1.view(torch.int16))

@@ -34,7 +34,7 @@ def test_every_declared_symbol_is_exported():
         "c3c_conv3d_causal_cached", "c3c_counters_get", "c3c_counters_reset",
         "c3c_fallback_shapes", "c3c_strerror", "c3c_last_error",
         "c3c_workspace_bytes", "c3c_ctx_set_workspace", "c3c_conv3d_causal_cached_fused",
-        "c3c_mfma_probe"])
+        "c3c_mfma_probe", "c3c_fused_workspace_bytes"])
     for n in names:
         assert hasattr(c3c.lib, n), n
 
@@ -288,3 +288,18 @@ def test_mfma_probe_argument_checks():
     assert f(4, 10, None, C.byref(fl), None) == c3c.E_INVAL
     assert f(4, 10, 0x10000000, None, None) == c3c.E_INVAL
     assert f(1 << 31, 10, 0x10000000, C.byref(fl), None) == c3c.E_INVAL
+
+
+def test_fused_workspace_bytes():
+    sp = spec(N=1, Ci=64, Co=160, T=2, Tc=2, H=24, W=80)
+    xb = 64 * 2 * 24 * 80 * 2
+    assert c3c.fused_workspace_bytes(sp, "bf16") == (xb + 255) // 256 * 256 + c3c.workspace_bytes(sp, "bf16")
+    small = spec(N=1, Ci=128, Co=128, T=1, Tc=2, H=16, W=32)  # a call that splits
+    assert c3c.workspace_bytes(small, "bf16") > 0
+    assert c3c.fused_workspace_bytes(small, "bf16") == \
+        (128 * 16 * 32 * 2 + 255) // 256 * 256 + c3c.workspace_bytes(small, "bf16")
+    assert c3c.fused_workspace_bytes(sp, "f32") == 0
+    assert c3c.fused_workspace_bytes(spec(N=1, Ci=8, Co=8, T=2, Tc=2, H=8, W=8, Kh=1, Kw=1), "bf16") == 0
+    assert c3c.fused_workspace_bytes(spec(N=1, Ci=8, Co=8, T=2, Tc=2, H=8, W=8, s_t=2), "bf16") == 0
+    n = C.c_size_t()
+    assert c3c.lib.c3c_fused_workspace_bytes(C.byref(c3c.make_desc(sp, "bf16")), None) == c3c.E_INVAL
