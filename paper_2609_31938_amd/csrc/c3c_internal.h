@@ -81,7 +81,7 @@ int64_t device_compute_units();
 // output channels per workgroup of the two bf16 1x1 kernels of the fast route
 constexpr int64_t kTap1x1TileCo = 192;     // conv_tap1x1.hip
 constexpr int64_t kPointwiseTileCo = 160;  // pointwise.hip
-// fast route, bf16, 1x1 spatial kernel (conv_tap1x1.hip): 192 x 320 output
+// fast route, bf16, 1x1 spatial kernel (conv_tap1x1.hip): 192 x 128 output
 // tiles on 4 waves; needs H * W a multiple of 8 and aligned pointers.  The
 // caller copies the cache.
 bool tap1x1_eligible(const Geo& g, const void* x, const void* cache, const void* y);

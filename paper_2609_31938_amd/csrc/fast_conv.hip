@@ -318,16 +318,15 @@ hipError_t launch_fast(const Geo& g, const void* x, const void* cache, const voi
   hipError_t e;
   if (g.d.dtype == C3C_DTYPE_BF16) {
     if (one) {
-      // Two kernels.  The 8-wave pointwise kernel (160-channel tiles, any
-      // alignment) does more useful work per cycle when both pad the output
-      // channels alike (measured: about 8% at Co = 768); the 4-wave kernel
-      // (192-channel tiles) wins where it pads at least 10% fewer channels
-      // (Co = 384: 384 against 480) and its 192 x 320 tiles still give every
-      // compute unit half a workgroup.  The fused form (prologue / residual)
-      // is in the pointwise kernel only.
+      // Two kernels: the 4-wave 192 x 128 kernel (aligned calls; 1.2-1.5x
+      // the pointwise kernel at Co = 768 and 384) unless its padded output
+      // channels exceed the 160-channel pointwise tile's by more than 10%
+      // (Co = 96, 160, 256, 320 stay on the pointwise kernel) or its tiles
+      // leave half the compute units idle.  The fused form (prologue /
+      // residual) is in the pointwise kernel only.
       const int64_t pad_tap = (g.d.Co + kTap1x1TileCo - 1) / kTap1x1TileCo * kTap1x1TileCo;
       const int64_t pad_pw = (g.d.Co + kPointwiseTileCo - 1) / kPointwiseTileCo * kPointwiseTileCo;
-      if (!fu.any() && 10 * pad_tap <= 9 * pad_pw && tap1x1_eligible(g, x, cache, y) &&
+      if (!fu.any() && 10 * pad_tap <= 11 * pad_pw && tap1x1_eligible(g, x, cache, y) &&
           2 * tap1x1_blocks(g) >= device_compute_units())
         e = launch_tap1x1(g, x, cache, wpack, bias, y, s);
       else
