@@ -777,13 +777,16 @@ Plan plan_bf16(const Geo& g) {
     set_tiles(g, 192, 4, 64, &p);
   } else if (Co <= 16) {
     // a head conv with a few output channels (e.g. 3, to RGB): one 16-channel
-    // fragment per wave, so the matrix cores do 1/6 of the 96-channel tile's
-    // work on the same staged activations
+    // fragment per wave on an 8 x 64 tile, 1/6 of the matrix-core work of a
+    // 96-channel tile
     p.cfg = CFG_C16;
     set_tiles(g, 16, 8, 64, &p);
   } else if (Co <= 96) {
+    // 96 channels x 6 x 64 pixels on 2 x 2 waves (48 channels x 3 rows each):
+    // each weight fragment is fetched by two waves, not four, and the smaller
+    // halo tile leaves room for three LDS buffers
     p.cfg = CFG_C96;
-    set_tiles(g, 96, 8, 64, &p);
+    set_tiles(g, 96, 6, 64, &p);
   } else {
     // 160-channel tiles of 4 x 80 or 10 x 32 pixels.  A workgroup of either
     // shape takes about the same time (measured), so the shape with fewer
@@ -886,7 +889,7 @@ hipError_t launch_fast_bf16(const Geo& g, const void* x, const void* cache, cons
   a.part = split ? static_cast<float*>(ws) : nullptr;
   switch (pl.cfg) {
     case CFG_C192: return run<6, 2, 4, 2, 2, 3>(g, a, pl, aligned, fused, s);
-    case CFG_C96: return run<6, 2, 4, 1, 4, 2>(g, a, pl, aligned, fused, s);
+    case CFG_C96: return run<3, 3, 4, 2, 2, 3>(g, a, pl, aligned, fused, s);
     case CFG_C16: return run<1, 2, 4, 1, 4, 2>(g, a, pl, aligned, fused, s);
     case CFG_C160_4X80: return run<5, 2, 5, 2, 2, 3>(g, a, pl, aligned, fused, s);
     default: return run<5, 5, 2, 2, 2, 3>(g, a, pl, aligned, fused, s);

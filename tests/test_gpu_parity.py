@@ -76,6 +76,7 @@ FAST_CASES = [
     ("bf16", dict(N=1, Ci=48, Co=80, T=3, Tc=2, H=37, W=70)),
     ("bf16", dict(N=2, Ci=32, Co=64, T=2, Tc=1, H=9, W=33)),
     ("bf16", dict(N=1, Ci=160, Co=96, T=4, Tc=2, H=20, W=100)),
+    ("bf16", dict(N=1, Ci=96, Co=96, T=2, Tc=2, H=20, W=136)),         # 6 x 64 tiles, ragged both ways
     ("bf16", dict(N=1, Ci=16, Co=32, T=1, Tc=0, H=5, W=5)),
     ("bf16", dict(N=1, Ci=24, Co=40, T=2, Tc=3, H=11, W=65)),          # p_l < 0
     ("bf16", dict(N=1, Ci=64, Co=192, T=4, Tc=2, H=16, W=64)),
