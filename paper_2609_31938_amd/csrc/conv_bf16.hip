@@ -313,9 +313,6 @@ __global__ __launch_bounds__(64 * WAVES_CO * WAVES_PX, 1) void conv3d_bf16(Args 
           st.rs, h_ok[hh] ? h_ch[hh] * st.cs + h_pix[hh] : OOB, 0, 0);
   };
 
-  // PRO: the prologue on the staged registers of a new-chunk stage (a
-  // workgroup-uniform skip for cache frames, selects inside).  A task is in
-  // the image when t_ok; without ALIGNED its pixels past W are padding too.
   // PRO: the prologue on the staged registers of part `part` of a stage
   // (rows 2 part, 2 part + 1 of every task for part 0..3, the halo for part
   // 4), applied a few steps after that part's loads were issued so that the
