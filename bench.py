@@ -19,6 +19,7 @@ TFLOP/s and fraction of the 2.5 PFLOP/s bf16 matrix peak, the dominant
 kernel's roofline, and the oracle's CPU rate on a bounded sample.
 """
 import argparse
+import gc
 import json
 import math
 import os
@@ -145,6 +146,11 @@ def main():
     ev = [[[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in layers]
           for _ in range(args.steps)]
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    # Python's cyclic collector can stall the host for tens of milliseconds
+    # between two launches (seen at fixed points of a run): run it before the
+    # timed region and hold it off inside
+    gc.collect()
+    gc.disable()
     torch.cuda.synchronize()
     t_wall = time.perf_counter()
     start.record()
@@ -153,6 +159,7 @@ def main():
     stop.record()
     torch.cuda.synchronize()
     t_wall = time.perf_counter() - t_wall
+    gc.enable()
     total_ms = start.elapsed_time(stop)
 
     counters = ctx.counters()
@@ -288,6 +295,8 @@ def fused_block(workload, iters):
 
     def timed(fn, n):
         fn()
+        gc.collect()
+        gc.disable()  # no collector pause inside the timed launches
         torch.cuda.synchronize()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record()
@@ -295,6 +304,7 @@ def fused_block(workload, iters):
             fn()
         e1.record()
         torch.cuda.synchronize()
+        gc.enable()
         return e0.elapsed_time(e1) / n
 
     for lid, (lname, sp) in enumerate(wl["layers"]):
