@@ -134,6 +134,12 @@ def main():
                 L_["cur"] = 1 - L_["cur"]
 
     # ---------------------------------------------------------------- warmup
+    # Python's cyclic collector can stall the host for tens of milliseconds
+    # between two launches (seen at fixed points of a run): it runs before
+    # the warm-up and is held off until the timed region ends.  Not between
+    # the two: an idle gap there lets the clocks fall before the timed steps.
+    gc.collect()
+    gc.disable()
     reset_caches()
     for s in range(args.warmup):
         step(s)
@@ -146,11 +152,6 @@ def main():
     ev = [[[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in layers]
           for _ in range(args.steps)]
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    # Python's cyclic collector can stall the host for tens of milliseconds
-    # between two launches (seen at fixed points of a run): run it before the
-    # timed region and hold it off inside
-    gc.collect()
-    gc.disable()
     torch.cuda.synchronize()
     t_wall = time.perf_counter()
     start.record()
@@ -294,9 +295,9 @@ def fused_block(workload, iters):
     out = []
 
     def timed(fn, n):
-        fn()
         gc.collect()
-        gc.disable()  # no collector pause inside the timed launches
+        gc.disable()  # no collector pause from the warm-up call to the end
+        fn()
         torch.cuda.synchronize()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record()
