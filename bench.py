@@ -295,8 +295,6 @@ def fused_block(workload, iters):
     out = []
 
     def timed(fn, n):
-        gc.collect()
-        gc.disable()  # no collector pause from the warm-up call to the end
         fn()
         torch.cuda.synchronize()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -305,10 +303,14 @@ def fused_block(workload, iters):
             fn()
         e1.record()
         torch.cuda.synchronize()
-        gc.enable()
         return e0.elapsed_time(e1) / n
 
     for lid, (lname, sp) in enumerate(wl["layers"]):
+        # the collector runs here, before the layer's inputs are made, and
+        # is held off through its measurements (no pause between launches,
+        # no idle gap that lets the clocks fall before a timed call)
+        gc.collect()
+        gc.disable()
         w, b = inputs.layer_tensors(sp, dtype, wl["id"], lid, dev)
         route, _ = c3c.route_query(None, sp, dtype)
         wpack = c3c.weight_repack(ctx, sp, w) if route == "fast" else None
@@ -371,6 +373,7 @@ def fused_block(workload, iters):
         print(json.dumps(out[-1]), flush=True)
         ctx_ws.set_workspace(None)
         del x, y, r, cin, cout, w, b, wpack, ws
+        gc.enable()
         torch.cuda.empty_cache()
     print(json.dumps({"fused_block": workload, "layers": out}), flush=True)
 
