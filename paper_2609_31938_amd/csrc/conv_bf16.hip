@@ -888,7 +888,9 @@ hipError_t launch_fast_bf16(const Geo& g, const void* x, const void* cache, cons
     case CFG_C192: return run<6, 2, 4, 2, 2, 3>(g, a, pl, aligned, fused, s);
     case CFG_C96: return run<3, 3, 4, 2, 2, 3>(g, a, pl, aligned, fused, s);
     case CFG_C16: return run<1, 2, 4, 1, 4, 2>(g, a, pl, aligned, fused, s);
-    case CFG_C160_4X80: return run<5, 2, 5, 2, 2, 3>(g, a, pl, aligned, fused, s);
+    // two LDS buffers measured 1.4-3.4% faster than three on the 720p
+    // layers for this tile (the 192- and 96-channel tiles keep three)
+    case CFG_C160_4X80: return run<5, 2, 5, 2, 2, 2>(g, a, pl, aligned, fused, s);
     default: return run<5, 5, 2, 2, 2, 3>(g, a, pl, aligned, fused, s);
   }
 }
