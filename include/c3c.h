@@ -130,8 +130,10 @@ typedef struct c3c_conv_desc {
 } c3c_conv_desc;
 
 typedef struct c3c_counters {
-  /* Invariants: calls = fast + fallback + strict_rejects
-   *             fallback = unsupported + forced + fast_error */
+  /* Invariants: calls = fast + fallback + strict_rejects + failed
+   *             fallback = unsupported + forced + fast_error
+   * A call is counted in fast / fallback (and its reason) only once its
+   * kernels were enqueued without error. */
   uint64_t calls;          /* valid calls (EINVAL calls are not counted)     */
   uint64_t fast;           /* completed on the fast route                    */
   uint64_t fallback;       /* completed on the fallback route                */
@@ -140,6 +142,8 @@ typedef struct c3c_counters {
   uint64_t fast_error;     /* fell back because the fast route failed        */
   uint64_t strict_rejects; /* refused in strict mode                         */
   uint64_t repacks;        /* weight repacks enqueued                        */
+  uint64_t failed;         /* the fallback's own launch failed: the call
+                              returned C3C_E_DEVICE and computed nothing     */
 } c3c_counters;
 
 /* One entry of the fallback-shape histogram: the reason and the full call
@@ -185,6 +189,47 @@ int c3c_flops(const c3c_conv_desc* d, double* flops);
 int c3c_route_query(const c3c_ctx* ctx, const c3c_conv_desc* d, int* route,
                     int* reason);
 
+/* ---------------------------------------------------------------- launch plan */
+/* The kernels of the library.  The fast route's 3x3 form runs on
+ * CONV3D_BF16 (or FAST_F32), with HEAD for few output channels; its 1x1 form
+ * on TAP1X1 or POINTWISE; the fallback on POINTWISE (1x1x1 calls) or
+ * FALLBACK_DIRECT. */
+typedef enum c3c_kernel {
+  C3C_KERNEL_NONE = 0,            /* nothing to compute (no output frame)      */
+  C3C_KERNEL_CONV3D_BF16 = 1,     /* the implicit-GEMM kernel, bf16, 3x3       */
+  C3C_KERNEL_HEAD = 2,            /* bf16, 3x3, Co <= 5: taps as GEMM columns  */
+  C3C_KERNEL_TAP1X1 = 3,          /* bf16, 1x1: 192-channel x 128-pixel tiles  */
+  C3C_KERNEL_POINTWISE = 4,       /* bf16 / f16 per-frame matrix products      */
+  C3C_KERNEL_FAST_F32 = 5,        /* fp32 matrix cores, 3x3 and 1x1            */
+  C3C_KERNEL_FALLBACK_DIRECT = 6  /* generic direct Conv3D, fp32 accumulation  */
+} c3c_kernel;
+
+/* What one plain call (c3c_conv3d_causal_cached) would launch: its route,
+ * the main kernel and its workgroup tile, as chosen by the same code that
+ * launches it.  tile_h == 0 marks a kernel that tiles the flattened Ho*Wo
+ * plane: tile_w is then a run of consecutive pixels of that plane. */
+typedef struct c3c_plan {
+  int32_t route;           /* enum c3c_route                                 */
+  int32_t reason;          /* enum c3c_reason                                */
+  int32_t kernel;          /* enum c3c_kernel                                */
+  int32_t splits;          /* split-K factor (1: unsplit)                    */
+  int64_t tile_co;         /* output channels per workgroup                  */
+  int64_t tile_h, tile_w;  /* output rows x columns per workgroup            */
+  int64_t workgroups;      /* of the main launch, every split included       */
+  int32_t cache_in_kernel; /* 1: the main kernel writes cache_out itself     */
+  int32_t reserved;
+} c3c_plan;
+
+/* Fill *out with the plan of a plain call under ctx's mode (ctx may be NULL:
+ * mode 0) with a split-K workspace of ws_bytes attached.  Pure host code; it
+ * reads the current device's compute-unit count as the launch does (256 when
+ * no device is visible).  The plan assumes 16-byte-aligned tensors: a call
+ * with misaligned tensors may take an unaligned variant of the same tile or,
+ * for HEAD and TAP1X1, the CONV3D_BF16 and POINTWISE kernels.
+ * EINVAL for an invalid descriptor or NULL out. */
+int c3c_plan_query(const c3c_ctx* ctx, const c3c_conv_desc* d, size_t ws_bytes,
+                   c3c_plan* out);
+
 /* ---------------------------------------------------------------- workspace */
 /* Split-K workspace.  A bf16 fast call whose output tiles cannot fill the
  * device's compute units (few output frames at a low resolution, such as one
@@ -196,8 +241,11 @@ int c3c_route_query(const c3c_ctx* ctx, const c3c_conv_desc* d, int* route,
  *
  * c3c_workspace_bytes: the bytes a call with this descriptor would use, 0
  * when it would run unsplit (large calls, non-bf16, or not routing fast).
- * Depends on the current device's compute-unit count (256 is assumed when no
- * device is visible).  EINVAL for an invalid descriptor or NULL bytes.
+ * The split is planned from the compute-unit count of the device that is
+ * current when the query runs (256 is assumed when no device is visible):
+ * query and launch with the same device current, since a workspace sized for
+ * one device can be too small for the plan on another, and the call then
+ * runs unsplit.  EINVAL for an invalid descriptor or NULL bytes.
  *
  * c3c_ctx_set_workspace: attach a device buffer (caller-owned, 16-byte
  * aligned) to the context; (NULL, 0) detaches.  A call splits only when the
@@ -238,9 +286,11 @@ int c3c_weight_unpack(const c3c_conv_desc* d, const void* wpack, void* w_out,
  * Fallback route: the direct-Conv3D kernel reads w (wpack may be NULL), then a
  * copy kernel writes cache_out.
  *
- * Counters: calls++ first; then fast++, or fallback++ with unsupported /
- * forced / fast_error, or strict_rejects++ (with C3C_E_UNSUPPORTED or
- * C3C_E_INJECTED).  A call returning EINVAL is not counted.
+ * Counters: calls++ first; then, once the call's kernels are enqueued,
+ * fast++, or fallback++ with unsupported / forced / fast_error; or
+ * strict_rejects++ (with C3C_E_UNSUPPORTED, C3C_E_INJECTED or C3C_E_DEVICE
+ * in strict mode); or failed++ when the fallback's own launch fails
+ * (C3C_E_DEVICE).  A call returning EINVAL is not counted.
  * EINVAL: NULL ctx/desc, invalid descriptor, a required pointer NULL,
  * cache_out overlapping cache or x, y overlapping any input, or wpack NULL
  * on a call that routes fast. */

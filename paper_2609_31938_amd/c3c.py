@@ -30,6 +30,7 @@ MODE_STRICT, MODE_FORCE_FALLBACK, MODE_INJECT_FAST_FAILURE = 1, 2, 4
 ROUTES = ["fast", "fallback"]
 REASONS = ["none", "forced", "dtype", "groups", "stride_t", "pad_right", "no_output",
            "no_tap", "kt1", "spatial", "fast_error"]
+KERNELS = ["none", "conv3d_bf16", "head", "tap1x1", "pointwise", "fast_f32", "fallback_direct"]
 
 
 class C3CError(RuntimeError):
@@ -48,7 +49,14 @@ class Desc(C.Structure):
 
 class Counters(C.Structure):
     _fields_ = [(n, C.c_uint64) for n in ("calls", "fast", "fallback", "unsupported", "forced",
-                                          "fast_error", "strict_rejects", "repacks")]
+                                          "fast_error", "strict_rejects", "repacks", "failed")]
+
+
+class Plan(C.Structure):
+    _fields_ = [("route", C.c_int32), ("reason", C.c_int32), ("kernel", C.c_int32),
+                ("splits", C.c_int32), ("tile_co", C.c_int64), ("tile_h", C.c_int64),
+                ("tile_w", C.c_int64), ("workgroups", C.c_int64), ("cache_in_kernel", C.c_int32),
+                ("reserved", C.c_int32)]
 
 
 class SigCount(C.Structure):
@@ -66,6 +74,7 @@ lib.c3c_output_dims.argtypes = [_P(Desc), _P(_i64), _P(_i64), _P(_i64), _P(_i64)
 lib.c3c_tap_interval.argtypes = [_P(Desc), _i64, _P(_i64), _P(_i64)]
 lib.c3c_flops.argtypes = [_P(Desc), _P(C.c_double)]
 lib.c3c_route_query.argtypes = [_vp, _P(Desc), _P(C.c_int), _P(C.c_int)]
+lib.c3c_plan_query.argtypes = [_vp, _P(Desc), C.c_size_t, _P(Plan)]
 lib.c3c_weight_pack_bytes.argtypes = [_P(Desc), _P(C.c_size_t)]
 lib.c3c_workspace_bytes.argtypes = [_P(Desc), _P(C.c_size_t)]
 lib.c3c_fused_workspace_bytes.argtypes = [_P(Desc), _P(C.c_size_t)]
@@ -214,6 +223,19 @@ def route_query(ctx, spec: dict, dtype: str):
     return ROUTES[r.value], REASONS[why.value]
 
 
+def plan_query(ctx, spec: dict, dtype: str, ws_bytes: int = 0) -> dict:
+    """What a plain call would launch (c3c_plan_query): route, reason, kernel
+    name, workgroup tile (tile_h == 0: tile_w pixels of the flattened plane),
+    workgroups, split-K factor, and whether the kernel writes the cache."""
+    p = Plan()
+    _raise(lib.c3c_plan_query(ctx._h if ctx is not None else None,
+                              C.byref(make_desc(spec, dtype)), ws_bytes, C.byref(p)),
+           ctx, "c3c_plan_query")
+    return dict(route=ROUTES[p.route], reason=REASONS[p.reason], kernel=KERNELS[p.kernel],
+                splits=p.splits, tile_co=p.tile_co, tile_h=p.tile_h, tile_w=p.tile_w,
+                workgroups=p.workgroups, cache_in_kernel=bool(p.cache_in_kernel))
+
+
 def weight_pack_bytes(spec: dict, dtype: str) -> int:
     n = C.c_size_t()
     _raise(lib.c3c_weight_pack_bytes(C.byref(make_desc(spec, dtype)), C.byref(n)),
@@ -253,18 +275,41 @@ def dtype_of(t) -> str:
     return {torch.bfloat16: "bf16", torch.float32: "f32", torch.float16: "f16"}[t.dtype]
 
 
-def _ptr(t, name, dtype, numel=None):
+def _check(t, name, dtype, numel=None):
+    """A tensor's dtype, layout and element count (every extent the kernels
+    use comes from the descriptor, so a short buffer would be read or written
+    out of bounds)."""
     if t is None:
-        return None
-    if not t.is_cuda:
-        raise ValueError(f"{name} must be a device tensor")
-    if not t.is_contiguous():
-        raise ValueError(f"{name} must be contiguous")
+        return
     if t.dtype != _torch_dtype(dtype):
         raise ValueError(f"{name} has dtype {t.dtype}, expected {dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
     if numel is not None and t.numel() != numel:
         raise ValueError(f"{name} has {t.numel()} elements, expected {numel}")
+
+
+def _ptr(t, name, dtype, numel=None):
+    """The device address of a checked tensor."""
+    if t is None:
+        return None
+    _check(t, name, dtype, numel)
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
     return t.data_ptr() or None
+
+
+def _sizes(spec: dict, dtype: str):
+    """Element counts of every tensor of a call: x, cache, w, wpack (0 when
+    the call has no fast layout), bias, y, cache_out."""
+    To, Ho, Wo, L = output_dims(spec, dtype)
+    hw = spec["H"] * spec["W"]
+    nci = spec["N"] * spec["Ci"]
+    es = 4 if dtype == "f32" else 2
+    return dict(x=nci * spec["T"] * hw, cache=nci * spec["Tc"] * hw,
+                w=spec["Co"] * (spec["Ci"] // spec["groups"]) * spec["Kt"] * spec["Kh"] * spec["Kw"],
+                wpack=weight_pack_bytes(spec, dtype) // es, bias=spec["Co"],
+                y=spec["N"] * spec["Co"] * To * Ho * Wo, cache_out=nci * L * hw)
 
 
 def _stream(stream):
@@ -314,16 +359,33 @@ def conv3d_causal_cached(ctx, spec: dict, x, cache, w, wpack, bias, y=None, cach
     if cache_out is None:
         cache_out = torch.empty((spec["N"], spec["Ci"], L, spec["H"], spec["W"]),
                                 dtype=w.dtype, device=dev)
-    hw = spec["H"] * spec["W"]
+    n = _sizes(spec, dtype)
     st = lib.c3c_conv3d_causal_cached(
-        ctx._h, C.byref(make_desc(spec, dtype)),
-        _ptr(x, "x", dtype, spec["N"] * spec["Ci"] * spec["T"] * hw),
-        _ptr(cache, "cache", dtype, spec["N"] * spec["Ci"] * spec["Tc"] * hw) if spec["Tc"] else None,
-        _ptr(w, "w", dtype), _ptr(wpack, "wpack", dtype),
-        _ptr(bias, "bias", dtype, spec["Co"]) if spec["has_bias"] else None,
-        _ptr(y, "y", dtype), _ptr(cache_out, "cache_out", dtype), _stream(stream))
+        ctx._h, C.byref(make_desc(spec, dtype)), *_call_ptrs(spec, dtype, n, x, cache, w, wpack,
+                                                            bias, y, cache_out),
+        _stream(stream))
     _raise(st, ctx, "c3c_conv3d_causal_cached")
     return y, cache_out
+
+
+def _call_ptrs(spec, dtype, n, x, cache, w, wpack, bias, y, cache_out):
+    """Checked addresses of (x, cache, w, wpack, bias, y, cache_out).  wpack
+    must hold exactly the packed layout when the call has one (a pack made
+    for another layer would be read out of bounds); it may be None only
+    where the call does not route fast (the library then rejects it)."""
+    if wpack is not None and n["wpack"] == 0:
+        raise ValueError("wpack given, but this call has no fast-route weight layout")
+    for t, name in ((x, "x"), (cache if spec["Tc"] else None, "cache"), (w, "w"),
+                    (wpack, "wpack"), (bias if spec["has_bias"] else None, "bias"), (y, "y"),
+                    (cache_out, "cache_out")):
+        _check(t, name, dtype, n[name])
+    return (_ptr(x, "x", dtype, n["x"]),
+            _ptr(cache, "cache", dtype, n["cache"]) if spec["Tc"] else None,
+            _ptr(w, "w", dtype, n["w"]),
+            _ptr(wpack, "wpack", dtype, n["wpack"]),
+            _ptr(bias, "bias", dtype, n["bias"]) if spec["has_bias"] else None,
+            _ptr(y, "y", dtype, n["y"]),
+            _ptr(cache_out, "cache_out", dtype, n["cache_out"]))
 
 
 def conv3d_causal_cached_fused(ctx, spec: dict, x, cache, w, wpack, bias, scale=None, shift=None,
@@ -341,17 +403,16 @@ def conv3d_causal_cached_fused(ctx, spec: dict, x, cache, w, wpack, bias, scale=
     if cache_out is None:
         cache_out = torch.empty((spec["N"], spec["Ci"], L, spec["H"], spec["W"]),
                                 dtype=w.dtype, device=dev)
-    hw = spec["H"] * spec["W"]
     nc = spec["N"] * spec["Ci"]
+    n = _sizes(spec, dtype)
+    _check(scale, "scale", "f32", nc)
+    _check(shift, "shift", "f32", nc)
+    _check(residual, "residual", dtype, n["y"])
+    px, pc, pw, pp, pb, py, po = _call_ptrs(spec, dtype, n, x, cache, w, wpack, bias, y, cache_out)
     st = lib.c3c_conv3d_causal_cached_fused(
-        ctx._h, C.byref(make_desc(spec, dtype)),
-        _ptr(x, "x", dtype, spec["N"] * spec["Ci"] * spec["T"] * hw),
-        _ptr(cache, "cache", dtype, spec["N"] * spec["Ci"] * spec["Tc"] * hw) if spec["Tc"] else None,
-        _ptr(w, "w", dtype), _ptr(wpack, "wpack", dtype),
-        _ptr(bias, "bias", dtype, spec["Co"]) if spec["has_bias"] else None,
+        ctx._h, C.byref(make_desc(spec, dtype)), px, pc, pw, pp, pb,
         _ptr(scale, "scale", "f32", nc), _ptr(shift, "shift", "f32", nc),
-        _ptr(residual, "residual", dtype, y.numel()),
-        _ptr(y, "y", dtype), _ptr(cache_out, "cache_out", dtype), _stream(stream))
+        _ptr(residual, "residual", dtype, n["y"]), py, po, _stream(stream))
     _raise(st, ctx, "c3c_conv3d_causal_cached_fused")
     return y, cache_out
 

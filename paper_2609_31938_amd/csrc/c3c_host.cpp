@@ -5,6 +5,8 @@
 //
 // Everything before a kernel launch is plain host code: route queries, output
 // sizes, strict-mode rejections and argument errors never touch the device.
+// The split-K plan (workspace size, plan query) reads the current device's
+// compute-unit count, once per device.
 #include <hip/hip_runtime.h>
 
 #include <cstring>
@@ -255,6 +257,47 @@ int c3c_route_query(const c3c_ctx* ctx, const c3c_conv_desc* d, int* route, int*
   return C3C_OK;
 }
 
+int c3c_plan_query(const c3c_ctx* ctx, const c3c_conv_desc* d, size_t ws_bytes, c3c_plan* out) {
+  Geo g;
+  if (*make_geo(d, &g) || !out) return C3C_E_INVAL;
+  std::memset(out, 0, sizeof *out);
+  const int r = decide(g, ctx ? ctx->mode : 0u);
+  out->reason = r;
+  out->route = r == C3C_REASON_NONE ? C3C_ROUTE_FAST : C3C_ROUTE_FALLBACK;
+  // Stand-in tensor addresses: 256-byte aligned and never dereferenced (a
+  // launcher given a LaunchInfo returns before any device call).  Only
+  // their alignment and whether they are NULL steer the choices.
+  void* const p = reinterpret_cast<void*>(uintptr_t(1) << 20);
+  const void* cache = d->Tc > 0 ? p : nullptr;
+  void* cache_out = g.L > 0 ? p : nullptr;
+  void* ws = ws_bytes > 0 ? p : nullptr;
+  LaunchInfo li;
+  hipError_t e;
+  if (g.To == 0)
+    e = hipSuccess;
+  else if (r == C3C_REASON_NONE)
+    e = launch_fast(g, p, cache, p, p, p, cache_out, ws, static_cast<int64_t>(ws_bytes), nullptr,
+                    Fuse{}, &li);
+  else
+    e = launch_fallback(g, p, cache, p, p, p, nullptr, Fuse{}, &li);
+  if (e != hipSuccess && r == C3C_REASON_NONE) {
+    // the fast route refuses this size: the call falls back (fast_error)
+    out->reason = C3C_REASON_FAST_ERROR;
+    out->route = C3C_ROUTE_FALLBACK;
+    li = LaunchInfo{};
+    e = launch_fallback(g, p, cache, p, p, p, nullptr, Fuse{}, &li);
+  }
+  if (e != hipSuccess) return C3C_E_INVAL;
+  out->kernel = li.kernel;
+  out->splits = li.splits;
+  out->tile_co = li.tile_co;
+  out->tile_h = li.tile_h;
+  out->tile_w = li.tile_w;
+  out->workgroups = li.workgroups;
+  out->cache_in_kernel = li.cache_in_kernel ? 1 : 0;
+  return C3C_OK;
+}
+
 int c3c_workspace_bytes(const c3c_conv_desc* d, size_t* bytes) {
   Geo g;
   if (*make_geo(d, &g) || !bytes) return C3C_E_INVAL;
@@ -432,21 +475,26 @@ int run_call(c3c_ctx* ctx, const c3c_conv_desc* d, const void* x, const void* ca
       ++ctx->ctr.strict_rejects;
       return fail(ctx, C3C_E_DEVICE, hipGetErrorString(e));
     }
-    ++ctx->ctr.fast_error;
     fb_reason = C3C_REASON_FAST_ERROR;
   } else if (strict) {
     ++ctx->ctr.strict_rejects;
     return fail(ctx, C3C_E_UNSUPPORTED, "call does not route fast (strict mode)");
-  } else if (reason == C3C_REASON_FORCED) {
-    ++ctx->ctr.forced;
-  } else {
-    ++ctx->ctr.unsupported;
   }
-  ++ctx->ctr.fallback;
-  record_shape(ctx, fb_reason, *d);
   hipError_t e = launch_fallback(g, x, cache, w, bias, y, s, fu);
   if (e == hipSuccess) e = launch_cache_copy(g, x, cache, cache_out, s, fu);
-  if (e != hipSuccess) return fail(ctx, C3C_E_DEVICE, hipGetErrorString(e));
+  if (e != hipSuccess) {
+    // nothing was computed: the call counts as failed, not as a fallback
+    ++ctx->ctr.failed;
+    return fail(ctx, C3C_E_DEVICE, hipGetErrorString(e));
+  }
+  ++ctx->ctr.fallback;
+  if (fb_reason == C3C_REASON_FAST_ERROR)
+    ++ctx->ctr.fast_error;
+  else if (fb_reason == C3C_REASON_FORCED)
+    ++ctx->ctr.forced;
+  else
+    ++ctx->ctr.unsupported;
+  record_shape(ctx, fb_reason, *d);
   return C3C_OK;
 }
 

@@ -52,6 +52,20 @@ struct Fuse {
   bool any() const { return scale != nullptr || residual != nullptr; }
 };
 
+// What a call would launch, for the plan query (c3c_plan_query): every
+// launcher takes an optional LaunchInfo*; when it is given, the launcher
+// makes the same choices it makes for a launch, fills it in and returns
+// hipSuccess without touching the device.
+struct LaunchInfo {
+  int kernel = 0;           // enum c3c_kernel
+  int64_t tile_co = 0;      // output channels per workgroup
+  int64_t tile_h = 0;       // output rows per workgroup (0: a flattened-plane tile)
+  int64_t tile_w = 0;       // output columns (or flattened pixels) per workgroup
+  int64_t workgroups = 0;   // of the main launch (every split included)
+  int splits = 1;
+  bool cache_in_kernel = false;
+};
+
 hipError_t launch_repack(const Geo& g, const void* w, void* wpack, hipStream_t s);
 // measurement support (mfma_probe.hip): back-to-back bf16 matrix-core products
 hipError_t launch_mfma_probe(int64_t blocks, int64_t iters, float* out, hipStream_t s);
@@ -60,7 +74,7 @@ hipError_t launch_unpack(const Geo& g, const void* wpack, void* w, hipStream_t s
 // ws / ws_bytes: the caller's split-K workspace (may be NULL / 0).
 hipError_t launch_fast(const Geo& g, const void* x, const void* cache, const void* wpack,
                        const void* bias, void* y, void* cache_out, void* ws, int64_t ws_bytes,
-                       hipStream_t s, const Fuse& fu = Fuse{});
+                       hipStream_t s, const Fuse& fu = Fuse{}, LaunchInfo* info = nullptr);
 // bf16 fast kernel (conv_bf16.hip); writes cache_out itself when it can
 // (returns *cache_written = true), else the caller copies the cache.  Splits
 // the stages of a call too small to fill the device over several workgroups
@@ -68,14 +82,15 @@ hipError_t launch_fast(const Geo& g, const void* x, const void* cache, const voi
 hipError_t launch_fast_bf16(const Geo& g, const void* x, const void* cache, const void* wpack,
                             const void* bias, void* y, void* cache_out, void* ws,
                             int64_t ws_bytes, bool* cache_written, hipStream_t s,
-                            const Fuse& fu = Fuse{});
+                            const Fuse& fu = Fuse{}, LaunchInfo* info = nullptr);
 // fp32 partial-sum bytes a bf16 fast call would split into (0: it runs unsplit)
 int64_t fast_bf16_workspace_bytes(const Geo& g);
 // fallback, pointwise case (pointwise.hip): 1x1x1, unit spatial stride, no
 // spatial padding, one group, bf16 / fp16, aligned buffers
 bool pointwise_eligible(const Geo& g, const void* x, const void* cache, const void* w, const void* y);
 hipError_t launch_pointwise(const Geo& g, const void* x, const void* cache, const void* w,
-                            const void* bias, void* y, hipStream_t s, const Fuse& fu = Fuse{});
+                            const void* bias, void* y, hipStream_t s, const Fuse& fu = Fuse{},
+                            LaunchInfo* info = nullptr);
 // compute units of the current device (256 when no device is visible)
 int64_t device_compute_units();
 // output channels per workgroup of the two bf16 1x1 kernels of the fast route
@@ -87,22 +102,24 @@ constexpr int64_t kPointwiseTileCo = 160;  // pointwise.hip
 bool tap1x1_eligible(const Geo& g, const void* x, const void* cache, const void* y);
 int64_t tap1x1_blocks(const Geo& g);
 hipError_t launch_tap1x1(const Geo& g, const void* x, const void* cache, const void* wpack,
-                         const void* bias, void* y, hipStream_t s);
+                         const void* bias, void* y, hipStream_t s, LaunchInfo* info = nullptr);
 // fast route, bf16, 3x3 spatial kernel with Co <= 5 (conv_head.hip): the 9
 // spatial taps x Co output channels as the matrix cores' N dimension, then a
 // 3x3 gather-sum; needs W a multiple of 8 and aligned pointers.  The caller
 // copies the cache.
 bool head_eligible(const Geo& g, const void* x, const void* cache, const void* y);
 hipError_t launch_head(const Geo& g, const void* x, const void* cache, const void* wpack,
-                       const void* bias, void* y, hipStream_t s);
+                       const void* bias, void* y, hipStream_t s, LaunchInfo* info = nullptr);
 // fast route, bf16, 1x1 spatial kernel (pointwise.hip): every active temporal
 // tap of a call as per-frame matrix products, reading the packed weights; any
 // temporal stride and dilation, any H * W and alignment.  The caller copies
 // the cache.
 hipError_t launch_fast_tap1x1(const Geo& g, const void* x, const void* cache, const void* wpack,
-                              const void* bias, void* y, hipStream_t s, const Fuse& fu = Fuse{});
+                              const void* bias, void* y, hipStream_t s, const Fuse& fu = Fuse{},
+                              LaunchInfo* info = nullptr);
 hipError_t launch_fallback(const Geo& g, const void* x, const void* cache, const void* w,
-                           const void* bias, void* y, hipStream_t s, const Fuse& fu = Fuse{});
+                           const void* bias, void* y, hipStream_t s, const Fuse& fu = Fuse{},
+                           LaunchInfo* info = nullptr);
 // the fused form's prologue as its own pass: u = RNE_bf16(SiLU(x * scale +
 // shift)) over the whole new chunk (fallback.hip)
 hipError_t launch_prologue(const Geo& g, const void* x, const float* scale, const float* shift,

@@ -687,11 +687,22 @@ void set_tiles(const Geo& g, int64_t bco, int64_t bh, int64_t bw, Plan* p) {
 }
 
 template <int WCO, int WR, int WCF, int WAVES_CO, int WAVES_PX, int NBUF>
-hipError_t run(const Geo& g, Args a, const Plan& p, bool aligned, int fused, hipStream_t s) {
+hipError_t run(const Geo& g, Args a, const Plan& p, bool aligned, int fused, hipStream_t s,
+               LaunchInfo* info) {
   a.tiles_co = static_cast<int>(p.tiles_co);
   a.tiles_w = static_cast<int>(p.tiles_w);
   a.tiles_h = static_cast<int>(p.tiles_h);
   const int64_t blocks = p.blocks * a.splits;
+  if (info) {
+    info->kernel = C3C_KERNEL_CONV3D_BF16;
+    info->tile_co = 16 * WCO * WAVES_CO;
+    info->tile_h = WR * WAVES_PX;
+    info->tile_w = 16 * WCF;
+    info->workgroups = blocks;
+    info->splits = a.splits;
+    info->cache_in_kernel = a.write_cache != 0;
+    return hipSuccess;
+  }
   if (blocks == 0) return hipSuccess;
   if (blocks > 0x7fffffff) return hipErrorInvalidConfiguration;
   a.nblocks = static_cast<int>(blocks);
@@ -834,7 +845,8 @@ int64_t fast_bf16_workspace_bytes(const Geo& g) { return plan_bf16(g).part_bytes
 
 hipError_t launch_fast_bf16(const Geo& g, const void* x, const void* cache, const void* wpack,
                             const void* bias, void* y, void* cache_out, void* ws,
-                            int64_t ws_bytes, bool* cache_written, hipStream_t s, const Fuse& fu) {
+                            int64_t ws_bytes, bool* cache_written, hipStream_t s, const Fuse& fu,
+                            LaunchInfo* info) {
   const PackDims p = pack_dims(g.d);
   Args a;
   a.x = static_cast<const uint16_t*>(x);
@@ -885,13 +897,13 @@ hipError_t launch_fast_bf16(const Geo& g, const void* x, const void* cache, cons
   a.splits = split ? pl.splits : 1;
   a.part = split ? static_cast<float*>(ws) : nullptr;
   switch (pl.cfg) {
-    case CFG_C192: return run<6, 2, 4, 2, 2, 3>(g, a, pl, aligned, fused, s);
-    case CFG_C96: return run<3, 3, 4, 2, 2, 3>(g, a, pl, aligned, fused, s);
-    case CFG_C16: return run<1, 2, 4, 1, 4, 2>(g, a, pl, aligned, fused, s);
+    case CFG_C192: return run<6, 2, 4, 2, 2, 3>(g, a, pl, aligned, fused, s, info);
+    case CFG_C96: return run<3, 3, 4, 2, 2, 3>(g, a, pl, aligned, fused, s, info);
+    case CFG_C16: return run<1, 2, 4, 1, 4, 2>(g, a, pl, aligned, fused, s, info);
     // two LDS buffers measured 1.4-3.4% faster than three on the 720p
     // layers for this tile (the 192- and 96-channel tiles keep three)
-    case CFG_C160_4X80: return run<5, 2, 5, 2, 2, 2>(g, a, pl, aligned, fused, s);
-    default: return run<5, 5, 2, 2, 2, 3>(g, a, pl, aligned, fused, s);
+    case CFG_C160_4X80: return run<5, 2, 5, 2, 2, 2>(g, a, pl, aligned, fused, s, info);
+    default: return run<5, 5, 2, 2, 2, 3>(g, a, pl, aligned, fused, s, info);
   }
 }
 

@@ -315,7 +315,7 @@ bool head_eligible(const Geo& g, const void* x, const void* cache, const void* y
 }
 
 hipError_t launch_head(const Geo& g, const void* x, const void* cache, const void* wpack,
-                       const void* bias, void* y, hipStream_t s) {
+                       const void* bias, void* y, hipStream_t s, LaunchInfo* info) {
   const c3c_conv_desc& d = g.d;
   if (!head_eligible(g, x, cache, y)) return hipErrorInvalidValue;
   const PackDims p = pack_dims(d);
@@ -345,6 +345,14 @@ hipError_t launch_head(const Geo& g, const void* x, const void* cache, const voi
   a.wpack_bytes = static_cast<uint32_t>(p.elems() * 2);
   a.has_bias = d.has_bias ? 1 : 0;
   const int64_t blocks = static_cast<int64_t>(a.tiles_w) * a.tiles_h * g.To * d.N;
+  if (info) {
+    info->kernel = C3C_KERNEL_HEAD;
+    info->tile_co = d.Co;
+    info->tile_h = OR;
+    info->tile_w = OC;
+    info->workgroups = blocks;
+    return hipSuccess;
+  }
   if (blocks == 0) return hipSuccess;
   if (blocks > 0x7fffffff) return hipErrorInvalidConfiguration;
   a.nblocks = static_cast<int>(blocks);

@@ -277,7 +277,7 @@ int64_t tap1x1_blocks(const Geo& g) {
 }
 
 hipError_t launch_tap1x1(const Geo& g, const void* x, const void* cache, const void* wpack,
-                         const void* bias, void* y, hipStream_t s) {
+                         const void* bias, void* y, hipStream_t s, LaunchInfo* info) {
   const c3c_conv_desc& d = g.d;
   const PackDims p = pack_dims(d);
   if (!tap1x1_eligible(g, x, cache, y)) return hipErrorInvalidValue;
@@ -306,6 +306,14 @@ hipError_t launch_tap1x1(const Geo& g, const void* x, const void* cache, const v
   a.wpack_bytes = static_cast<uint32_t>(p.elems() * 2);
   a.has_bias = d.has_bias ? 1 : 0;
   const int64_t blocks = tap1x1_blocks(g);
+  if (info) {
+    info->kernel = C3C_KERNEL_TAP1X1;
+    info->tile_co = TCO;
+    info->tile_h = 0;
+    info->tile_w = TPX;
+    info->workgroups = blocks;
+    return hipSuccess;
+  }
   if (blocks == 0) return hipSuccess;
   if (blocks > 0x7fffffff) return hipErrorInvalidConfiguration;
   a.nblocks = static_cast<int>(blocks);

@@ -209,7 +209,7 @@ __global__ __launch_bounds__(FB_THREADS) void fallback_conv3d(FbArgs a, const T*
 
 template <typename T>
 hipError_t launch_fb(const Geo& g, const void* x, const void* cache, const void* w,
-                     const void* bias, void* y, hipStream_t s, const Fuse& fu) {
+                     const void* bias, void* y, hipStream_t s, const Fuse& fu, LaunchInfo* info) {
   const c3c_conv_desc& d = g.d;
   FbArgs a;
   a.N = d.N; a.Ci = d.Ci; a.Co = d.Co; a.T = d.T; a.Tc = d.Tc; a.H = d.H; a.W = d.W;
@@ -227,6 +227,14 @@ hipError_t launch_fb(const Geo& g, const void* x, const void* cache, const void*
   const int64_t gx = (g.Ho * g.Wo + FB_THREADS * FB_PPT - 1) / (FB_THREADS * FB_PPT);
   const int64_t gy = d.groups * ((cog + FB_COB - 1) / FB_COB);
   const int64_t gz = d.N * g.To;
+  if (info) {
+    info->kernel = C3C_KERNEL_FALLBACK_DIRECT;
+    info->tile_co = FB_COB;
+    info->tile_h = 0;
+    info->tile_w = FB_THREADS * FB_PPT;
+    info->workgroups = gx * gy * gz;
+    return hipSuccess;
+  }
   if (gx == 0 || gz == 0) return hipSuccess;
   if (gx > 0x7fffffff || gy > 65535 || gz > 65535) return hipErrorInvalidConfiguration;
   hipLaunchKernelGGL((fallback_conv3d<T>), dim3(gx, gy, gz), dim3(FB_THREADS), 0, s, a,
@@ -330,14 +338,15 @@ bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) %
 }  // namespace
 
 hipError_t launch_fallback(const Geo& g, const void* x, const void* cache, const void* w,
-                           const void* bias, void* y, hipStream_t s, const Fuse& fu) {
+                           const void* bias, void* y, hipStream_t s, const Fuse& fu,
+                           LaunchInfo* info) {
   if (g.To == 0) return hipSuccess;
   // the pointwise kernel's aligned epilogue also reads the residual 8 bytes at a time
   if (pointwise_eligible(g, x, cache, w, y) &&
       (fu.residual == nullptr || (reinterpret_cast<uintptr_t>(fu.residual) & 7) == 0))
-    return launch_pointwise(g, x, cache, w, bias, y, s, fu);
-  if (g.d.dtype == C3C_DTYPE_F32) return launch_fb<float>(g, x, cache, w, bias, y, s, fu);
-  return launch_fb<uint16_t>(g, x, cache, w, bias, y, s, fu);
+    return launch_pointwise(g, x, cache, w, bias, y, s, fu, info);
+  if (g.d.dtype == C3C_DTYPE_F32) return launch_fb<float>(g, x, cache, w, bias, y, s, fu, info);
+  return launch_fb<uint16_t>(g, x, cache, w, bias, y, s, fu, info);
 }
 
 hipError_t launch_prologue(const Geo& g, const void* x, const float* scale, const float* shift,

@@ -255,12 +255,20 @@ __global__ __launch_bounds__(64 * WAVES_CO * WAVES_PX) void fast_conv3d(FastArgs
 }
 
 template <typename T, int CO_FRAGS, int PX_FRAGS, int WAVES_CO, int WAVES_PX, int BH, int BWF, int KS>
-hipError_t run_fast(const Geo& g, FastArgs a, hipStream_t s) {
+hipError_t run_fast(const Geo& g, FastArgs a, hipStream_t s, LaunchInfo* info) {
   constexpr int BCO = 32 * CO_FRAGS * WAVES_CO, BW = 32 * BWF;
   a.tiles_co = static_cast<int>((g.d.Co + BCO - 1) / BCO);
   a.tiles_w = static_cast<int>((g.Wo + BW - 1) / BW);
   a.tiles_h = static_cast<int>((g.Ho + BH - 1) / BH);
   const int64_t blocks = static_cast<int64_t>(a.tiles_co) * a.tiles_w * a.tiles_h * g.To * g.d.N;
+  if (info) {
+    info->kernel = C3C_KERNEL_FAST_F32;
+    info->tile_co = BCO;
+    info->tile_h = BH;
+    info->tile_w = BW;
+    info->workgroups = blocks;
+    return hipSuccess;
+  }
   if (blocks == 0) return hipSuccess;
   if (blocks > 0x7fffffff) return hipErrorInvalidConfiguration;
   hipLaunchKernelGGL((fast_conv3d<T, CO_FRAGS, PX_FRAGS, WAVES_CO, WAVES_PX, BH, BWF, KS>),
@@ -304,7 +312,7 @@ hipError_t launch_unpack(const Geo& g, const void* wpack, void* w, hipStream_t s
 
 hipError_t launch_fast(const Geo& g, const void* x, const void* cache, const void* wpack,
                        const void* bias, void* y, void* cache_out, void* ws, int64_t ws_bytes,
-                       hipStream_t s, const Fuse& fu) {
+                       hipStream_t s, const Fuse& fu, LaunchInfo* info) {
   const PackDims p = pack_dims(g.d);
   FastArgs a;
   a.x = x; a.cache = cache; a.wpack = wpack; a.bias = bias; a.y = y;
@@ -328,21 +336,23 @@ hipError_t launch_fast(const Geo& g, const void* x, const void* cache, const voi
       const int64_t pad_pw = (g.d.Co + kPointwiseTileCo - 1) / kPointwiseTileCo * kPointwiseTileCo;
       if (!fu.any() && 10 * pad_tap <= 11 * pad_pw && tap1x1_eligible(g, x, cache, y) &&
           2 * tap1x1_blocks(g) >= device_compute_units())
-        e = launch_tap1x1(g, x, cache, wpack, bias, y, s);
+        e = launch_tap1x1(g, x, cache, wpack, bias, y, s, info);
       else
-        e = launch_fast_tap1x1(g, x, cache, wpack, bias, y, s, fu);
+        e = launch_fast_tap1x1(g, x, cache, wpack, bias, y, s, fu, info);
     } else if (!fu.any() && head_eligible(g, x, cache, y)) {
       // few output channels (a decoder's RGB head): the spatial taps as N
-      e = launch_head(g, x, cache, wpack, bias, y, s);
+      e = launch_head(g, x, cache, wpack, bias, y, s, info);
     } else {
       bool written = false;
-      e = launch_fast_bf16(g, x, cache, wpack, bias, y, cache_out, ws, ws_bytes, &written, s, fu);
-      if (e != hipSuccess || written) return e;
+      e = launch_fast_bf16(g, x, cache, wpack, bias, y, cache_out, ws, ws_bytes, &written, s, fu,
+                           info);
+      if (e != hipSuccess || written || info) return e;
     }
   } else {
-    e = one ? run_fast<float, 1, 2, 1, 4, 4, 2, 1>(g, a, s) : run_fast<float, 1, 2, 1, 4, 4, 2, 3>(g, a, s);
+    e = one ? run_fast<float, 1, 2, 1, 4, 4, 2, 1>(g, a, s, info)
+            : run_fast<float, 1, 2, 1, 4, 4, 2, 3>(g, a, s, info);
   }
-  if (e != hipSuccess) return e;
+  if (e != hipSuccess || info) return e;
   return launch_cache_copy(g, x, cache, cache_out, s, fu);
 }
 

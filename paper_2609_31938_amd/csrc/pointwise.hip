@@ -427,7 +427,8 @@ namespace {
 // count of any output frame least (4, 3 or 2), the template instance by
 // element type, weight layout and alignment
 template <bool PACKED>
-hipError_t launch_pw(const Geo& g, PwArgs a, bool f16, bool al, hipStream_t s, int fused) {
+hipError_t launch_pw(const Geo& g, PwArgs a, bool f16, bool al, hipStream_t s, int fused,
+                     LaunchInfo* info) {
   const c3c_conv_desc& d = g.d;
   a.co_tiles = static_cast<int>((d.Co + PW_CO - 1) / PW_CO);
   // Fast route, aligned: 512-pixel workgroups (twice the products per
@@ -441,6 +442,14 @@ hipError_t launch_pw(const Geo& g, PwArgs a, bool f16, bool al, hipStream_t s, i
   const int px = wide ? pw_px(8) : pw_px(4);
   a.px_tiles = static_cast<int>((a.hw + px - 1) / px);
   const int64_t blocks = static_cast<int64_t>(a.px_tiles) * a.co_tiles * g.To * d.N;
+  if (info) {
+    info->kernel = C3C_KERNEL_POINTWISE;
+    info->tile_co = PW_CO;
+    info->tile_h = 0;
+    info->tile_w = px;
+    info->workgroups = blocks;
+    return hipSuccess;
+  }
   if (blocks == 0) return hipSuccess;
   if (blocks > 0x7fffffff) return hipErrorInvalidConfiguration;
   int ntap = 0;
@@ -517,7 +526,8 @@ PwArgs common_args(const Geo& g, const void* x, const void* cache, const void* b
 }  // namespace
 
 hipError_t launch_pointwise(const Geo& g, const void* x, const void* cache, const void* w,
-                            const void* bias, void* y, hipStream_t s, const Fuse& fu) {
+                            const void* bias, void* y, hipStream_t s, const Fuse& fu,
+                            LaunchInfo* info) {
   PwArgs a = common_args(g, x, cache, bias, y);
   a.w = static_cast<const uint16_t*>(w);
   a.w_bytes = static_cast<uint32_t>(g.d.Co * g.d.Ci * 2);
@@ -526,11 +536,13 @@ hipError_t launch_pointwise(const Geo& g, const void* x, const void* cache, cons
   a.shift = fu.shift;
   a.residual = fu.residual;
   // launch_fallback checked the residual's 8-byte alignment
-  return launch_pw<false>(g, a, g.d.dtype == C3C_DTYPE_F16, true, s, fu.pro() ? 2 : fu.residual ? 1 : 0);
+  return launch_pw<false>(g, a, g.d.dtype == C3C_DTYPE_F16, true, s, fu.pro() ? 2 : fu.residual ? 1 : 0,
+                          info);
 }
 
 hipError_t launch_fast_tap1x1(const Geo& g, const void* x, const void* cache, const void* wpack,
-                              const void* bias, void* y, hipStream_t s, const Fuse& fu) {
+                              const void* bias, void* y, hipStream_t s, const Fuse& fu,
+                              LaunchInfo* info) {
   const c3c_conv_desc& d = g.d;
   const PackDims p = pack_dims(d);
   // 32-bit buffer offsets: one 32-channel chunk of a source frame and the
@@ -547,7 +559,7 @@ hipError_t launch_fast_tap1x1(const Geo& g, const void* x, const void* cache, co
   a.residual = fu.residual;
   const bool al = (d.H * d.W) % 8 == 0 && aligned(x, 16) && (cache == nullptr || aligned(cache, 16)) &&
                   aligned(y, 8) && (fu.residual == nullptr || aligned(fu.residual, 8));
-  return launch_pw<true>(g, a, false, al, s, fu.pro() ? 2 : fu.residual ? 1 : 0);
+  return launch_pw<true>(g, a, false, al, s, fu.pro() ? 2 : fu.residual ? 1 : 0, info);
 }
 
 }  // namespace c3c

@@ -56,25 +56,84 @@ def chunk(sp, dtype, wid=900, lid=0, ci=0, device="cuda"):
     return inputs.chunk_input(sp, dtype, wid, lid, ci, device)
 
 
-def sample_indices(shape, n_random=2048, seed=0):
-    """Flat NCTHW indices: random ones plus every tile-border row/column of a
-    few (n, co, t) planes (first/last rows and columns, multiples of 32
-    around them)."""
+def tile_borders(extent, tile):
+    """Indices on both sides of every tile boundary along one axis, plus the
+    first and last index."""
+    out = {0, extent - 1}
+    if tile > 0:
+        for b in range(tile, extent, tile):
+            out.update((b - 1, b))
+    return sorted(i for i in out if 0 <= i < extent)
+
+
+def sample_indices(shape, plan=None, n_random=2048, seed=0, n_planes=6, per_border=3):
+    """Flat NCTHW indices: random ones, plus points on the tile borders of the
+    workgroup grid the call actually used (``plan`` from c3c.plan_query) in
+    several (n, co, t) planes -- every border row with a few random columns,
+    every border column with a few random rows (for a kernel that tiles the
+    flattened plane, every tile boundary of that plane) -- and the first and
+    last channel of every output-channel tile."""
     N, Co, To, Ho, Wo = shape
     rng = np.random.default_rng(seed)
     total = N * Co * To * Ho * Wo
+    if total == 0:
+        return np.zeros(0, np.int64)
     idx = [rng.integers(0, total, n_random)]
-    hs = sorted({0, 1, Ho - 2, Ho - 1} & set(range(Ho)))
-    ws = sorted(({0, 1, 31, 32, 33, 63, 64, 65, Wo - 33, Wo - 32, Wo - 2, Wo - 1}) & set(range(Wo)))
-    for n in {0, N - 1}:
-        for co in {0, Co - 1, Co // 2, min(31, Co - 1), min(32, Co - 1)}:
-            for t in {0, To - 1}:
-                base = ((n * Co + co) * To + t) * Ho * Wo
-                for h in hs:
-                    for w_ in ws:
-                        idx.append(np.array([base + h * Wo + w_]))
-    out = np.unique(np.concatenate(idx))
+    th = plan["tile_h"] if plan else 0
+    tw = plan["tile_w"] if plan else 32
+    tco = plan["tile_co"] if plan else 32
+    cos = set(tile_borders(Co, tco))
+    planes = {(0, 0, 0), (N - 1, Co - 1, To - 1)}
+    for _ in range(n_planes):
+        planes.add((int(rng.integers(N)), int(rng.choice(sorted(cos))), int(rng.integers(To))))
+    for n, co, t in planes:
+        base = ((n * Co + co) * To + t) * Ho * Wo
+        if th > 0:
+            for h in tile_borders(Ho, th):
+                idx.append(base + h * Wo + rng.integers(0, Wo, per_border))
+                idx.append(base + h * Wo + np.array([0, Wo - 1]))
+            for w_ in tile_borders(Wo, tw):
+                idx.append(base + rng.integers(0, Ho, per_border) * Wo + w_)
+                idx.append(base + np.array([0, Ho - 1]) * Wo + w_)
+        else:
+            idx.append(base + np.array(tile_borders(Ho * Wo, tw)))
+    # every output-channel tile's edge channels, at random positions
+    for co in cos:
+        n, t = int(rng.integers(N)), int(rng.integers(To))
+        base = ((n * Co + co) * To + t) * Ho * Wo
+        idx.append(base + rng.integers(0, Ho * Wo, per_border))
+    out = np.unique(np.concatenate([np.asarray(i, np.int64).ravel() for i in idx]))
     return out[(out >= 0) & (out < total)]
+
+
+def check_planes(y, sp, dtype, planes, oracle_in, what=""):
+    """Whole output planes (n, co, t) compared with the oracle, fp64."""
+    N, Co, To, Ho, Wo = y.shape
+    hx, hc, hw_, hb = oracle_in
+    worst = 0.0
+    for n, co, t in planes:
+        r0 = ((n * Co + co) * To + t) * Ho
+        ref = oracle.conv3d_rows(sp, dtype, hx, hc, hw_, hb, r0, r0 + Ho)
+        m = check(as_f64(y[n, co, t]), ref, dtype, f"{what} plane n={n} co={co} t={t}")
+        worst = max(worst, m["rel"])
+    return worst
+
+
+GUARD = 4096  # elements of poison on each side of an output
+
+
+def guarded(shape, dtype, device="cuda"):
+    """(tensor, backing buffer): a NaN-filled output inside a larger NaN-filled
+    buffer, GUARD elements of poison on each side (16-byte aligned)."""
+    td = {"bf16": torch.bfloat16, "f32": torch.float32, "f16": torch.float16}[dtype]
+    n = int(np.prod(shape))
+    buf = torch.full((n + 2 * GUARD,), float("nan"), dtype=td, device=device)
+    return buf[GUARD:GUARD + n].view(shape), buf
+
+
+def guards_intact(buf):
+    """True when the poison on both sides of a guarded output is untouched."""
+    return bool(torch.isnan(buf[:GUARD]).all().item()) and bool(torch.isnan(buf[-GUARD:]).all().item())
 
 
 def run(ctx, sp, x, cache, w, wpack, b):

@@ -13,15 +13,17 @@ import oracle
 from paper_2609_31938_amd import c3c, inputs
 from paper_2609_31938_amd.inputs import spec
 
-from gpu_util import (TOL, as_f64, check, chunk, host, layer, metrics, oracle_args, run,
-                      sample_indices, say)
+from gpu_util import (TOL, as_f64, check, chunk, guarded, guards_intact, host, layer, metrics,
+                      oracle_args, run, say)
 
 pytestmark = pytest.mark.gpu
 
 
-def _case(sp, dtype, mode=0, seed=0, poison=True):
-    """One call on fresh inputs, compared in full with the oracle."""
-    say(f"case {dtype} {sp} mode={mode}")
+def _case(sp, dtype, mode=0, seed=0, ws=False, kernel=None):
+    """One call on fresh inputs, compared in full with the oracle.  The
+    outputs are NaN-filled and sit inside NaN guard bands that must stay
+    untouched.  ws: attach a split-K workspace of the size the call asks
+    for.  kernel: the kernel the plan must name."""
     ctx = c3c.Context(mode)
     w, b = layer(sp, dtype, 901, seed)
     x = chunk(sp, dtype, 901, seed, 0)
@@ -29,14 +31,21 @@ def _case(sp, dtype, mode=0, seed=0, poison=True):
     wpack = None
     if c3c.route_query(None, sp, dtype)[0] == "fast":
         wpack = c3c.weight_repack(ctx, sp, w)
+    need = c3c.workspace_bytes(sp, dtype) if ws else 0
+    wsb = None
+    if need:
+        wsb = torch.empty(need // 4, dtype=torch.float32, device="cuda")
+        ctx.set_workspace(wsb)
+    plan = c3c.plan_query(ctx, sp, dtype, need)
+    say(f"case {dtype} {sp} mode={mode} plan={plan}")
+    if kernel is not None:
+        assert plan["kernel"] == kernel, plan
     To, Ho, Wo, L = c3c.output_dims(sp, dtype)
-    y = torch.empty((sp["N"], sp["Co"], To, Ho, Wo), dtype=w.dtype, device="cuda")
-    co = torch.empty((sp["N"], sp["Ci"], L, sp["H"], sp["W"]), dtype=w.dtype, device="cuda")
-    if poison:
-        y.fill_(float("nan"))
-        co.fill_(float("nan"))
+    y, ybuf = guarded((sp["N"], sp["Co"], To, Ho, Wo), dtype)
+    co, cbuf = guarded((sp["N"], sp["Ci"], L, sp["H"], sp["W"]), dtype)
     y, co = c3c.conv3d_causal_cached(ctx, sp, x, cache, w, wpack, b, y, co)
     torch.cuda.synchronize()
+    assert guards_intact(ybuf) and guards_intact(cbuf), "a write outside the outputs"
     args = oracle_args(sp, x, cache, w, b)
     ref = oracle.conv3d(sp, dtype, *args)
     assert tuple(y.shape) == ref.shape
@@ -80,6 +89,13 @@ FAST_CASES = [
     ("bf16", dict(N=1, Ci=16, Co=32, T=1, Tc=0, H=5, W=5)),
     ("bf16", dict(N=1, Ci=24, Co=40, T=2, Tc=3, H=11, W=65)),          # p_l < 0
     ("bf16", dict(N=1, Ci=64, Co=192, T=4, Tc=2, H=16, W=64)),
+    # the 160-channel tiles (97..191 output channels): 4x80 ragged in both
+    # directions and in the channel tile, two channel tiles, and 10x32
+    ("bf16", dict(N=1, Ci=64, Co=160, T=3, Tc=2, H=22, W=170)),
+    ("bf16", dict(N=1, Ci=72, Co=130, T=2, Tc=2, H=13, W=96)),
+    ("bf16", dict(N=2, Ci=40, Co=181, T=2, Tc=1, H=9, W=83)),
+    ("bf16", dict(N=1, Ci=48, Co=320, T=2, Tc=2, H=10, W=88)),
+    ("bf16", dict(N=1, Ci=40, Co=150, T=4, Tc=2, H=333, W=30)),
     ("bf16", dict(N=1, Ci=8, Co=8, T=5, Tc=4, H=6, W=40, d_t=2, p_base=4)),  # temporal dilation
     ("bf16", dict(N=1, Ci=20, Co=36, T=2, Tc=2, H=7, W=9, Kt=5, p_base=4)),  # Kt = 5
     ("bf16", dict(N=1, Ci=12, Co=20, T=3, Tc=2, H=6, W=35, p_r=1)),          # right pad

@@ -34,7 +34,7 @@ def test_every_declared_symbol_is_exported():
         "c3c_conv3d_causal_cached", "c3c_counters_get", "c3c_counters_reset",
         "c3c_fallback_shapes", "c3c_strerror", "c3c_last_error",
         "c3c_workspace_bytes", "c3c_ctx_set_workspace", "c3c_conv3d_causal_cached_fused",
-        "c3c_mfma_probe", "c3c_fused_workspace_bytes"])
+        "c3c_mfma_probe", "c3c_fused_workspace_bytes", "c3c_plan_query"])
     for n in names:
         assert hasattr(c3c.lib, n), n
 
@@ -42,7 +42,8 @@ def test_every_declared_symbol_is_exported():
 def test_descriptor_layout_matches_header():
     # 21 int64 fields + 2 int32 = 176 bytes, no padding surprises
     assert C.sizeof(c3c.Desc) == 21 * 8 + 2 * 4
-    assert C.sizeof(c3c.Counters) == 8 * 8
+    assert C.sizeof(c3c.Counters) == 9 * 8
+    assert C.sizeof(c3c.Plan) == 4 * 4 + 4 * 8 + 2 * 4
 
 
 @pytest.mark.parametrize("case", range(300))
@@ -162,7 +163,7 @@ def test_argument_errors_are_not_counted():
     bad = dict(sp, Ci=0)
     assert _call(ctx, bad) == c3c.E_INVAL
     assert ctx.counters() == dict(calls=0, fast=0, fallback=0, unsupported=0, forced=0,
-                                  fast_error=0, strict_rejects=0, repacks=0)
+                                  fast_error=0, strict_rejects=0, repacks=0, failed=0)
 
 
 @no_gpu
@@ -303,3 +304,140 @@ def test_fused_workspace_bytes():
     assert c3c.fused_workspace_bytes(spec(N=1, Ci=8, Co=8, T=2, Tc=2, H=8, W=8, s_t=2), "bf16") == 0
     n = C.c_size_t()
     assert c3c.lib.c3c_fused_workspace_bytes(C.byref(c3c.make_desc(sp, "bf16")), None) == c3c.E_INVAL
+
+
+# ---------------------------------------------------------------------------
+# a call whose kernels cannot be launched (no device here): counted as
+# failed, never as a completed fallback
+# ---------------------------------------------------------------------------
+
+@no_gpu
+def test_failed_launch_is_not_counted_as_a_fallback():
+    ctx = c3c.Context()
+    sp = spec(N=1, Ci=4, Co=4, T=2, Tc=2, H=8, W=8)
+    # a fallback call (f16 has no fast kernel), then a fast call whose fast
+    # launch and then fallback launch both fail
+    assert _call(ctx, sp, dtype="f16") == c3c.E_DEVICE
+    assert _call(ctx, sp) == c3c.E_DEVICE
+    ctx.mode = c3c.MODE_FORCE_FALLBACK
+    assert _call(ctx, sp) == c3c.E_DEVICE
+    c = ctx.counters()
+    assert (c["calls"], c["failed"]) == (3, 3)
+    assert c["fast"] == c["fallback"] == c["unsupported"] == c["forced"] == c["fast_error"] == 0
+    assert c["calls"] == c["fast"] + c["fallback"] + c["strict_rejects"] + c["failed"]
+    assert ctx.fallback_shapes() == []
+    # strict mode: the failed fast launch is a strict reject, not a failure
+    ctx.mode = c3c.MODE_STRICT
+    assert _call(ctx, sp) == c3c.E_DEVICE
+    c = ctx.counters()
+    assert (c["calls"], c["strict_rejects"], c["failed"]) == (4, 1, 3)
+
+
+# ---------------------------------------------------------------------------
+# the launch plan (c3c_plan_query)
+# ---------------------------------------------------------------------------
+
+@no_gpu
+def test_plan_of_the_workloads():
+    """The kernel and tile each benchmarked layer takes (256 compute units,
+    what the library assumes without a device)."""
+    from paper_2609_31938_amd.inputs import WORKLOADS
+    want = {
+        "c32_32x32": ("fast_f32", 32, 4, 64, 1),
+        "c384_60x104": ("conv3d_bf16", 192, 4, 64, 1),
+        "c192_240x416": ("conv3d_bf16", 192, 4, 64, 1),
+        "c384to192_240x416": ("conv3d_bf16", 192, 4, 64, 1),
+        "c96_480x832": ("conv3d_bf16", 96, 6, 64, 1),
+        "c640_44x80": ("conv3d_bf16", 160, 4, 80, 1),
+        "c320_176x320": ("conv3d_bf16", 160, 4, 80, 1),
+        "c320to160_352x640": ("conv3d_bf16", 160, 4, 80, 1),
+        "c160_704x1280": ("conv3d_bf16", 160, 4, 80, 1),
+        "shortcut_1x1x1_320to160_352x640": ("pointwise", 160, 0, 256, 1),
+        "head_96to3_480x832": ("head", 3, 6, 48, 1),
+        "tconv_up_384to768_60x104": ("tap1x1", 192, 0, 128, 1),
+        "tconv_up_384to768_120x208": ("tap1x1", 192, 0, 128, 1),
+        "tconv_down_s2_384_120x208": ("tap1x1", 192, 0, 128, 1),
+    }
+    for name, wl in WORKLOADS.items():
+        for lname, sp in wl["layers"]:
+            pl = c3c.plan_query(None, sp, wl["dtype"])
+            got = (pl["kernel"], pl["tile_co"], pl["tile_h"], pl["tile_w"], pl["splits"])
+            assert got == want[lname], (lname, pl)
+            assert pl["route"] == ("fallback" if sp["Kt"] == 1 else "fast")
+            if pl["kernel"] == "conv3d_bf16":
+                assert pl["cache_in_kernel"]
+                tiles = (-(-sp["Co"] // pl["tile_co"]) * -(-sp["H"] // pl["tile_h"]) *
+                         -(-sp["W"] // pl["tile_w"]))
+                To, _, _, _ = c3c.output_dims(sp, wl["dtype"])
+                assert pl["workgroups"] == tiles * To * sp["N"]
+
+
+@no_gpu
+def test_plan_splits_with_a_workspace():
+    sp = spec(N=1, Ci=384, Co=384, T=1, Tc=2, H=60, W=104)
+    need = c3c.workspace_bytes(sp, "bf16")
+    assert c3c.plan_query(None, sp, "bf16")["splits"] == 1
+    assert c3c.plan_query(None, sp, "bf16", need - 16)["splits"] == 1
+    pl = c3c.plan_query(None, sp, "bf16", need)
+    assert pl["splits"] == 4 and pl["workgroups"] == 4 * 2 * 15 * 2
+    forced = c3c.plan_query(c3c.Context(c3c.MODE_FORCE_FALLBACK), sp, "bf16")
+    assert (forced["route"], forced["reason"], forced["kernel"]) == \
+        ("fallback", "forced", "fallback_direct")
+    empty = c3c.plan_query(None, dict(sp, T=0), "bf16")
+    assert (empty["kernel"], empty["workgroups"]) == ("none", 0)
+
+
+# ---------------------------------------------------------------------------
+# the binding's size checks (host tensors of the wrong size are refused
+# before their device placement is even looked at)
+# ---------------------------------------------------------------------------
+
+def test_binding_refuses_wrongly_sized_tensors():
+    sp = spec(N=1, Ci=4, Co=8, T=2, Tc=2, H=8, W=8)
+    To, Ho, Wo, L = c3c.output_dims(sp, "bf16")
+    bf = torch.bfloat16
+    ok = dict(x=torch.zeros(1, 4, 2, 8, 8, dtype=bf), cache=torch.zeros(1, 4, 2, 8, 8, dtype=bf),
+              w=torch.zeros(8, 4, 3, 3, 3, dtype=bf),
+              wpack=torch.zeros(c3c.weight_pack_bytes(sp, "bf16") // 2, dtype=bf),
+              bias=torch.zeros(8, dtype=bf), y=torch.zeros(1, 8, To, Ho, Wo, dtype=bf),
+              cache_out=torch.zeros(1, 4, L, 8, 8, dtype=bf))
+    ctx = c3c.Context()
+    for name in ok:
+        args = dict(ok)
+        args[name] = torch.zeros(ok[name].numel() - 1, dtype=bf)
+        with pytest.raises(ValueError, match=f"{name} has"):
+            c3c.conv3d_causal_cached(ctx, sp, args["x"], args["cache"], args["w"], args["wpack"],
+                                     args["bias"], args["y"], args["cache_out"])
+        with pytest.raises(ValueError, match=f"{name} has"):
+            c3c.conv3d_causal_cached_fused(ctx, sp, args["x"], args["cache"], args["w"],
+                                           args["wpack"], args["bias"], y=args["y"],
+                                           cache_out=args["cache_out"])
+    # right sizes: refused only for living in host memory
+    with pytest.raises(ValueError, match="device tensor"):
+        c3c.conv3d_causal_cached(ctx, sp, *ok.values())
+    # a pack for a call with no fast layout
+    sc = spec(N=1, Ci=4, Co=8, T=2, Tc=0, H=8, W=8, Kt=1, Kh=1, Kw=1)
+    with pytest.raises(ValueError, match="no fast-route weight layout"):
+        c3c.conv3d_causal_cached(ctx, sc, torch.zeros(1, 4, 2, 8, 8, dtype=bf), None,
+                                 torch.zeros(8, 4, 1, 1, 1, dtype=bf), ok["wpack"], ok["bias"])
+    with pytest.raises(ValueError, match="residual has"):
+        c3c.conv3d_causal_cached_fused(ctx, sp, ok["x"], ok["cache"], ok["w"], ok["wpack"],
+                                       ok["bias"], residual=torch.zeros(5, dtype=bf), y=ok["y"],
+                                       cache_out=ok["cache_out"])
+    assert ctx.counters()["calls"] == 0
+
+
+@no_gpu
+def test_plan_of_the_160_channel_parity_cases():
+    """The GPU parity cases drawn for the 160-channel tiles land on them:
+    4x80 (ragged rows, columns and channel tiles) and, where it takes fewer
+    rounds of workgroups, 10x32."""
+    want = [(dict(N=1, Ci=64, Co=160, T=3, Tc=2, H=22, W=170), (160, 4, 80)),
+            (dict(N=1, Ci=72, Co=130, T=2, Tc=2, H=13, W=96), (160, 4, 80)),
+            (dict(N=2, Ci=40, Co=181, T=2, Tc=1, H=9, W=83), (160, 4, 80)),
+            (dict(N=1, Ci=48, Co=320, T=2, Tc=2, H=10, W=88), (160, 4, 80)),
+            (dict(N=1, Ci=40, Co=150, T=4, Tc=2, H=333, W=30), (160, 10, 32))]
+    for over, tile in want:
+        pl = c3c.plan_query(None, spec(**over), "bf16")
+        assert pl["kernel"] == "conv3d_bf16"
+        assert (pl["tile_co"], pl["tile_h"], pl["tile_w"]) == tile, (over, pl)
