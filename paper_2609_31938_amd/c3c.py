@@ -24,6 +24,12 @@ if not os.path.exists(LIB_PATH):
     raise ImportError(f"{LIB_PATH} is missing: build it with "
                       "`python -m paper_2609_31938_amd.build` (no CPU fallback exists)")
 
+# torch first: the library must bind to the HIP runtime torch loads, so that
+# both use one runtime (and see the same devices, streams and memory).  Loaded
+# the other way round, the library would load the system runtime next to
+# torch's bundled one, and its calls would find no device.
+import torch  # noqa: E402,F401
+
 OK, E_INVAL, E_UNSUPPORTED, E_DEVICE, E_INJECTED = 0, 1, 2, 3, 4
 DTYPES = {"bf16": 1, "f32": 2, "f16": 3}
 MODE_STRICT, MODE_FORCE_FALLBACK, MODE_INJECT_FAST_FAILURE = 1, 2, 4
