@@ -353,6 +353,30 @@ int c3c_conv3d_causal_cached_fused(c3c_ctx* ctx, const c3c_conv_desc* d,
                                    const float* shift, const void* residual,
                                    void* y, void* cache_out, void* stream);
 
+/* ---------------------------------------------------------------- no allocation */
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the plain
+ * call of c3c_conv3d_causal_cached, same arguments and results, that never
+ * uses a caller workspace and allocates nothing.  A call that splits its
+ * stages (split-K, see c3c_workspace_bytes) keeps its fp32 partial sums in
+ * a scratch array inside the library instead: C3C_NOALLOC_SCRATCH_BYTES
+ * bytes of device memory on each device the library runs on, held until the
+ * process ends.  The array is looked up on the call's first use of a device
+ * (no allocation).  A call whose split needs more than that returns EINVAL
+ * (not counted) with a message naming both sizes.  Every call on one device
+ * shares its array, which keeps the last call's partial sums: calls that
+ * overlap in time on one device (several streams or host threads) race and
+ * must be serialised by the caller.  The context's workspace, if any, is
+ * ignored.  Routing, counters, modes and errors otherwise as for
+ * c3c_conv3d_causal_cached (a failed symbol lookup is C3C_E_DEVICE, counted
+ * nowhere). */
+#define C3C_NOALLOC_SCRATCH_BYTES (64ll << 20)
+int c3c_conv3d_causal_cached_noalloc(c3c_ctx* ctx, const c3c_conv_desc* d,
+                                     const void* x, const void* cache,
+                                     const void* w, const void* wpack,
+                                     const void* bias, void* y,
+                                     void* cache_out, void* stream);
+
 /* ---------------------------------------------------------------- counters */
 int c3c_counters_get(const c3c_ctx* ctx, c3c_counters* out);
 int c3c_counters_reset(c3c_ctx* ctx); /* also clears the shape histogram */

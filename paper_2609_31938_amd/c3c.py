@@ -36,6 +36,7 @@ MODE_STRICT, MODE_FORCE_FALLBACK, MODE_INJECT_FAST_FAILURE = 1, 2, 4
 ROUTES = ["fast", "fallback"]
 REASONS = ["none", "forced", "dtype", "groups", "stride_t", "pad_right", "no_output",
            "no_tap", "kt1", "spatial", "fast_error"]
+NOALLOC_SCRATCH_BYTES = 64 << 20  # C3C_NOALLOC_SCRATCH_BYTES
 KERNELS = ["none", "conv3d_bf16", "head", "tap1x1", "pointwise", "fast_f32", "fallback_direct"]
 
 
@@ -90,6 +91,8 @@ lib.c3c_weight_unpack.argtypes = [_P(Desc), _vp, _vp, _vp]
 lib.c3c_conv3d_causal_cached.argtypes = [_vp, _P(Desc), _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp]
 lib.c3c_conv3d_causal_cached_fused.argtypes = [_vp, _P(Desc), _vp, _vp, _vp, _vp, _vp, _vp, _vp,
                                                _vp, _vp, _vp, _vp]
+lib.c3c_conv3d_causal_cached_noalloc.argtypes = [_vp, _P(Desc), _vp, _vp, _vp, _vp, _vp, _vp,
+                                                 _vp, _vp]
 lib.c3c_counters_get.argtypes = [_vp, _P(Counters)]
 lib.c3c_mfma_probe.argtypes = [C.c_int64, C.c_int64, _vp, _P(C.c_double), _vp]
 lib.c3c_counters_reset.argtypes = [_vp]
@@ -371,6 +374,24 @@ def conv3d_causal_cached(ctx, spec: dict, x, cache, w, wpack, bias, y=None, cach
                                                             bias, y, cache_out),
         _stream(stream))
     _raise(st, ctx, "c3c_conv3d_causal_cached")
+    return y, cache_out
+
+
+def conv3d_causal_cached_noalloc(ctx, spec: dict, x, cache, w, wpack, bias, y, cache_out,
+                                 stream=None):
+    """The allocation-free call (c3c_conv3d_causal_cached_noalloc): the
+    plain call with any split-K partial sums in the library's own device
+    scratch.  The caller passes every output; nothing is allocated here or in
+    the library.  Returns (y, cache_out)."""
+    dtype = dtype_of(w)
+    n = _sizes(spec, dtype)
+    if y is None or (cache_out is None and n["cache_out"] > 0):
+        raise ValueError("the allocation-free call takes caller-allocated y and cache_out")
+    st = lib.c3c_conv3d_causal_cached_noalloc(
+        ctx._h, C.byref(make_desc(spec, dtype)), *_call_ptrs(spec, dtype, n, x, cache, w, wpack,
+                                                            bias, y, cache_out),
+        _stream(stream))
+    _raise(st, ctx, "c3c_conv3d_causal_cached_noalloc")
     return y, cache_out
 
 

@@ -379,9 +379,11 @@ int c3c_weight_unpack(const c3c_conv_desc* d, const void* wpack, void* w_out, vo
 namespace {
 
 // One call, plain or fused (fu: the fused form's prologue / epilogue, or none).
+// ws / ws_cap: the split-K (and prologue-pass) workspace: the context's, or
+// the library's own scratch for the allocation-free entry point.
 int run_call(c3c_ctx* ctx, const c3c_conv_desc* d, const void* x, const void* cache,
              const void* w, const void* wpack, const void* bias, const Fuse& fu, void* y,
-             void* cache_out, void* stream) {
+             void* cache_out, void* stream, void* ws, size_t ws_cap) {
   if (!ctx) return C3C_E_INVAL;
   Geo g;
   const char* why = make_geo(d, &g);
@@ -408,20 +410,19 @@ int run_call(c3c_ctx* ctx, const c3c_conv_desc* d, const void* x, const void* ca
   if (overlap(y, yb, x, xb) || overlap(y, yb, cache, cb) || overlap(y, yb, w, wb) ||
       overlap(y, yb, bias, bb) || overlap(y, yb, cache_out, ob))
     return fail(ctx, C3C_E_INVAL, "y overlaps another tensor");
-  const int64_t wsb = static_cast<int64_t>(ctx->ws_bytes);
-  if (overlap(ctx->ws, wsb, x, xb) || overlap(ctx->ws, wsb, cache, cb) ||
-      overlap(ctx->ws, wsb, w, wb) || overlap(ctx->ws, wsb, bias, bb) ||
-      overlap(ctx->ws, wsb, y, yb) || overlap(ctx->ws, wsb, cache_out, ob))
+  const int64_t wsb = static_cast<int64_t>(ws_cap);
+  if (overlap(ws, wsb, x, xb) || overlap(ws, wsb, cache, cb) || overlap(ws, wsb, w, wb) ||
+      overlap(ws, wsb, bias, bb) || overlap(ws, wsb, y, yb) || overlap(ws, wsb, cache_out, ob))
     return fail(ctx, C3C_E_INVAL, "the context's workspace overlaps a tensor");
   if (fu.any()) {
     if (d->dtype != C3C_DTYPE_BF16) return fail(ctx, C3C_E_INVAL, "the fused form is bf16 only");
     const int64_t sb = fu.pro() ? d->N * d->Ci * 4 : 0;
     const int64_t rb = fu.residual ? yb : 0;
     for (const void* p : {static_cast<const void*>(fu.scale), static_cast<const void*>(fu.shift)})
-      if (overlap(p, sb, y, yb) || overlap(p, sb, cache_out, ob) || overlap(p, sb, ctx->ws, wsb))
+      if (overlap(p, sb, y, yb) || overlap(p, sb, cache_out, ob) || overlap(p, sb, ws, wsb))
         return fail(ctx, C3C_E_INVAL, "scale or shift overlaps an output");
     if ((fu.residual != y && overlap(fu.residual, rb, y, yb)) || overlap(fu.residual, rb, cache_out, ob) ||
-        overlap(fu.residual, rb, ctx->ws, wsb))
+        overlap(fu.residual, rb, ws, wsb))
       return fail(ctx, C3C_E_INVAL, "residual overlaps an output other than y itself");
   }
 
@@ -432,7 +433,7 @@ int run_call(c3c_ctx* ctx, const c3c_conv_desc* d, const void* x, const void* ca
     if (!wpack) return fail(ctx, C3C_E_INVAL, "wpack is NULL on a call that routes fast");
     if (overlap(y, yb, wpack, static_cast<int64_t>(pb)) ||
         overlap(cache_out, ob, wpack, static_cast<int64_t>(pb)) ||
-        overlap(ctx->ws, wsb, wpack, static_cast<int64_t>(pb)))
+        overlap(ws, wsb, wpack, static_cast<int64_t>(pb)))
       return fail(ctx, C3C_E_INVAL, "an output or the workspace overlaps wpack");
   }
 
@@ -454,17 +455,15 @@ int run_call(c3c_ctx* ctx, const c3c_conv_desc* d, const void* x, const void* ca
       // activated chunk (the 3x3 kernels would evaluate it per staging);
       // the rest of the workspace serves split-K
       const int64_t pr = fu.pro() ? prologue_region_bytes(g) : 0;
-      if (pr > 0 && static_cast<int64_t>(ctx->ws_bytes) >= pr && d->T > 0) {
-        unsigned char* u = static_cast<unsigned char*>(ctx->ws);
+      if (pr > 0 && wsb >= pr && d->T > 0) {
+        unsigned char* u = static_cast<unsigned char*>(ws);
         e = launch_prologue(g, x, fu.scale, fu.shift, u, s);
         Fuse rest;
         rest.residual = fu.residual;
         if (e == hipSuccess)
-          e = launch_fast(g, u, cache, wpack, bias, y, cache_out, u + pr,
-                          static_cast<int64_t>(ctx->ws_bytes) - pr, s, rest);
+          e = launch_fast(g, u, cache, wpack, bias, y, cache_out, u + pr, wsb - pr, s, rest);
       } else {
-        e = launch_fast(g, x, cache, wpack, bias, y, cache_out, ctx->ws,
-                        static_cast<int64_t>(ctx->ws_bytes), s, fu);
+        e = launch_fast(g, x, cache, wpack, bias, y, cache_out, ws, wsb, s, fu);
       }
     }
     if (e == hipSuccess) {
@@ -503,7 +502,32 @@ int run_call(c3c_ctx* ctx, const c3c_conv_desc* d, const void* x, const void* ca
 int c3c_conv3d_causal_cached(c3c_ctx* ctx, const c3c_conv_desc* d, const void* x,
                              const void* cache, const void* w, const void* wpack,
                              const void* bias, void* y, void* cache_out, void* stream) {
-  return run_call(ctx, d, x, cache, w, wpack, bias, Fuse{}, y, cache_out, stream);
+  return run_call(ctx, d, x, cache, w, wpack, bias, Fuse{}, y, cache_out, stream,
+                  ctx ? ctx->ws : nullptr, ctx ? ctx->ws_bytes : 0);
+}
+
+int c3c_conv3d_causal_cached_noalloc(c3c_ctx* ctx, const c3c_conv_desc* d, const void* x,
+                                     const void* cache, const void* w, const void* wpack,
+                                     const void* bias, void* y, void* cache_out, void* stream) {
+  if (!ctx) return C3C_E_INVAL;
+  Geo g;
+  const char* why = make_geo(d, &g);
+  if (*why) return fail(ctx, C3C_E_INVAL, why);
+  // the split-K bytes this call plans for, when it routes fast
+  int64_t need = 0;
+  if (decide(g, ctx->mode) == C3C_REASON_NONE && d->dtype == C3C_DTYPE_BF16 && spatial_3x3(*d))
+    need = fast_bf16_workspace_bytes(g);
+  if (need > kNoallocScratchBytes)
+    return fail(ctx, C3C_E_INVAL,
+                "split-K needs " + std::to_string(need) + " bytes of scratch; the allocation-free "
+                "call has " + std::to_string(kNoallocScratchBytes));
+  void* ws = nullptr;
+  if (need > 0) {
+    const hipError_t e = noalloc_scratch(&ws);
+    if (e != hipSuccess) return fail(ctx, C3C_E_DEVICE, hipGetErrorString(e));
+  }
+  return run_call(ctx, d, x, cache, w, wpack, bias, Fuse{}, y, cache_out, stream, ws,
+                  static_cast<size_t>(need));
 }
 
 int c3c_conv3d_causal_cached_fused(c3c_ctx* ctx, const c3c_conv_desc* d, const void* x,
@@ -517,7 +541,8 @@ int c3c_conv3d_causal_cached_fused(c3c_ctx* ctx, const c3c_conv_desc* d, const v
   fu.scale = scale;
   fu.shift = shift;
   fu.residual = static_cast<const uint16_t*>(residual);
-  return run_call(ctx, d, x, cache, w, wpack, bias, fu, y, cache_out, stream);
+  return run_call(ctx, d, x, cache, w, wpack, bias, fu, y, cache_out, stream,
+                  ctx ? ctx->ws : nullptr, ctx ? ctx->ws_bytes : 0);
 }
 
 int c3c_counters_get(const c3c_ctx* ctx, c3c_counters* out) {

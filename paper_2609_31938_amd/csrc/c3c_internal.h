@@ -126,5 +126,10 @@ hipError_t launch_prologue(const Geo& g, const void* x, const float* scale, cons
                            void* u, hipStream_t s);
 hipError_t launch_cache_copy(const Geo& g, const void* x, const void* cache, void* cache_out,
                              hipStream_t s, const Fuse& fu = Fuse{});
+// The allocation-free entry point's split-K scratch (noalloc.hip): a
+// file-scope device array of kNoallocScratchBytes; *ptr receives its address
+// on the current device (looked up once per device).
+constexpr int64_t kNoallocScratchBytes = C3C_NOALLOC_SCRATCH_BYTES;
+hipError_t noalloc_scratch(void** ptr);
 
 }  // namespace c3c

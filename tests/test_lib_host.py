@@ -34,7 +34,8 @@ def test_every_declared_symbol_is_exported():
         "c3c_conv3d_causal_cached", "c3c_counters_get", "c3c_counters_reset",
         "c3c_fallback_shapes", "c3c_strerror", "c3c_last_error",
         "c3c_workspace_bytes", "c3c_ctx_set_workspace", "c3c_conv3d_causal_cached_fused",
-        "c3c_mfma_probe", "c3c_fused_workspace_bytes", "c3c_plan_query"])
+        "c3c_mfma_probe", "c3c_fused_workspace_bytes", "c3c_plan_query",
+        "c3c_conv3d_causal_cached_noalloc"])
     for n in names:
         assert hasattr(c3c.lib, n), n
 
@@ -441,3 +442,25 @@ def test_plan_of_the_160_channel_parity_cases():
         pl = c3c.plan_query(None, spec(**over), "bf16")
         assert pl["kernel"] == "conv3d_bf16"
         assert (pl["tile_co"], pl["tile_h"], pl["tile_w"]) == tile, (over, pl)
+
+
+@no_gpu
+def test_noalloc_refuses_an_oversized_split_before_device_work():
+    ctx = c3c.Context()
+    big = spec(N=1, Ci=384, Co=192, T=1, Tc=2, H=184, W=160)
+    assert c3c.workspace_bytes(big, "bf16") > c3c.NOALLOC_SCRATCH_BYTES
+    d = c3c.make_desc(big, "bf16")
+    f = c3c.lib.c3c_conv3d_causal_cached_noalloc
+    p = FAKE
+    assert f(ctx._h, C.byref(d), p["x"], p["cache"], p["w"], p["wpack"], p["b"], p["y"], p["co"],
+             None) == c3c.E_INVAL
+    assert "scratch" in ctx.last_error and str(64 << 20) in ctx.last_error
+    assert f(None, C.byref(d), p["x"], p["cache"], p["w"], p["wpack"], p["b"], p["y"], p["co"],
+             None) == c3c.E_INVAL
+    assert ctx.counters()["calls"] == 0
+    # forced onto the fallback, the same call needs no scratch: it is counted
+    # (and fails here only for want of a device)
+    ctx.mode = c3c.MODE_FORCE_FALLBACK
+    assert f(ctx._h, C.byref(d), p["x"], p["cache"], p["w"], p["wpack"], p["b"], p["y"], p["co"],
+             None) == c3c.E_DEVICE
+    assert ctx.counters()["failed"] == 1
