@@ -16,7 +16,14 @@ in device memory.
 Prints ONE JSON line: whole-chunk TFLOP/s (algorithmic FLOP: only valid
 temporal taps, padded spatial positions counted), chunk latency, per-layer
 TFLOP/s and fraction of the 2.5 PFLOP/s bf16 matrix peak, the dominant
-kernel's roofline, and the oracle's CPU rate on a bounded sample.
+kernel's roofline, and the oracle's CPU rate on a bounded sample.  The same
+line carries the other layer configurations, each streamed once untimed and
+once timed from a zero cache ("configs": the tiny fp32 layer against the
+157.3 TFLOP/s fp32 matrix peak, the 384-channel 60x104 one-frame layer with
+and without the split-K workspace, the two 240x416 layers, the 96-channel
+480x832 layer), and the run's provenance (host CPU, thread counts, ROCm,
+hipcc and torch versions, library and kernel-source hashes, SHA-256 of every
+input buffer).
 """
 import argparse
 import gc
@@ -38,14 +45,41 @@ PEAK_F32_TFLOPS = 157.3     # MI355X fp32 matrix peak (published)
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E peak (published)
 
 
+# The library's compute kernels, by the plan query's name for them (the
+# kernel a call's plan names is its one main launch); the auxiliary kernels a
+# call may add after it (split-K reduction, cache copy, prologue pass).
+MAIN_KERNELS = {"conv3d_bf16": "conv3d_bf16", "head": "conv_head", "tap1x1": "conv_tap1x1",
+                "pointwise": "pointwise_conv", "fast_f32": "fast_conv3d",
+                "fallback_direct": "fallback_conv3d"}
+AUX_KERNELS = ("splitk_reduce", "cache_copy", "cache_copy_pro", "prologue_pass")
+
+# Further configurations timed by a default run, after the headline one:
+# (label, workload, with the split-K workspace attached).
+EXTRA_CONFIGS = (("C1", "tiny_f32", False), ("C2", "low_res", False),
+                 ("C2+workspace", "low_res", True), ("C3", "mid_res", False),
+                 ("C4", "full_res", False))
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="stack_720p")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-configs", action="store_true",
+                    help="time the headline workload only (skip the other configurations)")
+    ap.add_argument("--no-hash", action="store_true",
+                    help="skip the SHA-256 of the inputs (provenance)")
+    ap.add_argument("--launch-log", default=None,
+                    help="write every library call of the run (workload, layer, phase, "
+                         "planned kernel) and the printed line to this JSON file, for "
+                         "--trace-summary")
+    ap.add_argument("--trace-summary", nargs=2, metavar=("KERNEL_TRACE_CSV", "LAUNCH_LOG"),
+                    default=None,
+                    help="print the per-layer kernel times of a rocprofv3 --kernel-trace "
+                         "run of this script (matched to its --launch-log) and exit")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a plain 512 MiB device copy (the reference kernel "
                          "for scaling FETCH_SIZE / WRITE_SIZE counters) and exit")
@@ -61,6 +95,9 @@ def main():
                          "conv-shaped problems and exit: what the matrix cores reach "
                          "on this device outside this library")
     args = ap.parse_args()
+    if args.trace_summary:
+        trace_summary(*args.trace_summary)
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
               "(run with --gpus 1)", file=sys.stderr)
@@ -79,134 +116,68 @@ def main():
         fused_block(args.workload, args.steps)
         return
 
-    wl = inputs.WORKLOADS[args.workload]
-    dtype = wl["dtype"]
     dev = torch.device("cuda", 0)
     torch.cuda.set_device(dev)
-    ctx = c3c.Context()
-    chunks = wl["chunks"]
+    log = [] if args.launch_log else None
+    digests = {}
 
-    # ---------------------------------------------------------------- setup
-    layers = []
-    names = [lname for lname, _ in wl["layers"]]
-    if args.layer is not None and args.layer not in names:
-        print(f"unknown layer {args.layer!r}; the workload has {names}", file=sys.stderr)
-        sys.exit(2)
-    for lid, (lname, sp) in enumerate(wl["layers"]):
-        if args.layer is not None and lname != args.layer:
-            continue
-        w, b = inputs.layer_tensors(sp, dtype, wl["id"], lid, dev)
-        route, why = c3c.route_query(None, sp, dtype)
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        wpack = c3c.weight_repack(ctx, sp, w) if route == "fast" else None
-        torch.cuda.synchronize()
-        repack_ms = (time.perf_counter() - t0) * 1e3 if route == "fast" else None
-        To, Ho, Wo, L = c3c.output_dims(sp, dtype)
-        xs = [inputs.chunk_input(sp, dtype, wl["id"], lid, c, dev) for c in range(chunks)]
-        y = torch.empty((sp["N"], sp["Co"], To, Ho, Wo), dtype=w.dtype, device=dev)
-        cbuf = [torch.zeros((sp["N"], sp["Ci"], sp["Tc"], sp["H"], sp["W"]), dtype=w.dtype,
-                            device=dev) for _ in range(2)]
-        layers.append(dict(name=lname, sp=sp, w=w, b=b, wpack=wpack, xs=xs, y=y, cbuf=cbuf,
-                           route=route, reason=why, flops=c3c.flops(sp, dtype),
-                           repack_ms=repack_ms))
-    torch.cuda.synchronize()
-
-    def reset_caches():
-        for L_ in layers:
-            for cb in L_["cbuf"]:
-                cb.zero_()
-            L_["cur"] = 0
-
-    def step(s, evs=None):
-        c = s % chunks
-        for i, L_ in enumerate(layers):
-            sp = L_["sp"]
-            cin = L_["cbuf"][L_["cur"]] if sp["Tc"] else None
-            cout = L_["cbuf"][1 - L_["cur"]] if sp["Tc"] else None
-            if evs is not None:
-                evs[i][0].record()
-            c3c.conv3d_causal_cached(ctx, sp, L_["xs"][c], cin, L_["w"], L_["wpack"], L_["b"],
-                                     L_["y"], cout)
-            if evs is not None:
-                evs[i][1].record()
-            if sp["Tc"]:
-                L_["cur"] = 1 - L_["cur"]
-
-    # ---------------------------------------------------------------- warmup
-    # Python's cyclic collector can stall the host for tens of milliseconds
-    # between two launches (seen at fixed points of a run): it runs before
-    # the warm-up and is held off until the timed region ends.  Not between
-    # the two: an idle gap there lets the clocks fall before the timed steps.
-    gc.collect()
-    gc.disable()
-    reset_caches()
-    for s in range(args.warmup):
-        step(s)
-    torch.cuda.synchronize()
-    ctx.reset()
-    reset_caches()
-    torch.cuda.synchronize()
-
-    # ---------------------------------------------------------------- timed
-    ev = [[[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in layers]
-          for _ in range(args.steps)]
-    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t_wall = time.perf_counter()
-    start.record()
-    for s in range(args.steps):
-        step(s, ev[s])
-    stop.record()
-    torch.cuda.synchronize()
-    t_wall = time.perf_counter() - t_wall
-    gc.enable()
-    total_ms = start.elapsed_time(stop)
-
-    counters = ctx.counters()
-    per_layer = []
-    total_flops = 0.0
-    for i, L_ in enumerate(layers):
-        times = [ev[s][i][0].elapsed_time(ev[s][i][1]) for s in range(args.steps)]
-        fl = L_["flops"]
-        total_flops += fl * args.steps
-        med = statistics.median(times)
-        tf = fl / (med * 1e-3) / 1e12
-        peak = PEAK_BF16_TFLOPS if dtype == "bf16" else PEAK_F32_TFLOPS
-        per_layer.append(dict(layer=L_["name"], route=L_["route"], reason=L_["reason"],
-                              gflop=round(fl / 1e9, 3), ms_median=round(med, 4),
-                              ms_mean=round(sum(times) / len(times), 4),
-                              tflops=round(tf, 2), frac_peak=round(tf / peak, 4),
-                              repack_ms=(round(L_["repack_ms"], 3)
-                                         if L_["repack_ms"] is not None else None)))
+    # ------------------------------------------------------------ headline
+    head = Workload(args.workload, dev, layer=args.layer, log=log)
+    wl = head.wl
+    dtype = wl["dtype"]
+    total_ms, per_layer, t_wall, counters = head.time_steps(args.steps, args.warmup)
+    total_flops = sum(L_["flops"] for L_ in head.layers) * args.steps
     value = total_flops / (total_ms * 1e-3) / 1e12
 
     # dominant kernel: the fast conv on the largest layer
     fast_layers = [p for p in per_layer if p["route"] == "fast"] or per_layer
     dom = max(fast_layers, key=lambda p: p["gflop"])
     dom_i = [p["layer"] for p in per_layer].index(dom["layer"])
+    dom_L = head.layers[dom_i]
     dom_mean_ms = dom["ms_mean"]
     achieved = dom["gflop"] * 1e9 / (dom_mean_ms * 1e-3) / 1e12
     peak = PEAK_BF16_TFLOPS if dtype == "bf16" else PEAK_F32_TFLOPS
     if dom["route"] == "fast":
-        kname = "conv3d_bf16" if layers[dom_i]["sp"]["Kh"] == 3 else "pointwise_conv (1x1 spatial)"
+        kname = dom["kernel"]
         roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak,
                     "unit": "TFLOP/s", "frac": round(achieved / peak, 4),
                     "traffic": measured_traffic(dom["layer"]) if kname == "conv3d_bf16" else None,
-                    "kernel": f"{kname} (fast route), layer {dom['layer']}"}
+                    "kernel": f"{kname} (fast route), layer {dom['layer']}",
+                    "timing": f"mean of {args.steps} HIP-event-bracketed launches "
+                              "on the launch stream"}
     else:
         # a fallback layer timed alone (--layer): HBM-bound, algorithmic bytes
-        gbs = algorithmic_bytes(layers[dom_i]["sp"], dtype) / (dom_mean_ms * 1e-3) / 1e9
+        gbs = algorithmic_bytes(dom_L["sp"], dtype) / (dom_mean_ms * 1e-3) / 1e9
         roofline = {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS,
                     "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4), "traffic": None,
                     "kernel": f"fallback route, layer {dom['layer']}"}
-    # the matrix cores' sustained rate on this machine (outside the timed region):
-    # back-to-back bf16 products, one workgroup per compute unit
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(dom_L, dtype, args.cpu_seconds)
+    if not args.no_hash:
+        digests[args.workload] = head.input_sha256()
+    shapes = sorted({(L_["sp"]["T"], L_["sp"]["Tc"]) for L_ in head.layers})
+    frames = ", ".join(f"T={t} new + {tc} cached frames" for t, tc in shapes)
+    chunks = wl["chunks"]
+    layer_names = ", ".join(L_["name"] for L_ in head.layers)
+    dom_L = None
+    head.free()
+
+    # ----------------------------------------------- the other configurations
+    configs = {}
+    if not args.no_configs and args.layer is None and args.workload == "stack_720p":
+        for label, name, ws in EXTRA_CONFIGS:
+            w_ = Workload(name, dev, use_ws=ws, log=log, label=label)
+            configs[label] = w_.time_stream()
+            if not args.no_hash and name not in digests:
+                digests[name] = w_.input_sha256()
+            w_.free()
+
+    # the matrix cores' sustained rate on this machine (outside the timed regions):
+    # back-to-back bf16 products, four workgroups per compute unit
     probe = mfma_probe_rate()
     if roofline["bound"] == "mfma" and dtype == "bf16":
         roofline["frac_of_probe"] = round(achieved / probe["tflops"], 4)
-    shapes = sorted({(L_["sp"]["T"], L_["sp"]["Tc"]) for L_ in layers})
-    frames = ", ".join(f"T={t} new + {tc} cached frames" for t, tc in shapes)
 
     out = {
         "metric": METRIC,
@@ -221,20 +192,331 @@ def main():
         "vs_baseline": None,
         "dtype": dtype,
         "data": "synthetic",
-        "config": {"workload": f"{args.workload}: " + ", ".join(
-            f"{L_['name']}" for L_ in layers) + f"; N=1, {frames}, "
+        "config": {"workload": f"{args.workload}: {layer_names}; N=1, {frames}, "
             f"{chunks}-chunk cache carry; step = one chunk through every layer",
             "global_batch": 1, "chunks_per_stream": chunks},
         "chunk_latency_ms": round(total_ms / args.steps, 4),
         "layers": per_layer,
         "roofline": roofline,
+        "configs": configs,
         "mfma_probe": probe,
         "counters": counters,
         "wall_s": round(t_wall, 4),
+        "provenance": provenance(digests),
     }
-    if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(layers[dom_i], dtype, args.cpu_seconds)
-    print(json.dumps(out), flush=True)
+    if cpu is not None:
+        out["cpu_baseline"] = cpu
+    line = json.dumps(out)
+    print(line, flush=True)
+    if log is not None:
+        with open(args.launch_log, "w") as f:
+            json.dump({"calls": log, "bench_line": out}, f)
+
+
+class Workload:
+    """One workload's device tensors (weights repacked once, every chunk's
+    input resident in device memory, two cache buffers per layer that swap
+    roles between chunks) and its timed runs."""
+
+    def __init__(self, name, dev, use_ws=False, layer=None, log=None, label=None):
+        import torch
+        from paper_2609_31938_amd import c3c, inputs
+        self.name, self.label, self.log = name, label or name, log
+        self.wl = wl = inputs.WORKLOADS[name]
+        self.dtype = dtype = wl["dtype"]
+        self.chunks = wl["chunks"]
+        self.ctx = c3c.Context()
+        self.ws = None
+        names = [lname for lname, _ in wl["layers"]]
+        if layer is not None and layer not in names:
+            print(f"unknown layer {layer!r}; the workload has {names}", file=sys.stderr)
+            sys.exit(2)
+        self.layers = []
+        need = 0
+        for lid, (lname, sp) in enumerate(wl["layers"]):
+            if layer is not None and lname != layer:
+                continue
+            w, b = inputs.layer_tensors(sp, dtype, wl["id"], lid, dev)
+            route, why = c3c.route_query(None, sp, dtype)
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            wpack = c3c.weight_repack(self.ctx, sp, w) if route == "fast" else None
+            torch.cuda.synchronize()
+            repack_ms = (time.perf_counter() - t0) * 1e3 if route == "fast" else None
+            To, Ho, Wo, L = c3c.output_dims(sp, dtype)
+            xs = [inputs.chunk_input(sp, dtype, wl["id"], lid, c, dev) for c in range(self.chunks)]
+            y = torch.empty((sp["N"], sp["Co"], To, Ho, Wo), dtype=w.dtype, device=dev)
+            cbuf = [torch.zeros((sp["N"], sp["Ci"], sp["Tc"], sp["H"], sp["W"]), dtype=w.dtype,
+                                device=dev) for _ in range(2)]
+            if use_ws:
+                need = max(need, c3c.workspace_bytes(sp, dtype))
+            self.layers.append(dict(name=lname, sp=sp, w=w, b=b, wpack=wpack, xs=xs, y=y,
+                                    cbuf=cbuf, route=route, reason=why,
+                                    flops=c3c.flops(sp, dtype), repack_ms=repack_ms))
+        if need:
+            self.ws = torch.empty((need + 3) // 4, dtype=torch.float32, device=dev)
+            self.ctx.set_workspace(self.ws)
+        for L_ in self.layers:
+            L_["plan"] = c3c.plan_query(self.ctx, L_["sp"], dtype,
+                                        self.ws.numel() * 4 if self.ws is not None else 0)
+        torch.cuda.synchronize()
+
+    def reset_caches(self):
+        for L_ in self.layers:
+            for cb in L_["cbuf"]:
+                cb.zero_()
+            L_["cur"] = 0
+
+    def chunk(self, c, phase, evs=None):
+        """Chunk c through every layer, caches carried; evs[i] = (start, end)
+        events recorded around layer i's call."""
+        from paper_2609_31938_amd import c3c
+        for i, L_ in enumerate(self.layers):
+            sp = L_["sp"]
+            cin = L_["cbuf"][L_["cur"]] if sp["Tc"] else None
+            cout = L_["cbuf"][1 - L_["cur"]] if sp["Tc"] else None
+            if self.log is not None:
+                p = L_["plan"]
+                self.log.append(dict(workload=self.label, layer=L_["name"], phase=phase,
+                                     kernel=p["kernel"], splits=p["splits"],
+                                     workgroups=p["workgroups"]))
+            if evs is not None:
+                evs[i][0].record()
+            c3c.conv3d_causal_cached(self.ctx, sp, L_["xs"][c], cin, L_["w"], L_["wpack"],
+                                     L_["b"], L_["y"], cout)
+            if evs is not None:
+                evs[i][1].record()
+            if sp["Tc"]:
+                L_["cur"] = 1 - L_["cur"]
+
+    def _events(self, n):
+        import torch
+        return [[[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in self.layers]
+                for _ in range(n)]
+
+    def _per_layer(self, ev):
+        peak = PEAK_BF16_TFLOPS if self.dtype == "bf16" else PEAK_F32_TFLOPS
+        rows = []
+        for i, L_ in enumerate(self.layers):
+            times = [e[i][0].elapsed_time(e[i][1]) for e in ev]
+            fl = L_["flops"]
+            med = statistics.median(times)
+            tf = fl / (med * 1e-3) / 1e12
+            p = L_["plan"]
+            rows.append(dict(layer=L_["name"], route=L_["route"], reason=L_["reason"],
+                             kernel=p["kernel"], splits=p["splits"], workgroups=p["workgroups"],
+                             gflop=round(fl / 1e9, 3), ms_median=round(med, 4),
+                             ms_mean=round(sum(times) / len(times), 4),
+                             tflops=round(tf, 2), frac_peak=round(tf / peak, 4),
+                             repack_ms=(round(L_["repack_ms"], 3)
+                                        if L_["repack_ms"] is not None else None)))
+        return rows
+
+    def time_steps(self, steps, warmup):
+        """Headline timing: `warmup` untimed chunks, then `steps` timed chunks
+        (the chunk index wraps around the stream; caches keep carrying),
+        bracketed by synchronisations."""
+        import torch
+        # Python's cyclic collector can stall the host for tens of
+        # milliseconds between two launches: it runs before the warm-up and
+        # is held off until the timed region ends.  Not between the two: an
+        # idle gap there lets the clocks fall before the timed steps.
+        gc.collect()
+        gc.disable()
+        self.reset_caches()
+        for s in range(warmup):
+            self.chunk(s % self.chunks, "warmup")
+        torch.cuda.synchronize()
+        self.ctx.reset()
+        self.reset_caches()
+        torch.cuda.synchronize()
+        ev = self._events(steps)
+        start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        t_wall = time.perf_counter()
+        start.record()
+        for s in range(steps):
+            self.chunk(s % self.chunks, "timed", ev[s])
+        stop.record()
+        torch.cuda.synchronize()
+        t_wall = time.perf_counter() - t_wall
+        gc.enable()
+        return start.elapsed_time(stop), self._per_layer(ev), t_wall, self.ctx.counters()
+
+    def time_stream(self):
+        """One untimed pass over the whole stream (every chunk, caches carried
+        from a zero cache), then one timed pass from a zero cache again:
+        per-layer call times (median over the chunks), the chunk latency
+        (first layer's start to last layer's end, median over the chunks) and
+        the stream's whole time."""
+        import torch
+        gc.collect()
+        gc.disable()
+        self.reset_caches()
+        for c in range(self.chunks):
+            self.chunk(c, "warmup")
+        torch.cuda.synchronize()
+        self.ctx.reset()
+        self.reset_caches()
+        torch.cuda.synchronize()
+        ev = self._events(self.chunks)
+        start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        start.record()
+        for c in range(self.chunks):
+            self.chunk(c, "timed", ev[c])
+        stop.record()
+        torch.cuda.synchronize()
+        gc.enable()
+        lat = [e[0][0].elapsed_time(e[-1][1]) for e in ev]
+        stream_ms = start.elapsed_time(stop)
+        flops = sum(L_["flops"] for L_ in self.layers) * self.chunks
+        return {"workload": self.name, "dtype": self.dtype, "chunks": self.chunks,
+                "split_k_workspace_bytes": self.ws.numel() * 4 if self.ws is not None else 0,
+                "chunk_latency_ms_median": round(statistics.median(lat), 4),
+                "stream_ms": round(stream_ms, 4),
+                "stream_tflops": round(flops / (stream_ms * 1e-3) / 1e12, 2),
+                "layers": self._per_layer(ev), "counters": self.ctx.counters()}
+
+    def input_sha256(self):
+        """SHA-256 over every input buffer of the workload (per layer: w, b,
+        then each chunk's x; the first cache is zeros): the digest of the
+        concatenated per-buffer digests."""
+        import hashlib
+        from concurrent.futures import ThreadPoolExecutor
+        from paper_2609_31938_amd import inputs
+        bufs = []
+        for L_ in self.layers:
+            bufs += [L_["w"], L_["b"]] + list(L_["xs"])
+        with ThreadPoolExecutor(8) as ex:
+            parts = list(ex.map(inputs.sha256, bufs))
+        return {"sha256": hashlib.sha256("".join(parts).encode()).hexdigest(),
+                "buffers": len(parts)}
+
+    def free(self):
+        import torch
+        self.ctx.set_workspace(None)
+        self.layers = []
+        self.ws = None
+        gc.collect()
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+
+
+def provenance(digests):
+    """Host, toolchain and input records of the run."""
+    import platform
+    import subprocess
+    import torch
+    cpu_model = None
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                cpu_model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    rocm = None
+    try:
+        rocm = open("/opt/rocm/.info/version").read().strip()
+    except OSError:
+        pass
+    hipcc = None
+    try:
+        r = subprocess.run(["/opt/rocm/bin/hipcc", "--version"], capture_output=True, text=True,
+                           timeout=60)
+        hipcc = " | ".join(l.strip() for l in r.stdout.splitlines()
+                           if "version" in l.lower())[:200] or None
+    except (OSError, subprocess.SubprocessError):
+        pass
+    import oracle
+    props = torch.cuda.get_device_properties(0)
+    import hashlib
+    so = os.path.join(ROOT, "paper_2609_31938_amd", "libc3c.so")
+    return {"cpu_model": cpu_model, "host_threads_available": len(os.sched_getaffinity(0)),
+            "omp_num_threads": os.environ.get("OMP_NUM_THREADS"),
+            "oracle_threads": oracle.num_threads(), "python": platform.python_version(),
+            "torch": torch.__version__, "torch_hip": torch.version.hip, "rocm": rocm,
+            "hipcc": hipcc, "gpu": props.name, "gpu_arch": getattr(props, "gcnArchName", None),
+            "compute_units": props.multi_processor_count,
+            "libc3c_sha256": hashlib.sha256(open(so, "rb").read()).hexdigest(),
+            "conv_bf16_source_sha256": kernel_source_sha256(),
+            "inputs": digests}
+
+
+def trace_summary(csv_path, log_path):
+    """Per-layer kernel times from a rocprofv3 kernel trace of this script,
+    matched to the run's launch log: the library's main kernel launches in
+    dispatch order pair one to one with the logged calls; split-K reductions
+    and cache copies that follow a main launch belong to its call.  Prints
+    markdown."""
+    import csv
+    import re
+    rows = list(csv.DictReader(open(csv_path)))
+    if not rows:
+        sys.exit("empty kernel trace")
+    key = lambda *names: next(k for k in rows[0] if any(n == k for n in names))
+    kn, ks, ke = key("Kernel_Name"), key("Start_Timestamp"), key("End_Timestamp")
+    kd = next((k for k in rows[0] if k in ("Dispatch_Id", "Correlation_Id")), None)
+    rows.sort(key=lambda r: int(r[kd]) if kd else int(r[ks]))
+    main_re = re.compile(r"\b(" + "|".join(MAIN_KERNELS.values()) + r")\b")
+    aux_re = re.compile(r"\b(" + "|".join(AUX_KERNELS) + r")\b")
+    log = json.load(open(log_path))
+    calls, line = log["calls"], log["bench_line"]
+    launches = []  # [name, main ms, aux ms]
+    for r in rows:
+        name = r[kn]
+        ms = (int(r[ke]) - int(r[ks])) * 1e-6
+        m = main_re.search(name)
+        if m:
+            launches.append([name, ms, 0.0])
+        elif aux_re.search(name) and launches:
+            launches[-1][2] += ms
+    if len(launches) != len(calls):
+        sys.exit(f"{len(launches)} main kernel launches in the trace, {len(calls)} calls logged")
+    groups = {}
+    for c, (name, ms, aux) in zip(calls, launches):
+        if MAIN_KERNELS[c["kernel"]] not in name:
+            sys.exit(f"call {c} matched to launch {name}")
+        if c["phase"] != "timed":
+            continue
+        g = groups.setdefault((c["workload"], c["layer"]), dict(kernel=name, ms=[], aux=[]))
+        g["ms"].append(ms)
+        g["aux"].append(aux)
+    ev = {(line["config"]["workload"].split(":")[0], p["layer"]): p for p in line["layers"]}
+    for label, cfg in line.get("configs", {}).items():
+        for p in cfg["layers"]:
+            ev[(label, p["layer"])] = p
+    head = line["config"]["workload"].split(":")[0]
+    print("| workload | layer | kernel | launches | trace mean ms | trace median ms | "
+          "aux ms | TFLOP/s (trace mean) | % of peak (trace) | event mean ms | % of peak (events) |")
+    print("|---|---|---|---|---|---|---|---|---|---|---|")
+    for (wl, layer), g in groups.items():
+        wl_name = head if wl == head else wl
+        p = ev.get((wl_name, layer))
+        mean = sum(g["ms"]) / len(g["ms"])
+        med = statistics.median(g["ms"])
+        aux = sum(g["aux"]) / len(g["aux"])
+        km = re.search(r"\b(" + "|".join(MAIN_KERNELS.values()) + r")\b(<[^()]*>)?", g["kernel"])
+        kname = km.group(0) if km else g["kernel"]
+        if p is not None:
+            peak = p["tflops"] / p["frac_peak"] if p["frac_peak"] else PEAK_BF16_TFLOPS
+            tf = p["gflop"] * 1e9 / ((mean + aux) * 1e-3) / 1e12
+            print(f"| {wl} | {layer} | `{kname}` | {len(g['ms'])} | {mean:.4f} | {med:.4f} | "
+                  f"{aux:.4f} | {tf:.1f} | {100 * tf / peak:.1f} | {p['ms_mean']:.4f} | "
+                  f"{100 * p['frac_peak']:.1f} (median) |")
+    rf = line["roofline"]
+    dom = rf["kernel"].split("layer ")[-1]
+    g = groups.get((head, dom))
+    if g is not None:
+        mean = sum(g["ms"]) / len(g["ms"])
+        gflop = ev[(head, dom)]["gflop"]
+        tf = gflop * 1e9 / (mean * 1e-3) / 1e12
+        print(f"\nDominant kernel ({rf['kernel']}): trace mean {mean:.4f} ms over "
+              f"{len(g['ms'])} timed launches = {tf:.1f} TFLOP/s = frac {tf / rf['peak']:.4f} "
+              f"of {rf['peak']}; the line's event-based frac is {rf['frac']} "
+              f"(achieved {rf['achieved']}).")
+    print(f"\nBench line of the same run: value {line['value']} TFLOP/s, "
+          f"{line['ms_per_step']} ms per chunk.")
 
 
 def algorithmic_bytes(sp, dtype):
@@ -255,28 +537,34 @@ def algorithmic_bytes(sp, dtype):
 
 
 def mfma_probe_rate(iters=50000):
-    """TFLOP/s of the library's matrix-core probe (c3c_mfma_probe): four
-    workgroups of 4 waves per compute unit, 8 independent bf16 16x16x32
-    products back to back per wave, no memory traffic.  The published peak
-    times the clock the device holds under matrix-core load; the implied
-    clock is reported with it."""
+    """TFLOP/s of the library's matrix-core probe (c3c_mfma_probe): 8
+    independent bf16 16x16x32 products back to back per wave, no memory
+    traffic, at four workgroups of 4 waves per compute unit (4 waves per
+    SIMD) and at one (one wave per SIMD, as the convolution kernels run).  The
+    published peak times the clock the device holds under matrix-core load;
+    the implied clock is reported with it."""
     import torch
     from paper_2609_31938_amd import c3c
     cus = torch.cuda.get_device_properties(0).multi_processor_count
-    blocks = 4 * cus
-    c3c.mfma_probe(blocks, iters // 10)  # warm-up
-    torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record()
-    out, fl = c3c.mfma_probe(blocks, iters)
-    e1.record()
-    torch.cuda.synchronize()
-    ms = e0.elapsed_time(e1)
-    tf = fl / (ms * 1e-3) / 1e12
+
+    def rate(blocks, n):
+        c3c.mfma_probe(blocks, n // 10)  # warm-up
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        out, fl = c3c.mfma_probe(blocks, n)
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1)
+        return fl / (ms * 1e-3) / 1e12, ms, bool(torch.isfinite(out).all().item())
+
+    tf, ms, fin = rate(4 * cus, iters)
+    tf1, _, fin1 = rate(cus, 4 * iters)
     return {"tflops": round(tf, 1), "frac_of_published_peak": round(tf / PEAK_BF16_TFLOPS, 4),
             "implied_clock_ghz": round(2.4 * tf / PEAK_BF16_TFLOPS, 3), "ms": round(ms, 3),
-            "launch": f"{blocks} workgroups x 4 waves, 8 chains, {iters} iterations",
-            "finite": bool(torch.isfinite(out).all().item())}
+            "launch": f"{4 * cus} workgroups x 4 waves, 8 chains, {iters} iterations",
+            "tflops_one_wave_per_simd": round(tf1, 1),
+            "finite": fin and fin1}
 
 
 def fused_block(workload, iters):

@@ -16,8 +16,10 @@
 // columns left of the output tile, so that every 16-byte row segment of the
 // window is aligned).  4 waves, wave v owning window rows 2v, 2v + 1: 8
 // pixel fragments x NF column fragments of accumulators.  The window is
-// sized so that two workgroups fit a compute unit (67 KB of LDS, at most 128
-// registers a lane for NF <= 2): a stage is short (16 products per wave), and
+// sized so that two workgroups fit a compute unit for Co <= 3 (NF = 2: 67 KB
+// of LDS, at most 128 registers a lane; the NF = 3 instance for Co = 4, 5
+// needs 92.9 KB for its D rows and runs one workgroup per unit): a stage is
+// short (16 products per wave), and
 // the second workgroup's stages cover the first's memory waits (measured: 8 x
 // 80 windows at one workgroup per unit were 1.3x slower, 8 x 48 at three
 // 1.1x slower).  A stage is one active tap and one 32-channel chunk: its

@@ -2,12 +2,8 @@
 // with nothing else to do.  Each wave issues v_mfma_f32_16x16x32_bf16 back to
 // back on 8 independent accumulators (enough to cover the instruction's
 // latency), reads no memory in the loop, and writes one reduction per lane
-// at the end so the work is kept.  The compiler moves the accumulators
-// between registers at each loop trip; with two or more workgroups per
-// compute unit another wave's products cover those moves, and the rate is
-// the published peak scaled by the clock the device holds under matrix-core
-// load (measured: 6.6 TFLOP/s per compute unit at one workgroup per unit,
-// 8.0 at two).
+// at the end so the work is kept.  The rate is the published peak scaled by
+// the clock the device holds under matrix-core load.
 #include "c3c_internal.h"
 
 namespace c3c {
@@ -30,12 +26,18 @@ __global__ __launch_bounds__(256, 1) void mfma_probe(float* out, int iters) {
 #pragma unroll
   for (int q = 0; q < CHAINS; ++q) acc[q] = f32x4{0.f, 0.f, 0.f, 0.f};
   // four iterations per loop trip (iters is rounded up to a multiple of 4 by
-  // the host): every accumulator keeps its registers across the back edge
+  // the host)
+  // Each product is written with its accumulator as both source and
+  // destination (a tied "+a" operand), so every accumulator stays in the same
+  // registers for the whole loop: with the compiler's builtin, the register
+  // allocator rotated the accumulators through other registers at every loop
+  // trip, and those moves, not the matrix cores, set the one-wave rate.
   for (int i = 0; i < iters; i += 4) {
 #pragma unroll
     for (int u = 0; u < 4; ++u)
 #pragma unroll
-      for (int q = 0; q < CHAINS; ++q) acc[q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, acc[q], 0, 0, 0);
+      for (int q = 0; q < CHAINS; ++q)
+        asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+a"(acc[q]) : "v"(a), "v"(b));
   }
   float s = 0.f;
 #pragma unroll
