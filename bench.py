@@ -238,11 +238,18 @@ class Workload:
                 continue
             w, b = inputs.layer_tensors(sp, dtype, wl["id"], lid, dev)
             route, why = c3c.route_query(None, sp, dtype)
-            torch.cuda.synchronize()
-            t0 = time.perf_counter()
-            wpack = c3c.weight_repack(self.ctx, sp, w) if route == "fast" else None
-            torch.cuda.synchronize()
-            repack_ms = (time.perf_counter() - t0) * 1e3 if route == "fast" else None
+            wpack, repack_ms = None, None
+            if route == "fast":
+                # the second repack is timed (the first one also loads the
+                # kernel's code object)
+                wpack = c3c.weight_repack(self.ctx, sp, w)
+                torch.cuda.synchronize()
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record()
+                c3c.weight_repack(self.ctx, sp, w, wpack)
+                e1.record()
+                torch.cuda.synchronize()
+                repack_ms = e0.elapsed_time(e1)
             To, Ho, Wo, L = c3c.output_dims(sp, dtype)
             xs = [inputs.chunk_input(sp, dtype, wl["id"], lid, c, dev) for c in range(self.chunks)]
             y = torch.empty((sp["N"], sp["Co"], To, Ho, Wo), dtype=w.dtype, device=dev)

@@ -29,8 +29,9 @@ import os
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-# C3C_ORACLE_LIB lets the mutation test load a deliberately broken copy of
-# the oracle in a child process; nothing else sets it.
+# C3C_ORACLE_LIB loads another build of the oracle: the mutation test's
+# deliberately broken copies (in child processes) and the sanitizer build of
+# the host-side test run; nothing else sets it.
 _LIB_PATH = os.environ.get("C3C_ORACLE_LIB") or os.path.join(_HERE, "liboracle.so")
 
 _FIELDS = ["N", "Ci", "Co", "T", "Tc", "H", "W", "Kt", "Kh", "Kw",

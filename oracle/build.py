@@ -26,6 +26,24 @@ def build(verbose: bool = False) -> str:
     return LIB
 
 
+def build_sanitized(out_dir: str, verbose: bool = False) -> str:
+    """The same source under AddressSanitizer and UndefinedBehaviorSanitizer,
+    built with ROCm's clang so that it shares one sanitizer runtime with the
+    sanitized host code of libc3c (the runtime is preloaded into the test
+    process; see tests/run_sanitized.py)."""
+    os.makedirs(out_dir, exist_ok=True)
+    lib = os.path.join(out_dir, "liboracle.so")
+    cmd = ["/opt/rocm/llvm/bin/clang", "-std=c11", "-O1", "-g", "-fPIC", "-shared", "-fopenmp",
+           "-fno-fast-math", "-ffp-contract=off", "-Wall", "-Wextra",
+           "-fsanitize=address,undefined", "-fno-sanitize-recover=undefined",
+           "-fno-omit-frame-pointer", SRC, "-o", lib, "-lm",
+           "-Wl,-rpath,/opt/rocm/llvm/lib"]
+    if verbose:
+        print(" ".join(cmd))
+    subprocess.check_call(cmd)
+    return lib
+
+
 if __name__ == "__main__":
     build(verbose="-v" in sys.argv)
     print(LIB)

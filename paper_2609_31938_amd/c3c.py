@@ -17,7 +17,9 @@ import os
 import re
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libc3c.so")
+# C3C_LIB selects another build of the same library (the sanitizer build of
+# the host-side test run); by default the in-tree build next to this file
+LIB_PATH = os.environ.get("C3C_LIB") or os.path.join(_HERE, "libc3c.so")
 HEADER = os.path.join(os.path.dirname(_HERE), "include", "c3c.h")
 
 if not os.path.exists(LIB_PATH):

@@ -73,6 +73,44 @@ __global__ __launch_bounds__(256) void repack_kernel(const T* __restrict__ w, T*
   }
 }
 
+// 16-bit weights, fragment geometry rows = 16, kpl = 8 (32 input channels
+// per chunk): one workgroup per (chunk, output fragment) block.  The block's
+// 16 output channels x 32 input channels x all taps are contiguous runs of
+// w (32 * taps elements per output channel), read coalesced into LDS; each
+// thread then writes whole 16-byte lane slots (8 consecutive input channels
+// of one output channel at one tap) of the block's fragments, one 1 KiB
+// fragment per 64 threads.  Channels past Ci / Co are zeros.
+constexpr int kRepackMaxTaps = 48;
+__global__ __launch_bounds__(256) void repack_block16(const uint16_t* __restrict__ w,
+                                                      u32x4* __restrict__ wp, int64_t Ci,
+                                                      int64_t Co, int taps, int64_t chunks,
+                                                      int64_t cofrags) {
+  __shared__ uint16_t tile[16 * 32 * kRepackMaxTaps];
+  const int64_t cf = blockIdx.x % cofrags, ch = blockIdx.x / cofrags;
+  const int row = 32 * taps;  // elements of one output channel's run
+  const int64_t ci0 = ch * 32;
+  const int64_t ci_n = Ci - ci0 < 32 ? Ci - ci0 : 32;  // real input channels of the chunk
+  for (int q = threadIdx.x; q < 16 * row; q += 256) {
+    const int r = q / row, u = q - r * row;
+    const int64_t co = cf * 16 + r;
+    const bool ok = co < Co && u < ci_n * taps;
+    tile[q] = ok ? w[(co * Ci + ci0) * taps + u] : static_cast<uint16_t>(0);
+  }
+  __syncthreads();
+  // thread -> (tap t, lane L): lane L holds output channel L % 16, input
+  // channels 8 (L / 16) .. + 7
+  for (int q = threadIdx.x; q < taps * 64; q += 256) {
+    const int t = q >> 6, L = q & 63;
+    const int base = ((L & 15) * 32 + 8 * (L >> 4)) * taps + t;
+    uint32_t v[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      v[e] = static_cast<uint32_t>(tile[base + (2 * e) * taps]) |
+             (static_cast<uint32_t>(tile[base + (2 * e + 1) * taps]) << 16);
+    wp[((t * chunks + ch) * cofrags + cf) * 64 + L] = u32x4{v[0], v[1], v[2], v[3]};
+  }
+}
+
 template <typename T>
 __global__ __launch_bounds__(256) void unpack_kernel(const T* __restrict__ wp, T* __restrict__ w,
                                                      int64_t total, int64_t Ci, int64_t taps,
@@ -287,6 +325,11 @@ hipError_t launch_repack(const Geo& g, const void* w, void* wpack, hipStream_t s
     hipLaunchKernelGGL(repack_kernel<float>, dim3(blocks), dim3(256), 0, s,
                        static_cast<const float*>(w), static_cast<float*>(wpack), total, g.d.Ci,
                        g.d.Co, p.taps, p.chunks, p.cofrags, p.rows, p.kpl);
+  else if (p.rows == 16 && p.kpl == 8 && p.taps <= kRepackMaxTaps &&
+           p.chunks * p.cofrags <= 0x7fffffff && (reinterpret_cast<uintptr_t>(wpack) & 15u) == 0)
+    hipLaunchKernelGGL(repack_block16, dim3(static_cast<unsigned>(p.chunks * p.cofrags)), dim3(256),
+                       0, s, static_cast<const uint16_t*>(w), static_cast<u32x4*>(wpack), g.d.Ci,
+                       g.d.Co, static_cast<int>(p.taps), p.chunks, p.cofrags);
   else
     hipLaunchKernelGGL(repack_kernel<uint16_t>, dim3(blocks), dim3(256), 0, s,
                        static_cast<const uint16_t*>(w), static_cast<uint16_t*>(wpack), total,
@@ -348,6 +391,11 @@ hipError_t launch_fast(const Geo& g, const void* x, const void* cache, const voi
                            info);
       if (e != hipSuccess || written || info) return e;
     }
+  } else if (g.Wo <= 32) {
+    // narrow frames: 4 x 32-pixel tiles (a 64-pixel-wide tile would compute
+    // half its columns past the frame)
+    e = one ? run_fast<float, 1, 1, 1, 4, 4, 1, 1>(g, a, s, info)
+            : run_fast<float, 1, 1, 1, 4, 4, 1, 3>(g, a, s, info);
   } else {
     e = one ? run_fast<float, 1, 2, 1, 4, 4, 2, 1>(g, a, s, info)
             : run_fast<float, 1, 2, 1, 4, 4, 2, 3>(g, a, s, info);

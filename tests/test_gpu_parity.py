@@ -62,6 +62,30 @@ def _case(sp, dtype, mode=0, seed=0, ws=False, kernel=None):
 
 # ---------------------------------------------------------------- repack
 
+@pytest.mark.parametrize("Ci,Co,Kt,Kh", [(48, 80, 3, 3), (320, 160, 5, 3), (40, 21, 3, 1),
+                                         (64, 16, 2, 3), (33, 17, 6, 3), (96, 3, 1, 3)])
+def test_repack_layout_matches_its_definition(Ci, Co, Kt, Kh):
+    """bf16 packed weights against the layout written out on the host: the
+    16-byte slot of lane L in fragment (tap, chunk, output fragment) holds
+    w[16 f + L % 16][32 chunk + 8 (L / 16) + e][tap], e = 0..7, zero past Ci
+    / Co (45 and 54 taps: both sides of the block kernel's tap limit)."""
+    sp = spec(N=1, Ci=Ci, Co=Co, T=2, Tc=2, H=4, W=4, Kt=Kt, Kh=Kh, Kw=Kh)
+    say(f"repack layout {Ci}->{Co} Kt={Kt} K={Kh}")
+    ctx = c3c.Context()
+    w, _ = layer(sp, "bf16")
+    wp = c3c.weight_repack(ctx, sp, w)
+    torch.cuda.synchronize()
+    taps = Kt * Kh * Kh
+    chunks, frags = (Ci + 31) // 32, (Co + 15) // 16
+    wb = w.view(torch.int16).cpu().numpy().view(np.uint16).reshape(Co, Ci, taps)
+    pad = np.zeros((frags * 16, chunks * 32, taps), np.uint16)
+    pad[:Co, :Ci] = wb
+    # [co = 16 f + r][ci = 32 c + 8 g + e][tap] -> [tap][c][f][g][r][e]
+    want = pad.reshape(frags, 16, chunks, 4, 8, taps).transpose(5, 2, 0, 3, 1, 4)
+    got = wp.view(torch.int16).cpu().numpy().view(np.uint16).reshape(taps, chunks, frags, 4, 16, 8)
+    assert np.array_equal(got, want)
+
+
 @pytest.mark.parametrize("Ci,Co,dtype", [(48, 80, "bf16"), (384, 384, "bf16"), (3, 5, "bf16"),
                                          (32, 32, "f32"), (7, 45, "f32")])
 def test_repack_round_trip(Ci, Co, dtype):

@@ -344,7 +344,7 @@ def test_plan_of_the_workloads():
     what the library assumes without a device)."""
     from paper_2609_31938_amd.inputs import WORKLOADS
     want = {
-        "c32_32x32": ("fast_f32", 32, 4, 64, 1),
+        "c32_32x32": ("fast_f32", 32, 4, 32, 1),
         "c384_60x104": ("conv3d_bf16", 192, 4, 64, 1),
         "c192_240x416": ("conv3d_bf16", 192, 4, 64, 1),
         "c384to192_240x416": ("conv3d_bf16", 192, 4, 64, 1),
