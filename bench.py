@@ -639,6 +639,27 @@ def fused_block(workload, iters):
             c3c.conv3d_causal_cached(ctx, sp, u, cin, w, wpack, b, y, cout)
             y.add_(r)
 
+        # the normalised block form (per-pixel RMS over the channels, gain,
+        # bias, SiLU in one pass into the workspace; residual fused) against
+        # the same steps as torch ops around the plain call
+        ctx_b = c3c.Context()
+        need_b = c3c.block_workspace_bytes(sp, dtype)
+        ws_b = torch.empty((need_b + 3) // 4, dtype=torch.float32, device=dev)
+        ctx_b.set_workspace(ws_b)
+        gamma, beta = inputs.norm_inputs(sp, wl["id"], lid, dev)
+        g5, b5 = gamma[None, :, None, None, None], beta[None, :, None, None, None]
+
+        def block():
+            c3c.conv3d_causal_cached_block(ctx_b, sp, x, cin, w, wpack, b, gamma, beta, 1e-6, r,
+                                           y, cout)
+
+        def unfused_norm():
+            xf = x.float()
+            rr = torch.rsqrt(xf.square().mean(dim=1, keepdim=True) + 1e-6)
+            u = torch.nn.functional.silu(xf * rr * g5 + b5).to(w.dtype)
+            c3c.conv3d_causal_cached(ctx, sp, u, cin, w, wpack, b, y, cout)
+            y.add_(r)
+
         torch.cuda.synchronize()
         m0 = torch.cuda.memory_allocated()
         torch.cuda.reset_peak_memory_stats()
@@ -656,6 +677,8 @@ def fused_block(workload, iters):
         t_res = timed(lambda: fused(False, True), n)
         t_unf = timed(unfused, n)
         t_pass = timed(lambda: fused(c=ctx_ws), n) if need else None
+        t_block = timed(block, n)
+        t_unf_norm = timed(unfused_norm, n)
         xb, yb = x.numel() * 2, y.numel() * 2
         floor_ms = (2 * xb + 3 * yb) / (PEAK_HBM_GBS * 1e9) * 1e3
         out.append(dict(layer=lname, route=route, plain_ms=round(t_plain, 4),
@@ -664,10 +687,13 @@ def fused_block(workload, iters):
                         fused_prologue_pass_ms=round(t_pass, 4) if t_pass is not None else None,
                         prologue_pass_workspace_bytes=int(need),
                         unfused_floor_ms=round(t_plain + floor_ms, 4),
+                        block_norm_ms=round(t_block, 4), unfused_norm_torch_ms=round(t_unf_norm, 4),
+                        block_workspace_bytes=int(need_b),
                         extra_bytes_unfused=int(extra_unfused), extra_bytes_fused=int(extra_fused)))
         print(json.dumps(out[-1]), flush=True)
         ctx_ws.set_workspace(None)
-        del x, y, r, cin, cout, w, b, wpack, ws
+        ctx_b.set_workspace(None)
+        del x, y, r, cin, cout, w, b, wpack, ws, ws_b
         gc.enable()
         torch.cuda.empty_cache()
     print(json.dumps({"fused_block": workload, "layers": out}), flush=True)

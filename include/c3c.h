@@ -353,6 +353,46 @@ int c3c_conv3d_causal_cached_fused(c3c_ctx* ctx, const c3c_conv_desc* d,
                                    const float* shift, const void* residual,
                                    void* y, void* cache_out, void* stream);
 
+/* ---------------------------------------------------------------- normalised block form */
+/* The fused form with the residual block's normalisation computed inside the
+ * call instead of folded by the caller (bf16 only).  A decoder residual
+ * block normalises each pixel over its channels, applies a per-channel gain
+ * and bias and SiLU, then runs its cached causal convolution; the paper's
+ * Sec. 7 points at the temporary buffers around the lowering (buffer reuse,
+ * streamed accumulation).  Here the new chunk x becomes
+ *   u[n][ci][t][p] = RNE_bf16(SiLU(x[n][ci][t][p] * r[n][t][p] * gamma[ci] + beta[ci])),
+ *   r[n][t][p] = 1 / sqrt(mean over ci of x[n][ci][t][p]^2 + eps),
+ * in one pass over x (fp32 arithmetic, hardware reciprocal square root,
+ * exponential and reciprocal) into the first round_up(|x|, 256) bytes of the
+ * context's workspace (c3c_ctx_set_workspace).  The convolution then runs on
+ * [cache; u] exactly as c3c_conv3d_causal_cached does, with the rest of the
+ * workspace as its split-K workspace: cache frames are read as they are,
+ * cache_out receives the last L frames of [cache; u] (activated frames, as
+ * the cache of an unfused pipeline would hold), and residual (or NULL) is
+ * added after the bias, before the one rounding.
+ *
+ * gamma, beta: device fp32 [Ci].  eps: finite and >= 0.  residual: device,
+ *   [N][Co][To][Ho][Wo] bf16, or NULL; it may be y itself.
+ * Workspace: at least c3c_block_workspace_bytes(d) (the activated chunk,
+ *   then c3c_workspace_bytes); calls sharing a context's workspace must not
+ *   overlap in time.
+ * EINVAL (not counted): as c3c_conv3d_causal_cached; dtype not bf16; gamma
+ *   or beta NULL; eps negative, NaN or infinite; a context workspace smaller
+ *   than c3c_block_workspace_bytes; x, gamma or beta overlapping an output or
+ *   the workspace; residual overlapping the workspace or an output other
+ *   than y.
+ * Routing, counters and strict mode as c3c_conv3d_causal_cached; strict
+ *   rejections happen before the pass runs; a failed pass launch counts the
+ *   call as failed and returns C3C_E_DEVICE. */
+int c3c_block_workspace_bytes(const c3c_conv_desc* d, size_t* bytes);
+int c3c_conv3d_causal_cached_block(c3c_ctx* ctx, const c3c_conv_desc* d,
+                                   const void* x, const void* cache,
+                                   const void* w, const void* wpack,
+                                   const void* bias, const float* gamma,
+                                   const float* beta, float eps,
+                                   const void* residual, void* y,
+                                   void* cache_out, void* stream);
+
 /* ---------------------------------------------------------------- no allocation */
 /* For callers that cannot allocate device memory (code under HIP graph
  * capture, tight serving loops, harnesses that forbid hipMalloc): the plain

@@ -78,6 +78,8 @@ def _load():
         lib.ora_silu.argtypes = [C.c_double]
         lib.ora_silu.restype = C.c_double
         lib.ora_prologue_bf16.argtypes = [i64, i64, i64, i64, vp, vp, vp, vp]
+        lib.ora_rms_prologue_bf16.argtypes = [i64, i64, i64, i64, vp, vp, vp, C.c_double, vp,
+                                              vp]
         _lib = lib
     return _lib
 
@@ -259,9 +261,42 @@ def prologue_bf16(spec: dict, x, scale, shift) -> np.ndarray:
     return u
 
 
+def rms_prologue_bf16(spec: dict, x, gamma, beta, eps: float, with_rms: bool = False):
+    """u = RNE_bf16(SiLU(x / rms[n, t, p] * gamma[c] + beta[c])) over the new
+    chunk x (N, Ci, T, H, W) bf16 bits, rms = sqrt(mean over the Ci channels of
+    x^2 + eps) per pixel; gamma / beta fp32 (Ci,).  With ``with_rms`` also the
+    fp64 rms (N, T, H, W)."""
+    lib = _load()
+    N, Ci, T, hw = spec["N"], spec["Ci"], spec["T"], spec["H"] * spec["W"]
+    x = _host(x, "bf16")
+    g = np.ascontiguousarray(_host(gamma, "f32")).reshape(-1)
+    b = np.ascontiguousarray(_host(beta, "f32")).reshape(-1)
+    if x.size != N * Ci * T * hw or g.size != Ci or b.size != Ci:
+        raise ValueError("normalised prologue arguments have the wrong number of elements")
+    u = np.empty((N, Ci, T, spec["H"], spec["W"]), np.uint16)
+    rms = np.empty((N, T, spec["H"], spec["W"]), np.float64)
+    _check(lib.ora_rms_prologue_bf16(N, Ci, T, hw, _ptr(x), _ptr(g), _ptr(b), float(eps),
+                                     _ptr(u), _ptr(rms)), "rms_prologue_bf16")
+    return (u, rms) if with_rms else u
+
+
 def _widen_bf16(a) -> np.ndarray:
     a = _host(a, "bf16")
     return (a.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+
+
+def conv3d_block(spec: dict, x, cache, w, b, gamma, beta, eps: float, residual=None):
+    """The normalised residual-block call, bf16: the new chunk through
+    rms_prologue_bf16, the convolution on [C; u], the residual (bf16, y's
+    shape, or None) added after the bias.  Returns (y fp64, cache' bf16 bits)."""
+    u = rms_prologue_bf16(spec, x, gamma, beta, eps)
+    y = conv3d(spec, "bf16", u, cache, w, b)
+    if residual is not None:
+        r = _widen_bf16(residual)
+        if r.size != y.size:
+            raise ValueError("residual has the wrong number of elements")
+        y = y + r.reshape(y.shape)
+    return y, cache_update(spec, "bf16", u, cache)
 
 
 def conv3d_fused(spec: dict, x, cache, w, b, scale=None, shift=None, residual=None):

@@ -42,7 +42,11 @@
  * convolution in an unfused pipeline would), and a residual tensor of the
  * output's shape is added after the bias.  This file provides the rounding,
  * SiLU and the prologue; the residual sum is one fp64 addition per output,
- * done by the Python wrapper.
+ * done by the Python wrapper.  The normalised variant of the prologue
+ * replaces the folded per-(n, c) scale and shift with the block's own
+ * normalisation: each pixel's Ci channel values are divided by their root
+ * mean square (with eps inside the root), then a per-channel gain and bias
+ * apply before SiLU.
  *
  * The route rule (which calls the lowered fast route accepts) is the written
  * guard of Alg. 1 plus this library's fast-kernel contract: K_t >= 2, and
@@ -471,6 +475,37 @@ uint16_t ora_round_bf16(double v) {
 
 /* SiLU(v) = v * sigmoid(v) = v / (1 + e^{-v}), fp64. */
 double ora_silu(double v) { return v / (1.0 + exp(-v)); }
+
+/* The normalised prologue over x [N][Ci][T][hw] (bf16 bits): a per-pixel
+ * RMS normalisation over the input channels, a per-channel affine, SiLU and
+ * one rounding,
+ *   rms[n,t,p] = sqrt( (1/Ci) sum_c x[n,c,t,p]^2 + eps ),
+ *   u[n,c,t,p] = RNE_bf16( SiLU( x[n,c,t,p] / rms[n,t,p] * g[c] + b[c] ) ),
+ * all in fp64 (g, b fp32 [Ci]).  rms (optional, [N][T][hw]) receives the
+ * per-pixel root mean squares. */
+int ora_rms_prologue_bf16(int64_t N, int64_t Ci, int64_t T, int64_t hw,
+                          const uint16_t* x, const float* g, const float* b, double eps,
+                          uint16_t* u, double* rms) {
+  if (N < 0 || Ci < 0 || T < 0 || hw < 0 || !(eps >= 0.0)) return -1;
+  if (N * Ci * T * hw == 0) return 0;
+  if (!x || !g || !b || !u) return -1;
+#pragma omp parallel for schedule(static)
+  for (int64_t ntp = 0; ntp < N * T * hw; ++ntp) {
+    int64_t n = ntp / (T * hw), tp = ntp % (T * hw);
+    double ss = 0.0;
+    for (int64_t c = 0; c < Ci; ++c) {
+      double v = widen(x, ORA_BF16, (n * Ci + c) * T * hw + tp);
+      ss += v * v;
+    }
+    double r = sqrt(ss / (double)Ci + eps);
+    if (rms) rms[ntp] = r;
+    for (int64_t c = 0; c < Ci; ++c) {
+      int64_t i = (n * Ci + c) * T * hw + tp;
+      u[i] = ora_round_bf16(ora_silu(widen(x, ORA_BF16, i) / r * (double)g[c] + (double)b[c]));
+    }
+  }
+  return 0;
+}
 
 /* The fused prologue over x [N][Ci][T][hw] (bf16 bits), with per-(n, c)
  * fp32 scale s and shift t ([N][Ci]); u receives bf16 bits. */

@@ -19,7 +19,7 @@ BUILD = os.path.join(ROOT, "_build")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 SOURCES = ["c3c_host.cpp", "fast_conv.hip", "conv_bf16.hip", "conv_tap1x1.hip", "conv_head.hip",
-           "fallback.hip", "pointwise.hip", "mfma_probe.hip", "noalloc.hip"]
+           "fallback.hip", "pointwise.hip", "mfma_probe.hip", "noalloc.hip", "norm.hip"]
 COMMON = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall",
           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
           "-I", INC, "-I", CSRC]

@@ -95,6 +95,9 @@ lib.c3c_conv3d_causal_cached_fused.argtypes = [_vp, _P(Desc), _vp, _vp, _vp, _vp
                                                _vp, _vp, _vp, _vp]
 lib.c3c_conv3d_causal_cached_noalloc.argtypes = [_vp, _P(Desc), _vp, _vp, _vp, _vp, _vp, _vp,
                                                  _vp, _vp]
+lib.c3c_block_workspace_bytes.argtypes = [_P(Desc), _P(C.c_size_t)]
+lib.c3c_conv3d_causal_cached_block.argtypes = [_vp, _P(Desc), _vp, _vp, _vp, _vp, _vp, _vp, _vp,
+                                               C.c_float, _vp, _vp, _vp, _vp]
 lib.c3c_counters_get.argtypes = [_vp, _P(Counters)]
 lib.c3c_mfma_probe.argtypes = [C.c_int64, C.c_int64, _vp, _P(C.c_double), _vp]
 lib.c3c_counters_reset.argtypes = [_vp]
@@ -271,6 +274,15 @@ def fused_workspace_bytes(spec: dict, dtype: str) -> int:
     return int(n.value)
 
 
+def block_workspace_bytes(spec: dict, dtype: str = "bf16") -> int:
+    """Context workspace bytes the normalised block form needs: the activated
+    chunk (rounded up to 256 bytes), then the split-K bytes."""
+    n = C.c_size_t()
+    _raise(lib.c3c_block_workspace_bytes(C.byref(make_desc(spec, dtype)), C.byref(n)),
+           what="c3c_block_workspace_bytes")
+    return int(n.value)
+
+
 # ---------------------------------------------------------------- device calls
 
 _TORCH = {}
@@ -443,6 +455,36 @@ def conv3d_causal_cached_fused(ctx, spec: dict, x, cache, w, wpack, bias, scale=
         _ptr(scale, "scale", "f32", nc), _ptr(shift, "shift", "f32", nc),
         _ptr(residual, "residual", dtype, n["y"]), py, po, _stream(stream))
     _raise(st, ctx, "c3c_conv3d_causal_cached_fused")
+    return y, cache_out
+
+
+def conv3d_causal_cached_block(ctx, spec: dict, x, cache, w, wpack, bias, gamma, beta,
+                               eps: float, residual=None, y=None, cache_out=None, stream=None):
+    """The normalised residual-block form (bf16): the new chunk normalised per
+    pixel over its channels (RMS with eps), scaled by gamma and shifted by
+    beta (fp32, (Ci,)), through SiLU into the context's workspace (which must
+    hold block_workspace_bytes), then the convolution on [cache; u] with
+    residual (y's shape, may be ``y``) added before the rounding.  Returns
+    (y, cache_out)."""
+    import torch
+    dtype = dtype_of(w)
+    To, Ho, Wo, L = output_dims(spec, dtype)
+    dev = w.device
+    if y is None:
+        y = torch.empty((spec["N"], spec["Co"], To, Ho, Wo), dtype=w.dtype, device=dev)
+    if cache_out is None:
+        cache_out = torch.empty((spec["N"], spec["Ci"], L, spec["H"], spec["W"]),
+                                dtype=w.dtype, device=dev)
+    n = _sizes(spec, dtype)
+    _check(gamma, "gamma", "f32", spec["Ci"])
+    _check(beta, "beta", "f32", spec["Ci"])
+    _check(residual, "residual", dtype, n["y"])
+    px, pc, pw, pp, pb, py, po = _call_ptrs(spec, dtype, n, x, cache, w, wpack, bias, y, cache_out)
+    st = lib.c3c_conv3d_causal_cached_block(
+        ctx._h, C.byref(make_desc(spec, dtype)), px, pc, pw, pp, pb,
+        _ptr(gamma, "gamma", "f32", spec["Ci"]), _ptr(beta, "beta", "f32", spec["Ci"]),
+        float(eps), _ptr(residual, "residual", dtype, n["y"]), py, po, _stream(stream))
+    _raise(st, ctx, "c3c_conv3d_causal_cached_block")
     return y, cache_out
 
 

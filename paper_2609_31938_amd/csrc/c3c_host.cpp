@@ -378,12 +378,24 @@ int c3c_weight_unpack(const c3c_conv_desc* d, const void* wpack, void* w_out, vo
 
 namespace {
 
+// The normalised block form's pass, run by run_call after every check and
+// before the convolution: the new chunk src is normalised and activated into
+// the call's x (a region of the workspace).
+struct RmsPass {
+  const void* src = nullptr;
+  const float* gamma = nullptr;
+  const float* beta = nullptr;
+  float eps = 0.f;
+};
+
 // One call, plain or fused (fu: the fused form's prologue / epilogue, or none).
 // ws / ws_cap: the split-K (and prologue-pass) workspace: the context's, or
-// the library's own scratch for the allocation-free entry point.
+// the library's own scratch for the allocation-free entry point.  pre: the
+// block form's normalisation pass (writes x), or none.
 int run_call(c3c_ctx* ctx, const c3c_conv_desc* d, const void* x, const void* cache,
              const void* w, const void* wpack, const void* bias, const Fuse& fu, void* y,
-             void* cache_out, void* stream, void* ws, size_t ws_cap) {
+             void* cache_out, void* stream, void* ws, size_t ws_cap,
+             const RmsPass* pre = nullptr) {
   if (!ctx) return C3C_E_INVAL;
   Geo g;
   const char* why = make_geo(d, &g);
@@ -440,6 +452,22 @@ int run_call(c3c_ctx* ctx, const c3c_conv_desc* d, const void* x, const void* ca
   hipStream_t s = static_cast<hipStream_t>(stream);
   const bool strict = (ctx->mode & C3C_MODE_STRICT) != 0;
   ++ctx->ctr.calls;
+
+  if (pre) {
+    // strict rejections first: the pass runs only for a call that will compute
+    if (strict && (reason != C3C_REASON_NONE || (ctx->mode & C3C_MODE_INJECT_FAST_FAILURE))) {
+      ++ctx->ctr.strict_rejects;
+      return reason != C3C_REASON_NONE
+                 ? fail(ctx, C3C_E_UNSUPPORTED, "call does not route fast (strict mode)")
+                 : fail(ctx, C3C_E_INJECTED, "injected fast-route failure (strict mode)");
+    }
+    const hipError_t e = launch_rms_prologue(g, pre->src, pre->gamma, pre->beta, pre->eps,
+                                             const_cast<void*>(x), s);
+    if (e != hipSuccess) {
+      ++ctx->ctr.failed;
+      return fail(ctx, C3C_E_DEVICE, hipGetErrorString(e));
+    }
+  }
 
   int fb_reason = reason;
   if (reason == C3C_REASON_NONE) {
@@ -543,6 +571,63 @@ int c3c_conv3d_causal_cached_fused(c3c_ctx* ctx, const c3c_conv_desc* d, const v
   fu.residual = static_cast<const uint16_t*>(residual);
   return run_call(ctx, d, x, cache, w, wpack, bias, fu, y, cache_out, stream,
                   ctx ? ctx->ws : nullptr, ctx ? ctx->ws_bytes : 0);
+}
+
+int c3c_block_workspace_bytes(const c3c_conv_desc* d, size_t* bytes) {
+  Geo g;
+  if (*make_geo(d, &g) || !bytes || d->dtype != C3C_DTYPE_BF16) return C3C_E_INVAL;
+  const int64_t xb = d->N * d->Ci * d->T * d->H * d->W * 2;
+  int64_t splitk = 0;
+  if (decide(g, 0u) == C3C_REASON_NONE && spatial_3x3(*d)) splitk = fast_bf16_workspace_bytes(g);
+  *bytes = static_cast<size_t>((xb + 255) / 256 * 256 + splitk);
+  return C3C_OK;
+}
+
+int c3c_conv3d_causal_cached_block(c3c_ctx* ctx, const c3c_conv_desc* d, const void* x,
+                                   const void* cache, const void* w, const void* wpack,
+                                   const void* bias, const float* gamma, const float* beta,
+                                   float eps, const void* residual, void* y, void* cache_out,
+                                   void* stream) {
+  if (!ctx) return C3C_E_INVAL;
+  Geo g;
+  const char* why = make_geo(d, &g);
+  if (*why) return fail(ctx, C3C_E_INVAL, why);
+  if (d->dtype != C3C_DTYPE_BF16) return fail(ctx, C3C_E_INVAL, "the block form is bf16 only");
+  if (!gamma || !beta) return fail(ctx, C3C_E_INVAL, "gamma and beta must be non-NULL");
+  if (!(eps >= 0.f) || eps > 3.0e38f) return fail(ctx, C3C_E_INVAL, "eps must be finite and >= 0");
+  size_t need = 0;
+  c3c_block_workspace_bytes(d, &need);
+  if (ctx->ws_bytes < need)
+    return fail(ctx, C3C_E_INVAL,
+                "the block form needs a context workspace of " + std::to_string(need) +
+                    " bytes (c3c_block_workspace_bytes); it has " + std::to_string(ctx->ws_bytes));
+  const int64_t hw = d->H * d->W;
+  const int64_t xb = d->N * d->Ci * d->T * hw * 2;
+  const int64_t ub = (xb + 255) / 256 * 256;
+  if (xb > 0 && !x) return fail(ctx, C3C_E_INVAL, "x is NULL");
+  // the activated chunk takes the workspace's first ub bytes; the rest is the
+  // split-K workspace of the convolution that follows
+  unsigned char* u = static_cast<unsigned char*>(ctx->ws);
+  const int64_t yb = d->N * d->Co * g.To * g.Ho * g.Wo * 2;
+  const int64_t ob = d->N * d->Ci * g.L * hw * 2;
+  const int64_t gb = d->Ci * 4;
+  const int64_t wsb = static_cast<int64_t>(ctx->ws_bytes);
+  if (overlap(x, xb, ctx->ws, wsb) || overlap(x, xb, y, yb) || overlap(x, xb, cache_out, ob))
+    return fail(ctx, C3C_E_INVAL, "x overlaps an output or the workspace");
+  for (const void* p : {static_cast<const void*>(gamma), static_cast<const void*>(beta)})
+    if (overlap(p, gb, ctx->ws, wsb) || overlap(p, gb, y, yb) || overlap(p, gb, cache_out, ob))
+      return fail(ctx, C3C_E_INVAL, "gamma or beta overlaps an output or the workspace");
+  if (overlap(residual, yb, ctx->ws, wsb))
+    return fail(ctx, C3C_E_INVAL, "residual overlaps the workspace");
+  Fuse fu;
+  fu.residual = static_cast<const uint16_t*>(residual);
+  RmsPass pre;
+  pre.src = x;
+  pre.gamma = gamma;
+  pre.beta = beta;
+  pre.eps = eps;
+  return run_call(ctx, d, u, cache, w, wpack, bias, fu, y, cache_out, stream, u + ub,
+                  static_cast<size_t>(wsb - ub), &pre);
 }
 
 int c3c_counters_get(const c3c_ctx* ctx, c3c_counters* out) {

@@ -126,6 +126,10 @@ hipError_t launch_prologue(const Geo& g, const void* x, const float* scale, cons
                            void* u, hipStream_t s);
 hipError_t launch_cache_copy(const Geo& g, const void* x, const void* cache, void* cache_out,
                              hipStream_t s, const Fuse& fu = Fuse{});
+// the normalised block form's pass (norm.hip): u = RNE_bf16(SiLU(x * r * gamma
+// + beta)), r the per-pixel reciprocal root mean square over the channels
+hipError_t launch_rms_prologue(const Geo& g, const void* x, const float* gamma, const float* beta,
+                               float eps, void* u, hipStream_t s);
 // The allocation-free entry point's split-K scratch (noalloc.hip): a
 // file-scope device array of kNoallocScratchBytes; *ptr receives its address
 // on the current device (looked up once per device).

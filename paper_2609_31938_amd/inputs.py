@@ -9,7 +9,8 @@ Distributions (the decoder-layer stand-ins; no model weights are used):
 drawn in fp32 and rounded to nearest-even into the call's dtype.  The fused
 form's extra operands: scale ~ 1 + N(0, 0.2^2) and shift ~ N(0, 0.5^2) per
 (batch element, input channel), fp32 (a folded normalisation's scale and
-shift), and a residual ~ N(0, 1) shaped like the output.  Each tensor
+shift), and a residual ~ N(0, 1) shaped like the output; the normalised block
+form's gain ~ 1 + N(0, 0.2^2) and bias ~ N(0, 0.5^2) per input channel.  Each tensor
 has its own seed, derived from (workload, layer, tensor, chunk); weights and
 bias use chunk 0 so that a layer keeps its weights over a stream.
 """
@@ -22,6 +23,7 @@ import numpy as np
 
 TENSOR_X, TENSOR_W, TENSOR_B = 0, 1, 2
 TENSOR_SCALE, TENSOR_SHIFT, TENSOR_RES = 3, 4, 5
+TENSOR_GAMMA, TENSOR_BETA = 6, 7
 
 
 def spec(N=1, Ci=1, Co=1, T=1, Tc=0, H=1, W=1, Kt=3, Kh=3, Kw=3,
@@ -92,6 +94,15 @@ def affine_inputs(sp: dict, workload: int, layer: int, chunk: int, device="cpu")
     scale.add_(1.0)
     shift = randn(shape, seed_of(workload, layer, TENSOR_SHIFT, chunk), 0.5, "f32", device)
     return scale, shift
+
+
+def norm_inputs(sp: dict, workload: int, layer: int, device="cpu"):
+    """(gamma, beta), fp32 (Ci,): 1 + N(0, 0.04) and N(0, 0.25), the
+    normalised block form's per-channel gain and bias (a layer's own, chunk 0)."""
+    gamma = randn((sp["Ci"],), seed_of(workload, layer, TENSOR_GAMMA, 0), 0.2, "f32", device)
+    gamma.add_(1.0)
+    beta = randn((sp["Ci"],), seed_of(workload, layer, TENSOR_BETA, 0), 0.5, "f32", device)
+    return gamma, beta
 
 
 def residual_input(shape, dtype: str, workload: int, layer: int, chunk: int, device="cpu"):

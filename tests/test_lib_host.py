@@ -35,7 +35,8 @@ def test_every_declared_symbol_is_exported():
         "c3c_fallback_shapes", "c3c_strerror", "c3c_last_error",
         "c3c_workspace_bytes", "c3c_ctx_set_workspace", "c3c_conv3d_causal_cached_fused",
         "c3c_mfma_probe", "c3c_fused_workspace_bytes", "c3c_plan_query",
-        "c3c_conv3d_causal_cached_noalloc"])
+        "c3c_conv3d_causal_cached_noalloc", "c3c_block_workspace_bytes",
+        "c3c_conv3d_causal_cached_block"])
     for n in names:
         assert hasattr(c3c.lib, n), n
 
@@ -464,3 +465,66 @@ def test_noalloc_refuses_an_oversized_split_before_device_work():
     assert f(ctx._h, C.byref(d), p["x"], p["cache"], p["w"], p["wpack"], p["b"], p["y"], p["co"],
              None) == c3c.E_DEVICE
     assert ctx.counters()["failed"] == 1
+
+
+# ---------------------------------------------------------------- normalised block form
+def _block(ctx, sp, dtype="bf16", gamma=0x11000000, beta=0x12000000, eps=1e-6, res=None, **over):
+    p = dict(FAKE)
+    p.update(over)
+    return c3c.lib.c3c_conv3d_causal_cached_block(
+        ctx._h if ctx else None, C.byref(c3c.make_desc(sp, dtype)), p["x"], p["cache"], p["w"],
+        p["wpack"], p["b"], gamma, beta, eps, res, p["y"], p["co"], None)
+
+
+def test_block_workspace_bytes_closed_form():
+    for Ci, Co, T, H, W in [(384, 192, 4, 240, 416), (3, 5, 1, 7, 9), (384, 384, 1, 60, 104)]:
+        sp = spec(N=1, Ci=Ci, Co=Co, T=T, Tc=2, H=H, W=W)
+        xb = Ci * T * H * W * 2
+        want = -(-xb // 256) * 256 + c3c.workspace_bytes(sp, "bf16")
+        assert c3c.block_workspace_bytes(sp) == want
+    # the 1x1x1 shortcut (fallback route): the activated chunk only
+    sc = spec(N=1, Ci=32, Co=16, T=4, Tc=0, H=8, W=8, Kt=1, Kh=1, Kw=1)
+    assert c3c.block_workspace_bytes(sc) == 32 * 4 * 64 * 2
+    with pytest.raises(c3c.C3CError):
+        c3c.block_workspace_bytes(sc, "f32")
+
+
+@no_gpu
+def test_block_call_argument_errors_are_not_counted():
+    sp = spec(N=1, Ci=4, Co=4, T=2, Tc=2, H=8, W=8)
+    ctx = c3c.Context()
+    # no workspace
+    assert _block(ctx, sp) == c3c.E_INVAL and "workspace" in ctx.last_error
+    need = c3c.block_workspace_bytes(sp)
+    assert c3c.lib.c3c_ctx_set_workspace(ctx._h, 0x80000000, need - 16) == c3c.OK
+    assert _block(ctx, sp) == c3c.E_INVAL                       # one slot short
+    assert c3c.lib.c3c_ctx_set_workspace(ctx._h, 0x80000000, need) == c3c.OK
+    assert _block(ctx, sp, gamma=None) == c3c.E_INVAL
+    assert _block(ctx, sp, beta=None) == c3c.E_INVAL
+    assert _block(ctx, sp, eps=-1.0) == c3c.E_INVAL
+    assert _block(ctx, sp, eps=float("nan")) == c3c.E_INVAL
+    assert _block(ctx, sp, eps=float("inf")) == c3c.E_INVAL
+    assert _block(ctx, sp, "f32") == c3c.E_INVAL
+    assert _block(ctx, sp, x=0x80000000 + 64) == c3c.E_INVAL    # x inside the workspace
+    assert _block(ctx, sp, gamma=FAKE["y"]) == c3c.E_INVAL      # gamma overlapping y
+    assert _block(ctx, sp, res=0x80000000) == c3c.E_INVAL       # residual in the workspace
+    assert _block(ctx, sp, y=FAKE["x"]) == c3c.E_INVAL
+    assert _block(None, sp) == c3c.E_INVAL
+    assert ctx.counters()["calls"] == 0
+
+
+@no_gpu
+def test_block_call_strict_rejection_runs_no_pass():
+    """A strict call that does not route fast is rejected before the
+    normalisation pass: no device work (a launch would fail on this host and
+    count the call as failed instead)."""
+    sc = spec(N=1, Ci=4, Co=4, T=2, Tc=0, H=8, W=8, Kt=1, Kh=1, Kw=1)
+    ctx = c3c.Context(c3c.MODE_STRICT)
+    assert c3c.lib.c3c_ctx_set_workspace(ctx._h, 0x80000000, c3c.block_workspace_bytes(sc)) == c3c.OK
+    assert _block(ctx, sc, cache=None, co=None, wpack=None) == c3c.E_UNSUPPORTED
+    ctx.mode = c3c.MODE_STRICT | c3c.MODE_INJECT_FAST_FAILURE
+    sp = spec(N=1, Ci=4, Co=4, T=2, Tc=2, H=8, W=8)
+    assert c3c.lib.c3c_ctx_set_workspace(ctx._h, 0x80000000, c3c.block_workspace_bytes(sp)) == c3c.OK
+    assert _block(ctx, sp) == c3c.E_INJECTED
+    c = ctx.counters()
+    assert (c["calls"], c["strict_rejects"], c["failed"], c["fast"], c["fallback"]) == (2, 2, 0, 0, 0)

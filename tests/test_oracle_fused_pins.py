@@ -210,3 +210,134 @@ def test_fused_residual_is_added_once_and_plain_call_is_the_conv():
     assert np.array_equal(cp, O.cache_update(sp, "bf16", x, cache))
     with pytest.raises(ValueError):
         O.conv3d_fused(sp, x, cache, w, b, sc, None)
+
+
+# ---------------------------------------------------------------- normalised prologue
+# u = RNE_bf16(SiLU(x / rms * gamma[c] + beta[c])), rms = sqrt(mean_c x^2 + eps)
+# per pixel (n, t, p).  Pinned by reduction to the affine prologue (pinned
+# above), exact invariances, locality, and closed forms built from the
+# rounding and SiLU pinned above.
+
+def _bf16_bits(v):
+    return O.round_bf16(np.asarray(v, np.float64))
+
+
+def _unit_rms_chunk(rng, N, Ci, T, H, W):
+    """bf16 chunks whose every pixel has mean square exactly 1 over the
+    channels: signed, permuted copies of a fixed vector."""
+    base = {1: [1.0], 2: [1.0, 1.0], 3: [1.0, 1.0, 1.0], 5: [2.0, 1.0, 0.0, 0.0, 0.0],
+            8: [2.0, 1.0, 1.0, 1.0, 1.0, 0.0, 0.0, 0.0]}[Ci]
+    x = np.empty((N, Ci, T, H, W))
+    for n in range(N):
+        for t in range(T):
+            for h in range(H):
+                for w in range(W):
+                    v = rng.permutation(base) * rng.choice([-1.0, 1.0], Ci)
+                    x[n, :, t, h, w] = v
+    assert np.allclose((x ** 2).mean(axis=1), 1.0)
+    return _bf16_bits(x)
+
+
+@pytest.mark.parametrize("Ci", [1, 2, 3, 5, 8])
+def test_rms_prologue_reduces_to_the_affine_prologue_at_unit_rms(Ci):
+    rng = np.random.default_rng(700 + Ci)
+    sp = dict(N=2, Ci=Ci, T=2, H=3, W=4)
+    x = _unit_rms_chunk(rng, 2, Ci, 2, 3, 4)
+    g = rng.normal(1.0, 0.5, Ci).astype(np.float32)
+    b = rng.normal(0.0, 0.5, Ci).astype(np.float32)
+    u, rms = O.rms_prologue_bf16(sp, x, g, b, 0.0, with_rms=True)
+    assert np.array_equal(rms, np.ones_like(rms))
+    # the same per-channel gain and bias for every batch element
+    want = O.prologue_bf16(sp, x, np.tile(g, (2, 1)), np.tile(b, (2, 1)))
+    assert np.array_equal(u, want)
+
+
+def test_rms_prologue_is_invariant_to_a_power_of_two_scale_of_each_pixel():
+    rng = np.random.default_rng(711)
+    sp = dict(N=2, Ci=7, T=3, H=4, W=5)
+    x = _bf16_bits(rng.normal(0, 1, (2, 7, 3, 4, 5)))
+    k = rng.integers(-3, 4, (2, 1, 3, 4, 5)).astype(np.float64)
+    xs = _bf16_bits(bf16_to_f64(x) * 2.0 ** k)  # exact: a power of two per pixel
+    g = rng.normal(1.0, 0.3, 7).astype(np.float32)
+    b = rng.normal(0.0, 0.3, 7).astype(np.float32)
+    u0, r0 = O.rms_prologue_bf16(sp, x, g, b, 0.0, with_rms=True)
+    u1, r1 = O.rms_prologue_bf16(sp, xs, g, b, 0.0, with_rms=True)
+    assert np.array_equal(u0, u1)
+    assert np.allclose(r1, r0 * 2.0 ** k[:, 0], rtol=1e-15)
+
+
+def test_rms_prologue_is_local_to_each_pixel():
+    rng = np.random.default_rng(712)
+    sp = dict(N=2, Ci=6, T=3, H=4, W=5)
+    x = _bf16_bits(rng.normal(0, 1, (2, 6, 3, 4, 5)))
+    g = rng.normal(1.0, 0.3, 6).astype(np.float32)
+    b = rng.normal(0.0, 0.3, 6).astype(np.float32)
+    u0 = O.rms_prologue_bf16(sp, x, g, b, 1e-6)
+    x2 = x.copy()
+    x2[1, :, 2, 3, 1] = _bf16_bits(rng.normal(0, 3, 6))
+    u1 = O.rms_prologue_bf16(sp, x2, g, b, 1e-6)
+    diff = np.any(u0 != u1, axis=1)  # (N, T, H, W): pixels whose u changed
+    assert diff[1, 2, 3, 1] and diff.sum() == 1
+
+
+def test_rms_prologue_closed_forms():
+    sp = dict(N=1, Ci=2, T=1, H=1, W=1)
+    g = np.array([1.0, 1.0], np.float32)
+    b = np.zeros(2, np.float32)
+    # (3, 4): rms = sqrt(12.5)
+    x = _bf16_bits(np.array([3.0, 4.0]).reshape(1, 2, 1, 1, 1))
+    u, rms = O.rms_prologue_bf16(sp, x, g, b, 0.0, with_rms=True)
+    assert rms.item() == math.sqrt(12.5)
+    assert np.array_equal(u.ravel(), _bf16_bits([O.silu(np.array([3.0 / math.sqrt(12.5)]))[0],
+                                                 O.silu(np.array([4.0 / math.sqrt(12.5)]))[0]]))
+    # eps inside the root: x = (1, 1), eps = 3 -> rms = 2, x / rms = 1/2
+    x = _bf16_bits(np.ones((1, 2, 1, 1, 1)))
+    g2 = np.array([2.0, -6.0], np.float32)
+    b2 = np.array([0.25, 0.5], np.float32)
+    u, rms = O.rms_prologue_bf16(sp, x, g2, b2, 3.0, with_rms=True)
+    assert rms.item() == 2.0
+    assert np.array_equal(u.ravel(), _bf16_bits(O.silu(np.array([0.5 * 2.0 + 0.25,
+                                                                 0.5 * -6.0 + 0.5]))))
+    # a zero pixel: u = SiLU(beta) for any eps > 0
+    x = np.zeros((1, 2, 1, 1, 1), np.uint16)
+    u = O.rms_prologue_bf16(sp, x, g2, b2, 1e-5)
+    assert np.array_equal(u.ravel(), _bf16_bits(O.silu(b2.astype(np.float64))))
+
+
+def test_block_call_equals_the_affine_fused_call_at_unit_rms():
+    """With every pixel at unit RMS and eps = 0 the normalised block call is
+    the affine fused call with scale = gamma, shift = beta (output, cache')."""
+    rng = np.random.default_rng(720)
+    sp = dict(N=1, Ci=5, Co=6, T=3, Tc=2, H=5, W=6, Kt=3, Kh=3, Kw=3, s_t=1, s_h=1, s_w=1,
+              d_t=1, d_h=1, d_w=1, p_base=2, p_r=0, p_h=1, p_w=1, groups=1, has_bias=1)
+    x = _unit_rms_chunk(rng, 1, 5, 3, 5, 6)
+    cache = _bf16_bits(rng.normal(0, 1, (1, 5, 2, 5, 6)))
+    w = _bf16_bits(rng.normal(0, 0.2, (6, 5, 3, 3, 3)))
+    bias = _bf16_bits(rng.normal(0, 0.3, 6))
+    res = _bf16_bits(rng.normal(0, 1, (1, 6, 3, 5, 6)))
+    g = rng.normal(1.0, 0.3, 5).astype(np.float32)
+    b = rng.normal(0.0, 0.3, 5).astype(np.float32)
+    y1, c1 = O.conv3d_block(sp, x, cache, w, bias, g, b, 0.0, res)
+    y2, c2 = O.conv3d_fused(sp, x, cache, w, bias, g[None, :], b[None, :], res)
+    assert np.array_equal(y1, y2) and np.array_equal(c1, c2)
+
+
+def test_block_call_streams_like_one_whole_sequence():
+    """The normalisation is local to each frame, so chunked streaming with
+    the carried (activated) cache equals one call over the whole sequence."""
+    rng = np.random.default_rng(721)
+    base = dict(N=1, Ci=4, Co=3, Tc=0, H=4, W=5, Kt=3, Kh=3, Kw=3, s_t=1, s_h=1, s_w=1,
+                d_t=1, d_h=1, d_w=1, p_base=2, p_r=0, p_h=1, p_w=1, groups=1, has_bias=1)
+    xs = _bf16_bits(rng.normal(0, 1, (1, 4, 6, 4, 5)))
+    w = _bf16_bits(rng.normal(0, 0.2, (3, 4, 3, 3, 3)))
+    bias = _bf16_bits(rng.normal(0, 0.3, 3))
+    g = rng.normal(1.0, 0.3, 4).astype(np.float32)
+    b = rng.normal(0.0, 0.3, 4).astype(np.float32)
+    whole, _ = O.conv3d_block(dict(base, T=6), xs, None, w, bias, g, b, 1e-6)
+    cache, outs = None, []
+    for t0, t1 in ((0, 2), (2, 3), (3, 6)):
+        sp = dict(base, T=t1 - t0, Tc=0 if cache is None else cache.shape[2])
+        y, cache = O.conv3d_block(sp, np.ascontiguousarray(xs[:, :, t0:t1]), cache, w, bias,
+                                  g, b, 1e-6)
+        outs.append(y)
+    assert np.array_equal(np.concatenate(outs, axis=2), whole)

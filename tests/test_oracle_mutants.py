@@ -6,7 +6,9 @@ cache and chunk frames swapped, the bias added per tap, a transposed weight
 index, the wrong effective left pad of Eq. 3, the wrong cache rule, a wrong
 spatial pad sign, an off-by-one in Eq. 4, a missing route clause; in the
 fused form's parts, bf16 ties rounded away from zero, one significand bit
-short, the sign of SiLU's exponent, the shift of the wrong channel).  The copy
+short, the sign of SiLU's exponent, the shift of the wrong channel; in the
+normalised prologue, the sum of squares instead of their mean, eps outside
+the root, no root, one channel left out, the gain of the wrong channel).  The copy
 is compiled to a temporary library and the pin suite is run against it in a
 child process; every mutant must make the suite fail.  Nothing here touches
 the HIP library or the GPU.
@@ -47,6 +49,14 @@ MUTANTS = {
     "silu_sign": [("return v / (1.0 + exp(-v));", "return v / (1.0 + exp(v));")],
     "prologue_shift_of_next_channel": [("double sc = (double)s[nc], sh = (double)t[nc];",
                                         "double sc = (double)s[nc], sh = (double)t[(nc + 1) % (N * Ci)];")],
+    # the normalised prologue
+    "rms_sum_not_mean": [("double r = sqrt(ss / (double)Ci + eps);", "double r = sqrt(ss + eps);")],
+    "rms_eps_outside_root": [("double r = sqrt(ss / (double)Ci + eps);",
+                              "double r = sqrt(ss / (double)Ci) + eps;")],
+    "rms_without_root": [("double r = sqrt(ss / (double)Ci + eps);", "double r = ss / (double)Ci + eps;")],
+    "rms_over_one_channel_short": [("    for (int64_t c = 0; c < Ci; ++c) {\n      double v = widen(x, ORA_BF16, (n * Ci + c) * T * hw + tp);",
+                                    "    for (int64_t c = 0; c + 1 < Ci; ++c) {\n      double v = widen(x, ORA_BF16, (n * Ci + c) * T * hw + tp);")],
+    "rms_gain_of_next_channel": [("/ r * (double)g[c] + (double)b[c]", "/ r * (double)g[(c + 1) % Ci] + (double)b[c]")],
 }
 PIN_FILES = ["test_oracle_pins.py", "test_oracle_fused_pins.py"]
 
