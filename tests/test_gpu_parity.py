@@ -120,6 +120,8 @@ FAST_CASES = [
     ("bf16", dict(N=2, Ci=40, Co=181, T=2, Tc=1, H=9, W=83)),
     ("bf16", dict(N=1, Ci=48, Co=320, T=2, Tc=2, H=10, W=88)),
     ("bf16", dict(N=1, Ci=40, Co=150, T=4, Tc=2, H=333, W=30)),
+    # the 128-channel 4x80 tile: two exact channel tiles, ragged rows and columns
+    ("bf16", dict(N=1, Ci=40, Co=256, T=2, Tc=2, H=9, W=90)),
     ("bf16", dict(N=1, Ci=8, Co=8, T=5, Tc=4, H=6, W=40, d_t=2, p_base=4)),  # temporal dilation
     ("bf16", dict(N=1, Ci=20, Co=36, T=2, Tc=2, H=7, W=9, Kt=5, p_base=4)),  # Kt = 5
     ("bf16", dict(N=1, Ci=12, Co=20, T=3, Tc=2, H=6, W=35, p_r=1)),          # right pad
