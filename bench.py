@@ -176,6 +176,7 @@ def main():
     # the matrix cores' sustained rate on this machine (outside the timed regions):
     # back-to-back bf16 products, four workgroups per compute unit
     probe = mfma_probe_rate()
+    hbm = hbm_reference()
     if roofline["bound"] == "mfma" and dtype == "bf16":
         roofline["frac_of_probe"] = round(achieved / probe["tflops"], 4)
 
@@ -200,6 +201,7 @@ def main():
         "roofline": roofline,
         "configs": configs,
         "mfma_probe": probe,
+        "hbm_reference": hbm,
         "counters": counters,
         "wall_s": round(t_wall, 4),
         "provenance": provenance(digests),
@@ -572,6 +574,34 @@ def mfma_probe_rate(iters=50000):
             "launch": f"{4 * cus} workgroups x 4 waves, 8 chains, {iters} iterations",
             "tflops_one_wave_per_simd": round(tf1, 1),
             "finite": fin and fin1}
+
+
+def hbm_reference():
+    """What plain device streams reach on this machine (outside the timed
+    regions): torch's copy of 1 GiB (read + write) and fill of 1 GiB (write),
+    the practical ceiling for the HBM-bound kernels next to the published
+    8 TB/s."""
+    import torch
+    n = 512 * 1024 * 1024
+    a = torch.ones(n, device="cuda", dtype=torch.bfloat16)
+    b = torch.empty_like(a)
+
+    def rate(fn, nbytes, k=10):
+        fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(k):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return round(nbytes / (e0.elapsed_time(e1) / k * 1e-3) / 1e9, 1)
+
+    out = {"copy_GBps": rate(lambda: b.copy_(a), 2 * a.numel() * 2),
+           "fill_GBps": rate(lambda: b.fill_(0.5), a.numel() * 2), "bytes": a.numel() * 2}
+    del a, b
+    torch.cuda.empty_cache()
+    return out
 
 
 def fused_block(workload, iters):

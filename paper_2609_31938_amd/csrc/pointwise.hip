@@ -399,6 +399,171 @@ __global__ __launch_bounds__(PW_NT, 1) void pointwise_conv(PwArgs a) {
   }
 }
 
+// 1x1x1 calls (the fallback route's pointwise form, unfused) whose whole
+// weight matrix fits in LDS: Co <= 160 (one output-channel tile) and at most
+// kResidentChunks 32-channel chunks.  The workgroups are persistent (at most
+// one per compute unit) and walk the (frame, 256-pixel tile) pairs with a
+// grid stride.  Each loads the weights once, as 1 KiB matrix-core fragments
+// (fragment (chunk c, output fragment f) in slot 10 c + f; lane l holds
+// w[16 f + l % 16][32 c + 8 (l / 16) .. + 7], zeros past Co / Ci), so the
+// stage loop fetches activations only, from HBM, through a ring of PD
+// register sets that runs on across tile boundaries: the loads of the next
+// tile's first chunks are in flight while a tile finishes and its outputs
+// are stored.  The activation stage, its transposing LDS read and the
+// epilogue are those of pointwise_conv.
+constexpr int kResidentChunks = 11;
+constexpr int PW_RES_W = 10 * 1024 * kResidentChunks;  // resident weight bytes (max)
+
+template <bool F16, int PD>
+__global__ __launch_bounds__(PW_NT, 1) void pointwise_resident(PwArgs a, int tiles_total) {
+  constexpr int NPF = 4, PX = pw_px(NPF), PITCH = pw_pitch(NPF), SEG = PX / 128;
+  constexpr int ABUF = pw_row(NPF, PW_K);  // one activation stage
+  __shared__ __align__(16) unsigned char lds[PW_RES_W + 2 * ABUF];
+  constexpr uint32_t OOB = 0x80000000u;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wco = wave & 1, wpx = wave >> 1;
+  const int chunks = a.chunks;
+
+  // ---- the weights, once
+  {
+    const __amdgpu_buffer_rsrc_t wrs = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t*>(a.w), 0, static_cast<int>(a.w_bytes), 0x00020000);
+    for (int q = tid; q < chunks * 10 * 64; q += PW_NT) {
+      const int l = q & 63, frag = q >> 6, c = frag / 10, f = frag % 10;
+      const int co = 16 * f + (l & 15), ci = 32 * c + 8 * (l >> 4);
+      const bool ok = co < a.Co && ci < a.Ci;  // Ci % 8 == 0: a slot is all in or all out
+      *reinterpret_cast<u32x4*>(lds + q * 16) = __builtin_bit_cast(
+          u32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                     wrs, ok ? static_cast<uint32_t>(co * a.Ci + ci) * 2u : OOB, 0, 0));
+    }
+  }
+
+  // ---- this workgroup's tiles: t = blockIdx.x + k gridDim.x; tile t is
+  // (batch element, output frame, 256-pixel tile) with the pixel tile fastest
+  const int ntile = (tiles_total - static_cast<int>(blockIdx.x) + static_cast<int>(gridDim.x) - 1) /
+                    static_cast<int>(gridDim.x);
+  const int nst = ntile * chunks;  // stages: tile outer, chunk inner
+  const int64_t cs_x = static_cast<int64_t>(a.T) * a.hw, cs_c = static_cast<int64_t>(a.Tc) * a.hw;
+  struct Src {
+    __amdgpu_buffer_rsrc_t rs;
+    uint32_t cs;
+  };
+  // stage g: tile blockIdx.x + (g / chunks) gridDim.x, chunk g % chunks;
+  // past the last stage, and for an output frame whose one tap reads no
+  // frame of Z (Eq. 4: a left pad past the cache, or a right pad), an
+  // empty resource (zeros: the output is the bias alone)
+  auto src_of = [&](int g) {
+    const bool real = g < nst;
+    const int t = static_cast<int>(blockIdx.x) + (real ? g / chunks : 0) * static_cast<int>(gridDim.x);
+    const int c0 = (real ? g % chunks : 0) * PW_K;
+    const int pt = t % a.px_tiles, nt = t / a.px_tiles;
+    const int o = nt % a.To, n = nt / a.To;
+    const int f = o * a.st - a.p_l;  // Kt = 1: the one tap's source frame
+    const bool active = real && f >= 0 && f < a.Z;
+    const bool in_cache = active && f < a.Tc;
+    const int64_t cstride = in_cache ? cs_c : cs_x;
+    const uint16_t* base = in_cache ? a.cache : a.x;
+    const int64_t px0 = static_cast<int64_t>(pt) * PX;
+    const int64_t off = active ? static_cast<int64_t>(in_cache ? f : f - a.Tc) * a.hw +
+                                     static_cast<int64_t>(n) * a.Ci * cstride + px0 + c0 * cstride
+                               : 0;
+    int64_t bytes = ((a.Ci - 1 - c0) * cstride + a.hw - px0) * 2;
+    if (!active || bytes < 0) bytes = 0;
+    if (bytes > 0x7fffffff) bytes = 0x7fffffff;
+    Src r;
+    r.rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(base + off), 0,
+                                             static_cast<int>(bytes), 0x00020000);
+    r.cs = static_cast<uint32_t>(cstride * 2);
+    return r;
+  };
+  const int sch = tid >> 4, spx = (tid & 15) * 8;
+  const int slds = pw_row(NPF, sch) + spx * 2;
+  auto load = [&](int g, u32x4 (&x)[SEG]) {
+    const Src sr = src_of(g);
+    const uint32_t soff = static_cast<uint32_t>(sch) * sr.cs + static_cast<uint32_t>(spx) * 2u;
+#pragma unroll
+    for (int h = 0; h < SEG; ++h)
+      x[h] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(sr.rs, soff + 256u * h, 0, 0));
+  };
+  auto store = [&](const u32x4 (&x)[SEG], int buf) {
+#pragma unroll
+    for (int h = 0; h < SEG; ++h)
+      *reinterpret_cast<u32x4*>(lds + PW_RES_W + buf * ABUF + slds + 256 * h) = x[h];
+  };
+  const int j = lane & 15, gq = lane >> 4;
+  const int ra = pw_row(NPF, 8 * gq + (j >> 2)) + (wpx * 16 * NPF + 4 * (j & 3)) * 2;
+  auto read_a = [&](int buf, int pf) {
+    const unsigned char* p = lds + PW_RES_W + buf * ABUF + ra + pf * 32;
+    const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p));
+    const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p + 4 * PITCH));
+    return i16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+  };
+  auto read_b = [&](int c, int cf) {
+    return *reinterpret_cast<const u32x4*>(lds + ((c * 10 + wco * PW_WCO + cf) * 64 + lane) * 16);
+  };
+
+  f32x4 acc[PW_WCO][NPF];
+#pragma unroll
+  for (int cf = 0; cf < PW_WCO; ++cf)
+#pragma unroll
+    for (int pf = 0; pf < NPF; ++pf) acc[cf][pf] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  u32x4 ring[PD][SEG];
+#pragma unroll
+  for (int u = 0; u < PD; ++u) load(u, ring[u]);
+  const int padded = (nst + PD - 1) / PD * PD;
+  for (int g0 = 0; g0 < padded; g0 += PD) {
+#pragma unroll
+    for (int u = 0; u < PD; ++u) {
+      const int g = g0 + u, buf = g & 1;
+      // buffer `buf` was last read while computing stage g - 2, which every
+      // wave finished before the barrier of stage g - 1
+      store(ring[u], buf);
+      load(g + PD, ring[u]);
+      __syncthreads();
+      const int c = g % chunks;
+      i16x8 av[NPF];
+      u32x4 bv[PW_WCO];
+#pragma unroll
+      for (int pf = 0; pf < NPF; ++pf) av[pf] = read_a(buf, pf);
+#pragma unroll
+      for (int cf = 0; cf < PW_WCO; ++cf) bv[cf] = read_b(c, cf);
+#pragma unroll
+      for (int pf = 0; pf < NPF; ++pf)
+#pragma unroll
+        for (int cf = 0; cf < PW_WCO; ++cf) acc[cf][pf] = mma<F16>(av[pf], bv[cf], acc[cf][pf]);
+      // the tile's last chunk: bias once, one rounding, NCTHW store; the
+      // accumulators start again from zero (workgroup-uniform branch)
+      if (c == chunks - 1 && g < nst) {
+        const int t = static_cast<int>(blockIdx.x) + (g / chunks) * static_cast<int>(gridDim.x);
+        const int pt = t % a.px_tiles, nt = t / a.px_tiles;
+        const int o = nt % a.To, n = nt / a.To;
+        uint16_t* ybase = a.y + (static_cast<int64_t>(n) * a.Co * a.To + o) * a.hw;
+#pragma unroll
+        for (int cf = 0; cf < PW_WCO; ++cf) {
+          const int co = wco * 16 * PW_WCO + 16 * cf + j;
+          const float bb = (a.has_bias && co < a.Co) ? from_b16(a.bias[co], F16) : 0.f;
+          uint16_t* yrow = ybase + static_cast<int64_t>(co) * a.To * a.hw;
+#pragma unroll
+          for (int pf = 0; pf < NPF; ++pf) {
+            const int64_t p = static_cast<int64_t>(pt) * PX + wpx * 16 * NPF + pf * 16 + 4 * gq;
+            if (co < a.Co && p < a.hw) {  // hw % 8 == 0: four pixels all in or all out
+              uint16_t v[4];
+#pragma unroll
+              for (int r = 0; r < 4; ++r)
+                v[r] = F16 ? to_f16(acc[cf][pf][r] + bb) : to_bf16(acc[cf][pf][r] + bb);
+              *reinterpret_cast<uint2*>(yrow + p) =
+                  make_uint2(v[0] | (static_cast<uint32_t>(v[1]) << 16), v[2] | (static_cast<uint32_t>(v[3]) << 16));
+            }
+            acc[cf][pf] = f32x4{0.f, 0.f, 0.f, 0.f};
+          }
+        }
+      }
+    }
+  }
+}
+
 bool aligned(const void* p, uintptr_t m) { return (reinterpret_cast<uintptr_t>(p) & (m - 1)) == 0; }
 
 }  // namespace
@@ -529,6 +694,34 @@ hipError_t launch_pointwise(const Geo& g, const void* x, const void* cache, cons
                             const void* bias, void* y, hipStream_t s, const Fuse& fu,
                             LaunchInfo* info) {
   PwArgs a = common_args(g, x, cache, bias, y);
+  // unfused calls whose weights fit in LDS: the persistent resident-weight kernel
+  if (!fu.any() && g.d.Co <= PW_CO && a.chunks <= kResidentChunks && g.d.N * g.To > 0) {
+    a.w = static_cast<const uint16_t*>(w);
+    a.w_bytes = static_cast<uint32_t>(g.d.Co * g.d.Ci * 2);
+    a.cofrags = 0;
+    a.co_tiles = 1;
+    a.px_tiles = static_cast<int>((a.hw + pw_px(4) - 1) / pw_px(4));
+    const int64_t tiles = static_cast<int64_t>(a.px_tiles) * g.To * g.d.N;
+    const int64_t cus = device_compute_units();
+    const int64_t blocks = tiles < cus ? tiles : cus;
+    if (info) {
+      info->kernel = C3C_KERNEL_POINTWISE;
+      info->tile_co = PW_CO;
+      info->tile_h = 0;
+      info->tile_w = pw_px(4);
+      info->workgroups = blocks;
+      return hipSuccess;
+    }
+    if (tiles > 0x7fffffff) return hipErrorInvalidConfiguration;
+    const bool f16 = g.d.dtype == C3C_DTYPE_F16;
+    if (f16)
+      hipLaunchKernelGGL((pointwise_resident<true, 4>), dim3(static_cast<unsigned>(blocks)), dim3(PW_NT), 0,
+                         s, a, static_cast<int>(tiles));
+    else
+      hipLaunchKernelGGL((pointwise_resident<false, 4>), dim3(static_cast<unsigned>(blocks)), dim3(PW_NT), 0,
+                         s, a, static_cast<int>(tiles));
+    return hipGetLastError();
+  }
   a.w = static_cast<const uint16_t*>(w);
   a.w_bytes = static_cast<uint32_t>(g.d.Co * g.d.Ci * 2);
   a.cofrags = 0;

@@ -182,6 +182,16 @@ FALLBACK_CASES = FAST_CASES + [
                   has_bias=0)),
     # H*W not a multiple of 8: the generic kernel
     ("bf16", dict(N=1, Ci=8, Co=16, T=2, Tc=0, H=3, W=5, Kt=1, Kh=1, Kw=1)),
+    # the resident-weight pointwise kernel (Co <= 160, at most 11 channel
+    # chunks): all 11 chunks and 160 channels; ragged output fragments and a
+    # pixel tail; a right pad (the last output frame is the bias alone);
+    # stride 2 reading a cached frame; more tiles than workgroups (each
+    # workgroup walks two tiles, the ring running on across them)
+    ("bf16", dict(N=1, Ci=352, Co=160, T=2, Tc=0, H=10, W=40, Kt=1, Kh=1, Kw=1)),
+    ("bf16", dict(N=2, Ci=96, Co=100, T=3, Tc=0, H=9, W=24, Kt=1, Kh=1, Kw=1)),
+    ("bf16", dict(N=1, Ci=40, Co=24, T=3, Tc=0, H=8, W=8, Kt=1, Kh=1, Kw=1, p_r=1)),
+    ("f16", dict(N=1, Ci=48, Co=40, T=4, Tc=1, H=8, W=40, Kt=1, Kh=1, Kw=1, s_t=2, p_base=1)),
+    ("bf16", dict(N=1, Ci=64, Co=24, T=2, Tc=0, H=64, W=1024, Kt=1, Kh=1, Kw=1)),
 ]
 
 
