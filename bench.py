@@ -414,7 +414,6 @@ class Workload:
 def provenance(digests):
     """Host, toolchain and input records of the run."""
     import platform
-    import subprocess
     import torch
     cpu_model = None
     try:
@@ -429,13 +428,14 @@ def provenance(digests):
         rocm = open("/opt/rocm/.info/version").read().strip()
     except OSError:
         pass
+    # the compiler that built the library, as the build recorded it (no
+    # compiler is started here: under a profiler a child process would
+    # inherit the profiler's GPU-initialising preload)
     hipcc = None
     try:
-        r = subprocess.run(["/opt/rocm/bin/hipcc", "--version"], capture_output=True, text=True,
-                           timeout=60)
-        hipcc = " | ".join(l.strip() for l in r.stdout.splitlines()
-                           if "version" in l.lower())[:200] or None
-    except (OSError, subprocess.SubprocessError):
+        bi = json.load(open(os.path.join(ROOT, "paper_2609_31938_amd", "libc3c.buildinfo.json")))
+        hipcc = " | ".join(bi.get("hipcc", []))[:200] or None
+    except (OSError, ValueError):
         pass
     import oracle
     props = torch.cuda.get_device_properties(0)

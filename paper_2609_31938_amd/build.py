@@ -58,7 +58,22 @@ def build(verbose: bool = False) -> str:
         print(" ".join(cmd), flush=True)
     subprocess.check_call(cmd)
     os.replace(tmp, LIB)
+    _write_buildinfo()
     return LIB
+
+
+def _write_buildinfo() -> None:
+    """Record the compiler that built the library (read by bench.py's
+    provenance, which must not start the compiler on a GPU host)."""
+    import hashlib
+    import json
+    r = subprocess.run([HIPCC, "--version"], capture_output=True, text=True)
+    info = {"hipcc": [l.strip() for l in r.stdout.splitlines() if "version" in l.lower()],
+            "flags": COMMON[:2] + COMMON[3:5] + ["-Xclang -target-feature -Xclang -packed-fp32-ops"],
+            "sources_sha256": {f: hashlib.sha256(open(os.path.join(CSRC, f), "rb").read()).hexdigest()
+                               for f in sorted(os.listdir(CSRC))}}
+    with open(os.path.join(HERE, "libc3c.buildinfo.json"), "w") as f:
+        json.dump(info, f, indent=1)
 
 
 def build_sanitized(out_dir: str, verbose: bool = False) -> str:
