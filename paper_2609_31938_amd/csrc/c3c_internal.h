@@ -105,11 +105,13 @@ hipError_t launch_tap1x1(const Geo& g, const void* x, const void* cache, const v
                          const void* bias, void* y, hipStream_t s, LaunchInfo* info = nullptr);
 // fast route, bf16, 3x3 spatial kernel with Co <= 5 (conv_head.hip): the 9
 // spatial taps x Co output channels as the matrix cores' N dimension, then a
-// 3x3 gather-sum; needs W a multiple of 8 and aligned pointers.  The caller
-// copies the cache.
+// 3x3 gather-sum; needs W a multiple of 8 and aligned pointers.  Writes the
+// new cache itself when every cache frame is among the frames it stages
+// (*cache_written); otherwise the caller copies it.
 bool head_eligible(const Geo& g, const void* x, const void* cache, const void* y);
 hipError_t launch_head(const Geo& g, const void* x, const void* cache, const void* wpack,
-                       const void* bias, void* y, hipStream_t s, LaunchInfo* info = nullptr);
+                       const void* bias, void* y, void* cache_out, bool* cache_written,
+                       hipStream_t s, LaunchInfo* info = nullptr);
 // fast route, bf16, 1x1 spatial kernel (pointwise.hip): every active temporal
 // tap of a call as per-frame matrix products, reading the packed weights; any
 // temporal stride and dilation, any H * W and alignment.  The caller copies

@@ -384,7 +384,9 @@ hipError_t launch_fast(const Geo& g, const void* x, const void* cache, const voi
         e = launch_fast_tap1x1(g, x, cache, wpack, bias, y, s, fu, info);
     } else if (!fu.any() && head_eligible(g, x, cache, y)) {
       // few output channels (a decoder's RGB head): the spatial taps as N
-      e = launch_head(g, x, cache, wpack, bias, y, s, info);
+      bool written = false;
+      e = launch_head(g, x, cache, wpack, bias, y, cache_out, &written, s, info);
+      if (e != hipSuccess || written || info) return e;
     } else {
       bool written = false;
       e = launch_fast_bf16(g, x, cache, wpack, bias, y, cache_out, ws, ws_bytes, &written, s, fu,

@@ -327,7 +327,8 @@ def test_tap1x1_kernel_matches_oracle(over):
 # The head kernel (Co <= 5, W a multiple of 8): the 9 spatial taps x Co as
 # matrix-core columns, then a 3x3 gather-sum.  Every Co it serves, ragged
 # rows (H not a multiple of the 6-row tile) and columns (W not a multiple of
-# 64), a channel-chunk tail, dilation, p_l < 0, no cache, N = 2, Kt = 2.
+# 64), a channel-chunk tail, dilation, p_l < 0, no cache, N = 2, Kt = 2, and
+# more output frames than one pass of the kernel takes.
 HEAD_CASES = [
     dict(N=1, Ci=96, Co=3, T=4, Tc=2, H=37, W=136),
     dict(N=1, Ci=40, Co=1, T=2, Tc=2, H=20, W=72),
@@ -336,6 +337,10 @@ HEAD_CASES = [
     dict(N=1, Ci=32, Co=5, T=3, Tc=4, H=11, W=40, d_t=2),
     dict(N=1, Ci=72, Co=3, T=3, Tc=0, H=25, W=200),
     dict(N=1, Ci=24, Co=3, T=2, Tc=1, H=8, W=8, Kt=2),
+    # more output frames than one group (4, or 2 with three column
+    # fragments): the new cache written by the group that first stages it
+    dict(N=1, Ci=40, Co=3, T=6, Tc=2, H=14, W=56),
+    dict(N=2, Ci=36, Co=5, T=5, Tc=2, H=9, W=48),
 ]
 
 
