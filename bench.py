@@ -46,11 +46,14 @@ PEAK_HBM_GBS = 8000.0       # MI355X HBM3E peak (published)
 
 
 # The library's compute kernels, by the plan query's name for them (the
-# kernel a call's plan names is its one main launch); the auxiliary kernels a
-# call may add after it (split-K reduction, cache copy, prologue pass).
-MAIN_KERNELS = {"conv3d_bf16": "conv3d_bf16", "head": "conv_head", "tap1x1": "conv_tap1x1",
-                "pointwise": "pointwise_conv", "fast_f32": "fast_conv3d",
-                "fallback_direct": "fallback_conv3d"}
+# kernel a call's plan names is its one main launch, one of the listed
+# symbols); the auxiliary kernels a call may add after it (split-K reduction,
+# cache copy, prologue pass).
+MAIN_KERNELS = {"conv3d_bf16": ("conv3d_bf16",), "head": ("conv_head",),
+                "tap1x1": ("conv_tap1x1",),
+                "pointwise": ("pointwise_conv", "pointwise_resident"),
+                "fast_f32": ("fast_conv3d",), "fallback_direct": ("fallback_conv3d",)}
+MAIN_SYMBOLS = tuple(n for names in MAIN_KERNELS.values() for n in names)
 AUX_KERNELS = ("splitk_reduce", "cache_copy", "cache_copy_pro", "prologue_pass")
 
 # Further configurations timed by a default run, after the headline one:
@@ -467,7 +470,7 @@ def trace_summary(csv_path, log_path):
     kn, ks, ke = key("Kernel_Name"), key("Start_Timestamp"), key("End_Timestamp")
     kd = next((k for k in rows[0] if k in ("Dispatch_Id", "Correlation_Id")), None)
     rows.sort(key=lambda r: int(r[kd]) if kd else int(r[ks]))
-    main_re = re.compile(r"\b(" + "|".join(MAIN_KERNELS.values()) + r")\b")
+    main_re = re.compile(r"\b(" + "|".join(MAIN_SYMBOLS) + r")\b")
     aux_re = re.compile(r"\b(" + "|".join(AUX_KERNELS) + r")\b")
     log = json.load(open(log_path))
     calls, line = log["calls"], log["bench_line"]
@@ -484,7 +487,7 @@ def trace_summary(csv_path, log_path):
         sys.exit(f"{len(launches)} main kernel launches in the trace, {len(calls)} calls logged")
     groups = {}
     for c, (name, ms, aux) in zip(calls, launches):
-        if MAIN_KERNELS[c["kernel"]] not in name:
+        if main_re.search(name).group(1) not in MAIN_KERNELS[c["kernel"]]:
             sys.exit(f"call {c} matched to launch {name}")
         if c["phase"] != "timed":
             continue
@@ -505,7 +508,7 @@ def trace_summary(csv_path, log_path):
         mean = sum(g["ms"]) / len(g["ms"])
         med = statistics.median(g["ms"])
         aux = sum(g["aux"]) / len(g["aux"])
-        km = re.search(r"\b(" + "|".join(MAIN_KERNELS.values()) + r")\b(<[^()]*>)?", g["kernel"])
+        km = re.search(r"\b(" + "|".join(MAIN_SYMBOLS) + r")\b(<[^()]*>)?", g["kernel"])
         kname = km.group(0) if km else g["kernel"]
         if p is not None:
             peak = p["tflops"] / p["frac_peak"] if p["frac_peak"] else PEAK_BF16_TFLOPS
