@@ -97,12 +97,16 @@ int64_t device_compute_units();
 constexpr int64_t kTap1x1TileCo = 192;     // conv_tap1x1.hip
 constexpr int64_t kPointwiseTileCo = 160;  // pointwise.hip
 // fast route, bf16, 1x1 spatial kernel (conv_tap1x1.hip): 192 x 128 output
-// tiles on 4 waves; needs H * W a multiple of 8 and aligned pointers.  The
-// caller copies the cache.
+// tiles on 4 waves; needs H * W a multiple of 8 and aligned pointers.
+// tap1x1_blocks is the workgroup count of one output frame per workgroup
+// (the routing rule's measure).  Writes the new cache itself when every
+// cache frame is among the frames it stages (*cache_written); otherwise the
+// caller copies it.
 bool tap1x1_eligible(const Geo& g, const void* x, const void* cache, const void* y);
 int64_t tap1x1_blocks(const Geo& g);
 hipError_t launch_tap1x1(const Geo& g, const void* x, const void* cache, const void* wpack,
-                         const void* bias, void* y, hipStream_t s, LaunchInfo* info = nullptr);
+                         const void* bias, void* y, void* cache_out, bool* cache_written,
+                         hipStream_t s, LaunchInfo* info = nullptr);
 // fast route, bf16, 3x3 spatial kernel with Co <= 5 (conv_head.hip): the 9
 // spatial taps x Co output channels as the matrix cores' N dimension, then a
 // 3x3 gather-sum; needs W a multiple of 8 and aligned pointers.  Writes the

@@ -36,6 +36,8 @@
 // Requires H * W a multiple of 8 and 16-byte-aligned x / cache, 8-byte y.
 #include "c3c_internal.h"
 
+#include <type_traits>
+
 namespace c3c {
 namespace {
 
@@ -76,6 +78,9 @@ struct TapArgs {
   int chunks, cofrags, px_tiles, co_tiles, nblocks;
   uint32_t wpack_bytes;
   int has_bias;
+  // the new cache, written by the kernel when write_cache (L frames)
+  uint16_t* cache_out;
+  int L, write_cache;
 };
 
 __global__ __launch_bounds__(256, 2) void conv_tap1x1(TapArgs a) {
@@ -109,6 +114,22 @@ __global__ __launch_bounds__(256, 2) void conv_tap1x1(TapArgs a) {
   while (k_hi >= 0 && t * a.st + k_hi * a.dt - a.p_l >= a.Z) --k_hi;
   const int ntap = k_hi >= k_lo ? k_hi - k_lo + 1 : 0;
   const int nst = ntap * a.chunks;  // tap outer, chunk inner
+  // taps whose frame this workgroup writes to the new cache: output-channel
+  // tile 0, a frame of the new cache, and read by no earlier output frame
+  // (t' < t with t' s_t = f + p_l - k d_t); the launcher allows this only
+  // for Kt <= 32
+  uint32_t cwk = 0;
+  if (a.write_cache && ctile == 0)
+    for (int k = k_lo; k <= k_hi; ++k) {
+      const int f = t * a.st + k * a.dt - a.p_l;
+      if (f < a.Z - a.L) continue;
+      bool before = false;
+      for (int k2 = 0; k2 < a.Kt; ++k2) {
+        const int kd = f + a.p_l - k2 * a.dt;
+        if (kd >= 0 && kd % a.st == 0 && kd / a.st < t) before = true;
+      }
+      if (!before) cwk |= 1u << k;
+    }
   const int padded = (nst + 1) & ~1;
 
   // activation stages are loaded in order: (ak, ac) is the tap and channel
@@ -155,9 +176,29 @@ __global__ __launch_bounds__(256, 2) void conv_tap1x1(TapArgs a) {
     for (int i = 0; i < TSPT; ++i)
       v[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, s_row[i] * cs + s_px[i], 0, 0));
   };
-  auto store_act = [&](const u32x4 (&v)[TSPT], int buf) {
+  // stage q's activations into LDS buffer buf; a stage whose frame goes to
+  // the new cache [N][Ci][L][H*W] (frame f is its frame f - (Z - L)) is
+  // also written there from the same registers (the chunk's real rows,
+  // pixels inside the plane)
+  const int64_t cl = static_cast<int64_t>(a.L) * a.hw;
+  auto store_act = [&](const u32x4 (&v)[TSPT], int buf, int q) {
 #pragma unroll
     for (int i = 0; i < TSPT; ++i) *reinterpret_cast<u32x4*>(lds + buf * TBUF + s_lds[i]) = v[i];
+    const int k = k_lo + q / a.chunks, c0 = (q % a.chunks) * TK;
+    if (cwk != 0 && q < nst && ((cwk >> k) & 1u)) {
+      const int f = t * a.st + k * a.dt - a.p_l;
+      const uint32_t ccs = static_cast<uint32_t>(cl * 2);
+      const uint32_t cbytes = static_cast<uint32_t>(min(TK, a.Ci - c0) - 1) * ccs + static_cast<uint32_t>(a.hw) * 2u;
+      const __amdgpu_buffer_rsrc_t crs = __builtin_amdgcn_make_buffer_rsrc(
+          a.cache_out + (static_cast<int64_t>(n) * a.Ci + c0) * cl + static_cast<int64_t>(f - (a.Z - a.L)) * a.hw,
+          0, static_cast<int>(cbytes), 0x00020000);
+#pragma unroll
+      for (int i = 0; i < TSPT; ++i) {
+        const uint32_t px = px0 + s_px[i] / 2u;
+        __builtin_amdgcn_raw_buffer_store_b128(v[i], crs,
+                                               px < static_cast<uint32_t>(a.hw) ? s_row[i] * ccs + px * 2u : OOB, 0, 0);
+      }
+    }
   };
 
   // weights: fragment (tap k, chunk c, output fragment ctile 12 + wco 3 + cf),
@@ -206,7 +247,7 @@ __global__ __launch_bounds__(256, 2) void conv_tap1x1(TapArgs a) {
   load_w(0, w0);
   load_act(act0);
   load_act(act1);
-  store_act(act0, 0);
+  store_act(act0, 0, 0);
   __syncthreads();
 
   // one stage: weights of s + 1 and activations of s + 2 issued (their
@@ -226,7 +267,7 @@ __global__ __launch_bounds__(256, 2) void conv_tap1x1(TapArgs a) {
       for (int cf = 0; cf < WCO; ++cf)
         acc[cf][pf] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
             __builtin_bit_cast(bf16x8, av[pf]), __builtin_bit_cast(bf16x8, w_cur[cf]), acc[cf][pf], 0, 0, 0);
-    store_act(a_next, buf ^ 1);
+    store_act(a_next, buf ^ 1, s + 1);
     __syncthreads();
   };
   for (int s = 0; s < padded; s += 2) {
@@ -257,6 +298,296 @@ __global__ __launch_bounds__(256, 2) void conv_tap1x1(TapArgs a) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// Chunk-stage form, for calls with one output frame (a decoder's first
+// temporal upsampling).  The same 192 x 128 tile of one output frame, but one
+// stage is one 32-channel chunk of every tap (up to 3): its source frames
+// (one slot per tap, frame F0 + k d_t with F0 = t s_t - p_l) are staged into
+// LDS together, the weights of all taps of the chunk loaded together, so a
+// stage carries up to 3 x 24 products per wave and its barrier is paid over
+// three times the work.  A slot whose frame lies outside [0, Z) (Eq. 4) or
+// whose tap is >= Kt is staged as zeros with zero weights.
+// Staging: the activation tiles go from memory straight into LDS (buffer
+// loads with the LDS destination, 16 bytes a lane; no registers), each
+// [32 ch][128 px] tile as 32 rows of 256 bytes whose 16-byte segments are
+// permuted within the row (segment s of row r at s ^ sw(r)), so that the
+// transposing reads stay free of bank conflicts without padding.
+// Pipeline: three LDS buffers and three weight register sets; during chunk c
+// the waves issue chunk c + 2's weights and tiles into set and buffer
+// (c + 2) % 3 (last used in chunk c - 1), run chunk c's products from buffer
+// c % 3 (its first slot read before the previous barrier), then wait for
+// their own share of chunk c + 1's tiles (issued a stage earlier) and meet at
+// one barrier.  The explicit wait and a plain barrier (no release fence) let
+// chunk c + 2's loads stay in flight across it.
+// The new cache: the output-channel tile 0 workgroup of the first output
+// frame that reads a new-cache frame copies it from LDS (the launcher checks
+// that every new-cache frame is read by some output frame).
+constexpr int KTG = 3;       // taps this form holds weights for
+constexpr int GTILE = 8192;  // bytes of one staged [32 ch][128 px] tile
+// segment permutation of row r: rows {0..3, 8..11} (and {4..7, 12..15}),
+// which one transposing read pass serves, land in 8 distinct 32-byte bank
+// groups
+__device__ __forceinline__ uint32_t seg_swizzle(uint32_t r) { return ((r & 3u) | (((r >> 3) & 1u) << 2)) << 1; }
+typedef __attribute__((address_space(3))) void lds_void;
+
+__global__ __launch_bounds__(256, 1) void conv_tap1x1_chunk(TapArgs a) {
+  constexpr int NR = KTG;  // frame slots, one per tap
+  // three stage buffers, each its own array: the compiler then knows that a
+  // load into one does not write what is read from another (a single array
+  // makes it wait for every load into LDS before any LDS read)
+  __shared__ __align__(16) unsigned char lds0[NR * GTILE];
+  __shared__ __align__(16) unsigned char lds1[NR * GTILE];
+  __shared__ __align__(16) unsigned char lds2[NR * GTILE];
+  auto bufp = [&](auto B) -> unsigned char* { return B.value == 0 ? lds0 : B.value == 1 ? lds1 : lds2; };
+  constexpr uint32_t OOB = 0x80000000u;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+
+  // XCD-contiguous numbering, as above: the output-channel tiles of a pixel
+  // tile run close together
+  int b;
+  {
+    const int per = a.nblocks / 8, rem = a.nblocks % 8;
+    const int xcd = static_cast<int>(blockIdx.x) % 8, slot = static_cast<int>(blockIdx.x) / 8;
+    b = (xcd < rem ? xcd * (per + 1) : rem * (per + 1) + (xcd - rem) * per) + slot;
+  }
+  const int ctile = b % a.co_tiles;
+  b /= a.co_tiles;
+  const int pt = b % a.px_tiles;
+  b /= a.px_tiles;
+  const int t = b % a.To;
+  const int n = b / a.To;
+  const int px0 = pt * TPX;
+
+  // slot r (tap r) reads frame F0 + r d_t; live: r < Kt and the frame in
+  // [0, Z); cwm: live, a frame of the new cache, and read by no earlier
+  // output frame (t' < t with t' s_t = f + p_l - k d_t)
+  const int F0 = t * a.st - a.p_l;
+  auto slot_frame = [&](int r) { return F0 + r * a.dt; };
+  uint32_t live = 0, cwm = 0;
+#pragma unroll
+  for (int r = 0; r < NR; ++r) {
+    const int f = slot_frame(r);
+    if (r >= a.Kt || f < 0 || f >= a.Z) continue;
+    live |= 1u << r;
+    if (!a.write_cache || ctile != 0 || f < a.Z - a.L) continue;
+    bool before = false;
+    for (int k = 0; k < a.Kt; ++k) {
+      const int kd = f + a.p_l - k * a.dt;
+      if (kd >= 0 && kd % a.st == 0 && kd / a.st < t) before = true;
+    }
+    if (!before) cwm |= 1u << r;
+  }
+
+  // staging: this wave's two 1 KiB blocks of a tile are rows 4 (4 i + wv)
+  // .. + 3; lane l fills row 4 (4 i + wv) + l / 16, LDS segment l % 16, with
+  // the row's segment (l % 16) ^ sw(row) (pixels 8 of it .. + 7)
+  uint32_t d_row[2], d_px[2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const uint32_t r = static_cast<uint32_t>(4 * (4 * i + wv) + (lane >> 4));
+    d_row[i] = r;
+    d_px[i] = ((static_cast<uint32_t>(lane) & 15u) ^ seg_swizzle(r)) * 16u;
+  }
+  const int64_t cs_c = static_cast<int64_t>(a.Tc) * a.hw, cs_x = static_cast<int64_t>(a.T) * a.hw;
+  // slot r, channels 32 c ..: the chunk's real rows from pixel px0 (at most
+  // 32 channel planes: 32-bit sizes); empty (zeros) for a slot that is not
+  // live or a chunk past the last
+  auto act_rsrc = [&](int r, int c, uint32_t& cs) {
+    const int f = slot_frame(r), c0 = c * TK;
+    const bool real = ((live >> r) & 1u) && c < a.chunks;
+    const bool in_cache = f < a.Tc;
+    const int64_t cstride = in_cache ? cs_c : cs_x;
+    const uint16_t* base = in_cache ? a.cache : a.x;
+    const int64_t off = static_cast<int64_t>(in_cache ? f : f - a.Tc) * a.hw +
+                        static_cast<int64_t>(n) * a.Ci * cstride + px0 + c0 * cstride;
+    cs = static_cast<uint32_t>(cstride * 2);
+    const uint32_t bytes =
+        real ? static_cast<uint32_t>(min(TK, a.Ci - c0) - 1) * cs + static_cast<uint32_t>(a.hw - px0) * 2u : 0u;
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(real ? base + off : a.x), 0,
+                                             static_cast<int>(bytes), 0x00020000);
+  };
+  // chunk c's tiles into the LDS buffer at L (2 NR loads per lane)
+  auto stage_act = [&](int c, unsigned char* L) {
+#pragma unroll
+    for (int r = 0; r < NR; ++r) {
+      uint32_t cs;
+      const __amdgpu_buffer_rsrc_t rs = act_rsrc(r, c, cs);
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void*)(L + r * GTILE + (4 * i + wv) * 1024), 16,
+                                                 d_row[i] * cs + d_px[i], 0, 0, 0);
+    }
+  };
+  // the new cache [N][Ci][L][H*W] (frame f is its frame f - (Z - L)):
+  // chunk c's cache slots copied from the LDS buffer at L, 16 bytes a lane,
+  // rows as staged (segment permutation undone on the way out)
+  const int64_t cl = static_cast<int64_t>(a.L) * a.hw;
+  auto copy_cache = [&](int c, const unsigned char* L) {
+    const int c0 = c * TK;
+    const uint32_t ccs = static_cast<uint32_t>(cl * 2);
+    const uint32_t cbytes = static_cast<uint32_t>(min(TK, a.Ci - c0) - 1) * ccs + static_cast<uint32_t>(a.hw) * 2u;
+#pragma unroll
+    for (int r = 0; r < NR; ++r) {
+      if (!((cwm >> r) & 1u)) continue;
+      const __amdgpu_buffer_rsrc_t crs = __builtin_amdgcn_make_buffer_rsrc(
+          a.cache_out + (static_cast<int64_t>(n) * a.Ci + c0) * cl +
+              static_cast<int64_t>(slot_frame(r) - (a.Z - a.L)) * a.hw,
+          0, static_cast<int>(cbytes), 0x00020000);
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        const uint32_t q = static_cast<uint32_t>(tid + 256 * i), row = q >> 4, ls = q & 15u;
+        const u32x4 v = *reinterpret_cast<const u32x4*>(L + r * GTILE + q * 16);
+        const uint32_t px = px0 + (ls ^ seg_swizzle(row)) * 8u;
+        __builtin_amdgcn_raw_buffer_store_b128(v, crs, px < static_cast<uint32_t>(a.hw) ? row * ccs + px * 2 : OOB,
+                                               0, 0);
+      }
+    }
+  };
+
+  // weights: fragment (tap k, chunk c, output fragment ctile 12 + wv 3 + cf),
+  // clamped to the last packed fragment (padding rows are never stored); an
+  // out-of-range offset (zeros) for k >= Kt or a chunk past the last
+  const __amdgpu_buffer_rsrc_t wrs = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<u32x4*>(a.wpack), 0, static_cast<int>(a.wpack_bytes), 0x00020000);
+  uint32_t w_off[WCO];
+#pragma unroll
+  for (int cf = 0; cf < WCO; ++cf)
+    w_off[cf] = static_cast<uint32_t>(min(ctile * (TCO / 16) + wv * WCO + cf, a.cofrags - 1)) * 1024u +
+                static_cast<uint32_t>(lane) * 16u;
+  auto load_w = [&](int c, u32x4 (&v)[KTG][WCO]) {
+#pragma unroll
+    for (int k = 0; k < KTG; ++k) {
+      const bool real = k < a.Kt && c < a.chunks;
+      const uint32_t row = static_cast<uint32_t>((k * a.chunks + c) * a.cofrags) * 1024u;
+#pragma unroll
+      for (int cf = 0; cf < WCO; ++cf)
+        v[k][cf] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                                                 wrs, real ? row + w_off[cf] : OOB, 0, 0));
+    }
+  };
+
+  // transposing operand read: within each 16-lane block g = l / 16, lane j
+  // reads 8 bytes of channel row 8g + 4h + j / 4 (h = 0, 1) at pixel
+  // 16 pf + 4 (j % 4) of the tile, i.e. staged segment 2 pf + (j % 4) / 2;
+  // with the even permutation sw(row) that is byte
+  // row 256 + 32 (pf ^ sw(row) / 2) + 8 (j % 4) = ra ^ 32 pf.
+  // (z: a zero the compiler cannot see through, fresh each stage, so that
+  // the addresses are formed where they are used rather than held in
+  // registers across the loop for every buffer and slot)
+  const int j16 = lane & 15, g = lane >> 4;
+  const uint32_t rrow = static_cast<uint32_t>(8 * g + (j16 >> 2));
+  const uint32_t ra = rrow * 256u + 16u * seg_swizzle(rrow) + 8u * static_cast<uint32_t>(j16 & 3);
+  auto read_a = [&](const unsigned char* L, int r, i16x8 (&av)[NPF], uint32_t z) {
+#pragma unroll
+    for (int pf = 0; pf < NPF; ++pf) {
+      const unsigned char* p = L + r * GTILE + ((ra + z) ^ (32u * pf));
+      const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p));
+      const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p + 4 * 256));
+      av[pf] = i16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+    }
+  };
+
+  f32x4 acc[WCO][NPF];
+#pragma unroll
+  for (int cf = 0; cf < WCO; ++cf)
+#pragma unroll
+    for (int pf = 0; pf < NPF; ++pf) acc[cf][pf] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  // wait until at most n vector-memory operations of this wave are
+  // outstanding (the LDS and export counters left alone)
+#define C3C_VMCNT(n) __builtin_amdgcn_s_waitcnt(((n) & 15) | (((n) >> 4) << 14) | (7 << 4) | (15 << 8))
+  auto barrier = [] { asm volatile("s_barrier" ::: "memory"); };
+
+  // One stage: chunk c's products from LDS buffer B with weight set B, slot
+  // by slot.  A slot's operands are read during the previous slot's
+  // products (one read after each of the first 2 x NPF products; slot 0's
+  // before the previous barrier), slot r into operand set r % 2.  No
+  // instruction moves across a slot's end.
+  u32x4 w[3][KTG][WCO];
+  i16x8 avs[2][NPF];
+  auto stage = [&](int c, auto B) {
+    constexpr int b0 = decltype(B)::value, b1 = (b0 + 1) % 3, b2 = (b0 + 2) % 3;
+    unsigned char* const cur_b = bufp(B);
+    unsigned char* const next_b = bufp(std::integral_constant<int, b1>{});
+    unsigned char* const fill_b = bufp(std::integral_constant<int, b2>{});
+    uint32_t z;
+    asm volatile("v_mov_b32 %0, 0" : "=v"(z));
+    if (cwm != 0 && c < a.chunks) copy_cache(c, cur_b);
+    load_w(c + 2, w[b2]);
+    stage_act(c + 2, fill_b);
+#pragma unroll
+    for (int r = 0; r < NR; ++r) {
+      const i16x8(&cur)[NPF] = avs[r & 1];
+      if (r + 1 < NR) read_a(cur_b, r + 1, avs[(r + 1) & 1], z);
+#pragma unroll
+      for (int pf = 0; pf < NPF; ++pf)
+#pragma unroll
+        for (int cf = 0; cf < WCO; ++cf)
+          acc[cf][pf] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+              __builtin_bit_cast(bf16x8, cur[pf]), __builtin_bit_cast(bf16x8, w[b0][r][cf]), acc[cf][pf], 0, 0, 0);
+      if (r + 1 < NR) {
+#pragma unroll
+        for (int q = 0; q < 2 * NPF; ++q) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // a matrix-core product
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // an LDS read
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    read_a(next_b, 0, avs[0], z);
+    // this wave's loads of chunk c + 1 (issued a stage ago, the tiles after
+    // the weights) have landed; chunk c + 2's may still be in flight
+    C3C_VMCNT(KTG * WCO + 2 * NR);
+    barrier();
+  };
+
+  // prologue: chunks 0 and 1 into buffers and weight sets 0 and 1, slot 0
+  // of chunk 0 pre-read
+  using I0 = std::integral_constant<int, 0>;
+  using I1 = std::integral_constant<int, 1>;
+  using I2 = std::integral_constant<int, 2>;
+  load_w(0, w[0]);
+  stage_act(0, lds0);
+  load_w(1, w[1]);
+  stage_act(1, lds1);
+  C3C_VMCNT(KTG * WCO + 2 * NR);
+  barrier();
+  read_a(lds0, 0, avs[0], 0u);
+
+  // three stages a round: buffers and weight sets 0, 1, 2 in turn (stages
+  // past the last chunk read zeros: zero-size sources, out-of-range weights;
+  // a round with early exits made the register allocator copy the
+  // accumulators between the stage copies)
+  for (int c = 0; c < a.chunks; c += 3) {
+    stage(c, I0{});
+    stage(c + 1, I1{});
+    stage(c + 2, I2{});
+  }
+#undef C3C_VMCNT
+
+  // epilogue: lane l holds pixels 4 (l / 16) .. + 3 of output channel l % 16
+  // of each fragment; bias once, one round-to-nearest-even, NCTHW store
+  uint16_t* ybase = a.y + (static_cast<int64_t>(n) * a.Co * a.To + t) * a.hw;
+#pragma unroll
+  for (int cf = 0; cf < WCO; ++cf) {
+    const int co = ctile * TCO + wv * 16 * WCO + cf * 16 + (lane & 15);
+    if (co >= a.Co) continue;
+    const float bb = a.has_bias ? __uint_as_float(static_cast<uint32_t>(a.bias[co]) << 16) : 0.f;
+    uint16_t* yrow = ybase + static_cast<int64_t>(co) * a.To * a.hw;
+#pragma unroll
+    for (int pf = 0; pf < NPF; ++pf) {
+      const int p = px0 + pf * 16 + 4 * g;
+      if (p >= a.hw) continue;
+      const uint32_t v01 = __builtin_bit_cast(
+          uint32_t, __builtin_convertvector((f32x2{acc[cf][pf][0] + bb, acc[cf][pf][1] + bb}), bf16x2));
+      const uint32_t v23 = __builtin_bit_cast(
+          uint32_t, __builtin_convertvector((f32x2{acc[cf][pf][2] + bb, acc[cf][pf][3] + bb}), bf16x2));
+      *reinterpret_cast<uint2*>(yrow + p) = make_uint2(v01, v23);
+    }
+  }
+}
+
 bool aligned_to(const void* p, uintptr_t m) { return (reinterpret_cast<uintptr_t>(p) & (m - 1)) == 0; }
 
 }  // namespace
@@ -276,10 +607,32 @@ int64_t tap1x1_blocks(const Geo& g) {
   return (g.d.H * g.d.W + TPX - 1) / TPX * ((g.d.Co + TCO - 1) / TCO) * g.To * g.d.N;
 }
 
+namespace {
+
+// Whether every frame of the new cache is read by some output frame
+// (f = t s_t + k d_t - p_l with t < To, k < Kt), so that the kernels, which
+// copy a cache frame when they stage it, write the whole new cache.
+bool stages_new_cache(const Geo& g) {
+  const c3c_conv_desc& d = g.d;
+  for (int64_t f = g.Z - g.L; f < g.Z; ++f) {
+    bool found = false;
+    for (int64_t k = 0; k < d.Kt && !found; ++k) {
+      const int64_t kd = f + g.p_l - k * d.dil_t;
+      found = kd >= 0 && kd % d.stride_t == 0 && kd / d.stride_t < g.To;
+    }
+    if (!found) return false;
+  }
+  return true;
+}
+
+}  // namespace
+
 hipError_t launch_tap1x1(const Geo& g, const void* x, const void* cache, const void* wpack,
-                         const void* bias, void* y, hipStream_t s, LaunchInfo* info) {
+                         const void* bias, void* y, void* cache_out, bool* cache_written,
+                         hipStream_t s, LaunchInfo* info) {
   const c3c_conv_desc& d = g.d;
   const PackDims p = pack_dims(d);
+  if (cache_written) *cache_written = false;
   if (!tap1x1_eligible(g, x, cache, y)) return hipErrorInvalidValue;
   TapArgs a;
   a.x = static_cast<const uint16_t*>(x);
@@ -305,6 +658,16 @@ hipError_t launch_tap1x1(const Geo& g, const void* x, const void* cache, const v
   a.co_tiles = static_cast<int>((d.Co + TCO - 1) / TCO);
   a.wpack_bytes = static_cast<uint32_t>(p.elems() * 2);
   a.has_bias = d.has_bias ? 1 : 0;
+  a.cache_out = static_cast<uint16_t*>(cache_out);
+  a.L = static_cast<int>(g.L);
+  a.write_cache = 0;
+  // the chunk-stage form for one output frame (Kt <= 3), else one stage per
+  // tap and chunk
+  const bool chunk_form = g.To == 1 && d.Kt <= KTG;
+  // the new cache from the staged tiles when every frame of it is staged
+  // (32-bit offsets within a 32-channel slab of it; a tap mask of 32 bits)
+  a.write_cache = g.L > 0 && cache_out != nullptr && aligned_to(cache_out, 16) && d.Kt <= 32 &&
+                  static_cast<int64_t>(TK) * g.L * a.hw * 2 < 0x7fffffff && stages_new_cache(g);
   const int64_t blocks = tap1x1_blocks(g);
   if (info) {
     info->kernel = C3C_KERNEL_TAP1X1;
@@ -312,12 +675,19 @@ hipError_t launch_tap1x1(const Geo& g, const void* x, const void* cache, const v
     info->tile_h = 0;
     info->tile_w = TPX;
     info->workgroups = blocks;
+    info->cache_in_kernel = a.write_cache != 0;
+    if (cache_written) *cache_written = a.write_cache != 0;
     return hipSuccess;
   }
+  if (cache_written) *cache_written = a.write_cache != 0;
   if (blocks == 0) return hipSuccess;
   if (blocks > 0x7fffffff) return hipErrorInvalidConfiguration;
   a.nblocks = static_cast<int>(blocks);
-  hipLaunchKernelGGL(conv_tap1x1, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, s, a);
+  const dim3 grid(static_cast<unsigned>(blocks)), block(256);
+  if (chunk_form)
+    hipLaunchKernelGGL(conv_tap1x1_chunk, grid, block, 0, s, a);
+  else
+    hipLaunchKernelGGL(conv_tap1x1, grid, block, 0, s, a);
   return hipGetLastError();
 }
 

@@ -378,9 +378,11 @@ hipError_t launch_fast(const Geo& g, const void* x, const void* cache, const voi
       const int64_t pad_tap = (g.d.Co + kTap1x1TileCo - 1) / kTap1x1TileCo * kTap1x1TileCo;
       const int64_t pad_pw = (g.d.Co + kPointwiseTileCo - 1) / kPointwiseTileCo * kPointwiseTileCo;
       if (!fu.any() && 10 * pad_tap <= 11 * pad_pw && tap1x1_eligible(g, x, cache, y) &&
-          2 * tap1x1_blocks(g) >= device_compute_units())
-        e = launch_tap1x1(g, x, cache, wpack, bias, y, s, info);
-      else
+          2 * tap1x1_blocks(g) >= device_compute_units()) {
+        bool written = false;
+        e = launch_tap1x1(g, x, cache, wpack, bias, y, cache_out, &written, s, info);
+        if (e != hipSuccess || written || info) return e;
+      } else
         e = launch_fast_tap1x1(g, x, cache, wpack, bias, y, s, fu, info);
     } else if (!fu.any() && head_eligible(g, x, cache, y)) {
       // few output channels (a decoder's RGB head): the spatial taps as N

@@ -304,6 +304,21 @@ TAP1X1_CASES = [
     dict(N=1, Ci=64, Co=384, T=16, Tc=1, H=64, W=80, s_t=2, p_base=1),
     dict(N=1, Ci=48, Co=576, T=6, Tc=0, H=56, W=64, d_t=2, p_base=4),
     dict(N=2, Ci=48, Co=768, T=2, Tc=2, H=30, W=52),             # H*W = 1560: ragged tile
+    # frame groups: the first group's taps clipped by the left pad, an odd
+    # number of output frames (the last group half used)
+    dict(N=1, Ci=64, Co=192, T=5, Tc=0, H=64, W=64, p_base=2),
+    # stride 3 (one output frame per group), and a new cache frame that no
+    # output frame reads (the copy kernel writes it)
+    dict(N=1, Ci=40, Co=192, T=9, Tc=1, H=96, W=64, s_t=3, p_base=1),
+    # Kt = 2 at stride 2: two-tap slots, new cache again by the copy
+    dict(N=1, Ci=64, Co=180, T=8, Tc=1, H=64, W=64, Kt=2, s_t=2, p_base=1),
+    # one output frame (all taps of a chunk per stage), and one with no
+    # cache whose first two taps fall on the left pad (one live tap; the
+    # new cache is the chunk's only frame)
+    dict(N=1, Ci=96, Co=384, T=1, Tc=2, H=128, W=128),
+    dict(N=2, Ci=40, Co=180, T=1, Tc=0, H=64, W=128, p_base=2),
+    # Kt = 4: the one-frame-per-workgroup kernel
+    dict(N=1, Ci=32, Co=192, T=4, Tc=3, H=64, W=64, Kt=4),
 ]
 
 
