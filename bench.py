@@ -50,7 +50,7 @@ PEAK_HBM_GBS = 8000.0       # MI355X HBM3E peak (published)
 # symbols); the auxiliary kernels a call may add after it (split-K reduction,
 # cache copy, prologue pass).
 MAIN_KERNELS = {"conv3d_bf16": ("conv3d_bf16",), "head": ("conv_head",),
-                "tap1x1": ("conv_tap1x1",),
+                "tap1x1": ("conv_tap1x1", "conv_tap1x1_chunk"),
                 "pointwise": ("pointwise_conv", "pointwise_resident"),
                 "fast_f32": ("fast_conv3d",), "fallback_direct": ("fallback_conv3d",)}
 MAIN_SYMBOLS = tuple(n for names in MAIN_KERNELS.values() for n in names)

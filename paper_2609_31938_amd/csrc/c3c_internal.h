@@ -97,7 +97,9 @@ int64_t device_compute_units();
 constexpr int64_t kTap1x1TileCo = 192;     // conv_tap1x1.hip
 constexpr int64_t kPointwiseTileCo = 160;  // pointwise.hip
 // fast route, bf16, 1x1 spatial kernel (conv_tap1x1.hip): 192 x 128 output
-// tiles on 4 waves; needs H * W a multiple of 8 and aligned pointers.
+// tiles on 4 waves (one stage per tap and chunk, or, for one output frame,
+// per chunk with all its taps); needs H * W a multiple of 8 and aligned
+// pointers.
 // tap1x1_blocks is the workgroup count of one output frame per workgroup
 // (the routing rule's measure).  Writes the new cache itself when every
 // cache frame is among the frames it stages (*cache_written); otherwise the

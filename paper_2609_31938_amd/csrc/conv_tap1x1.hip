@@ -32,6 +32,12 @@
 // alternate), the stage count padded to even with stages that read zeros.
 // Pixels past the end of a frame plane are loaded (the next plane, or zeros
 // past the tensor) but only feed outputs that are never stored.
+// The new cache (the last L frames of [cache; x]) is written from the staging
+// registers: by the output-channel tile 0 workgroup of the first output frame
+// that reads each of its frames, as that frame's tiles go to LDS, when every
+// new-cache frame is read by some output frame (the launcher checks;
+// otherwise the caller copies it).
+// Calls with one output frame take the chunk-stage form further down.
 //
 // Requires H * W a multiple of 8 and 16-byte-aligned x / cache, 8-byte y.
 #include "c3c_internal.h"
