@@ -346,7 +346,9 @@ def test_plan_of_the_workloads():
     from paper_2609_31938_amd.inputs import WORKLOADS
     want = {
         "c32_32x32": ("fast_f32", 32, 4, 32, 1),
-        "c384_60x104": ("conv3d_bf16", 192, 4, 64, 1),
+        # one output frame, 60 tiles of 192 x 4 x 64: unsplit (no workspace),
+        # the 128 x 4 x 80 tiling (90 workgroups, less work in the round)
+        "c384_60x104": ("conv3d_bf16", 128, 4, 80, 1),
         "c192_240x416": ("conv3d_bf16", 192, 4, 64, 1),
         "c384to192_240x416": ("conv3d_bf16", 192, 4, 64, 1),
         "c96_480x832": ("conv3d_bf16", 96, 6, 64, 1),
