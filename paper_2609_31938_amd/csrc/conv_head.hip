@@ -23,28 +23,43 @@
 // once per group instead of once per output frame that uses it.  4 waves,
 // wave v owning window rows 2v, 2v + 1: 8 pixel fragments x NF column
 // fragments per output frame of the group (up to 256 accumulator registers,
-// one workgroup per compute unit).  A stage's [32 ch][512 px] window tile
-// is copied into LDS as it lies in memory and read back with the
+// one workgroup per compute unit).
+// Staging: a stage's [32 ch][512 px] window tile goes from memory straight
+// into LDS (buffer loads with the LDS destination, 16 bytes a lane, no
+// registers): one load instruction of a wave fills one channel's 8 x 64
+// window, lane l taking window row l / 8, columns 8 (l % 8) .. + 7 (zeros
+// outside the image or past the last channel).  It is read back with the
 // transposing ds_read_b64_tr_b16 (the A operand: 8 channels of one pixel per
-// lane); the B operand for column n = 9-tap index ij times Co plus co is the
-// 16-byte lane slot of the packed 3x3 weights' fragment (tap k*9 + ij,
-// chunk, 0) that holds output channel co, so the fast route's one weight
-// packing serves this kernel too.  Two-stage pipeline with one barrier per
-// stage.  After a group's last stage, each of its output frames' accumulators
-// go to LDS as D[n][px] in fp32 in turn, and the workgroup sums the nine
-// shifted D values of each output, adds the bias once and rounds once.
-// A frame of the new cache is written from the staging registers by the
-// group that first stages it (its interior segments: each element has one
+// lane).  The B operand for column n = 9-tap index ij times Co plus co is
+// the 16-byte lane slot of the packed 3x3 weights' fragment (tap k*9 + ij,
+// chunk, 0) that holds output channel co (the fast route's one weight
+// packing serves this kernel too); every wave needs the same B operands, so
+// the workgroup gathers them once, at its start, into an LDS table of 1 KiB
+// lane-ordered entries (temporal tap k, chunk, column fragment q), and a
+// stage reads its B operands from there: a stage's only vector-memory loads
+// are its window's 32 (one per channel; on these loads the texture
+// addresser, not HBM, sets the pace).
+// Pipeline: NB = 4 (or 3, when the table needs the room) LDS buffers; during
+// stage s the waves issue stage s + NB - 1's window loads into buffer
+// (s + NB - 1) % NB (last read in stage s - 1), run stage s's products from
+// buffer s % NB, then wait for their own loads of stage s + 1 and meet at
+// one plain barrier, so the later stages' loads stay in flight across it.
+// The stage count is padded to a multiple of NB with stages that read zeros
+// and skip their products.  Per stage the scalar work is a few additions:
+// the source pointer and the table offsets step by one chunk, and only a
+// new source frame recomputes them (with the tap of each output frame).
+// After a group's last stage, its output frames' accumulators go to LDS as
+// D[n][px] in fp32, NB / NF frames at a time (one stage buffer per column
+// fragment), and the workgroup sums the nine shifted D values of each
+// output, adds the bias once and rounds once.
+// A frame of the new cache is copied out of the stage buffer by the group
+// that first stages it (its interior segments: each element has one
 // writer), so the caller copies no cache when every cache frame is staged.
-//
-// Measured on the 96 -> 3 480x832 layer (5 chunks): the same 0.24-0.25 ms
-// as the earlier per-output-frame form (with its separate cache copy), with
-// half the window traffic; three register sets of staged windows (two
-// stages of load latency) measured the same as two.
 //
 // Requires W a multiple of 8, 16-byte-aligned x / cache, 8-byte-aligned y
 // (and a 16-byte-aligned cache_out for the fused cache write).
 #include <algorithm>
+#include <type_traits>
 
 #include "c3c_internal.h"
 
@@ -59,12 +74,16 @@ typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef short i16x8 __attribute__((ext_vector_type(8)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+typedef __attribute__((address_space(3))) void lds_void;
 
 constexpr int HK = 32;                 // input channels per stage
 constexpr int HR = 8, HC = 64;         // input window rows x columns
 constexpr int OR = 6, OC = 48;         // output rows x columns per workgroup
 constexpr int HPX = HR * HC;           // window pixels
 constexpr int HPF = 2 * (HC / 16);     // pixel fragments per wave (2 rows)
+constexpr int HSEG = HK * HPX / 8;     // 16-byte segments of a stage tile
+static_assert(HSEG == 256 * 8 && HR * HC / 8 == 64,
+              "a wave stages 8 channels, one 64-segment window per load instruction");
 // LDS offset of staged channel row c: 1024 B + 32 B, and 128 B more after
 // every 8 channels.  The 32 lanes one transposing read serves per cycle take
 // 32 B from each of channels {0..3, 8..11} (+4, +16, +20 for the other
@@ -72,17 +91,20 @@ constexpr int HPF = 2 * (HC / 16);     // pixel fragments per wave (2 rows)
 constexpr int HPITCH = HPX * 2 + 32;
 constexpr int hrow(int c) { return c * HPITCH + (c >> 3) * 128; }
 constexpr int HBUF = hrow(HK);
-constexpr int HSEG = HK * HPX / 8;     // 16-byte segments of a stage tile
-constexpr int HSPT = HSEG / 256;       // per thread
-static_assert(HSEG % 256 == 0, "the stage tile splits evenly over the threads");
+constexpr int kLdsBytes = 160 * 1024;  // LDS of a compute unit
 constexpr int max_co(int nf) { return 16 * nf / 9; }
+// the weight table beside NB stage buffers: bytes, and 1 KiB entries
+constexpr int wtab_bytes(int nb) { return (kLdsBytes - nb * HBUF - (nb == 4 ? 0 : 16)) / 1024 * 1024; }
+constexpr int wtab_entries(int nb) { return wtab_bytes(nb) / 1024; }
+int head_table_entries(const c3c_conv_desc& d) {
+  return static_cast<int>(d.Kt * ((d.Ci + HK - 1) / HK) * ((9 * d.Co + 15) / 16));
+}
 // D rows (one per column n) of the window's 512 pixels, 516 floats apart: the
 // 16 lanes of a fragment row write 16 consecutive n with 16-byte stores, and
-// 516 = 4 mod 64 banks puts them in 16 disjoint 4-bank groups
+// 516 = 4 mod 64 banks puts them in 16 disjoint 4-bank groups; the 16 rows of
+// one column fragment fill one stage buffer
 constexpr int DPITCH = HPX + 4;
-constexpr int lds_bytes(int nf) {
-  return 2 * HBUF > 9 * max_co(nf) * DPITCH * 4 ? 2 * HBUF : 9 * max_co(nf) * DPITCH * 4;
-}
+static_assert(16 * DPITCH * 4 <= HBUF, "a column fragment of D fits one stage buffer");
 
 struct HeadArgs {
   const uint16_t* x;
@@ -98,10 +120,24 @@ struct HeadArgs {
   int has_bias, write_cache;
 };
 
-// OG output frames per pass (a group); NF 16-column fragments of D per tap.
-template <int NF, int OG>
+template <int V>
+using IC = std::integral_constant<int, V>;
+
+// OG output frames per pass (a group); NF 16-column fragments of D per tap;
+// NB stage buffers.
+template <int NF, int OG, int NB>
 __global__ __launch_bounds__(256, 1) void conv_head(HeadArgs a) {
-  __shared__ __align__(16) unsigned char lds[lds_bytes(NF)];
+  static_assert(NF <= NB && (NB == 3 || NB == 4), "D's column fragments go one per stage buffer");
+  constexpr int AHEAD = NB - 1;  // stages between a window load and its use
+  // the stage buffers and the weight table, each its own array: the
+  // compiler then knows that a load into one does not write what is read
+  // from another
+  __shared__ __align__(16) unsigned char lds0[HBUF];
+  __shared__ __align__(16) unsigned char lds1[HBUF];
+  __shared__ __align__(16) unsigned char lds2[HBUF];
+  __shared__ __align__(16) unsigned char lds3[NB == 4 ? HBUF : 16];
+  __shared__ __align__(16) unsigned char wtab[wtab_bytes(NB)];
+  auto bufp = [&](int q) -> unsigned char* { return q == 0 ? lds0 : q == 1 ? lds1 : q == 2 ? lds2 : lds3; };
   constexpr uint32_t OOB = 0x80000000u;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -120,40 +156,34 @@ __global__ __launch_bounds__(256, 1) void conv_head(HeadArgs a) {
   const int n = b / a.tiles_h;
   const int h0 = th * OR, w0 = tw * OC;
   const int wh0 = h0 - 1, ww0 = w0 - 8;  // window origin
-  const int64_t cs_c = static_cast<int64_t>(a.Tc) * a.hw, cs_x = static_cast<int64_t>(a.T) * a.hw;
 
-  // staging: segment q = tid + 256 i -> channel q / 64, window row (q % 64) / 8,
-  // columns 8 (q % 8) .. + 7; outside the image an out-of-range offset (zeros;
-  // W is a multiple of 8, so a segment is wholly inside or outside).  s_in:
-  // the segment lies in this tile's output rows and columns (the part of the
-  // window the new cache takes from this workgroup)
-  uint32_t s_ch[HSPT], s_px[HSPT], s_lds[HSPT];
-  bool s_in[HSPT];
-#pragma unroll
-  for (int i = 0; i < HSPT; ++i) {
-    const int q = tid + 256 * i, ch = q / (HPX / 8), rem = q % (HPX / 8);
-    const int r = rem / (HC / 8), sg = rem % (HC / 8);
-    const int gh = wh0 + r, gw = ww0 + 8 * sg;
-    const bool ok = gh >= 0 && gh < a.H && gw >= 0 && gw < a.W;
-    s_ch[i] = static_cast<uint32_t>(ch);
-    s_px[i] = ok ? static_cast<uint32_t>(gh * a.W + gw) * 2u : OOB;
-    s_lds[i] = static_cast<uint32_t>(hrow(ch) + (r * HC + 8 * sg) * 2);
-    s_in[i] = ok && r >= 1 && r <= OR && sg >= 1 && sg <= OC / 8;
-  }
+  // this lane's window segment (row lane / 8, columns 8 (lane % 8) .. + 7),
+  // staged for channels 8 wave .. + 7 of each stage; outside the image an
+  // out-of-range offset (zeros; W is a multiple of 8, so a segment is wholly
+  // inside or outside).  s_in: the segment lies in this tile's output rows
+  // and columns (the part of the window the new cache takes from here)
+  const int sr = lane >> 3, ssg = lane & 7;
+  const int gh = wh0 + sr, gw = ww0 + 8 * ssg;
+  const bool s_ok = gh >= 0 && gh < a.H && gw >= 0 && gw < a.W;
+  const uint32_t s_px = s_ok ? static_cast<uint32_t>(gh * a.W + gw) * 2u : OOB;
+  const bool s_in = s_ok && sr >= 1 && sr <= OR && ssg >= 1 && ssg <= OC / 8;
+  const int ch0 = 8 * wave;                                  // first staged channel
+  const uint32_t lrow = static_cast<uint32_t>(hrow(8) * wave);  // its LDS row
 
-  // weights: column n = 16 q + lane % 16 is (ij = n / Co, co = n % Co) for
-  // n < 9 Co; its 8 channels are the lane slot co + 16 (lane / 16) of packed
-  // fragment (tap k 9 + ij, chunk, output fragment 0); other columns are zero
+  // weight table: entry e = (k chunks + c) NF + q holds, for lane l, the B
+  // operand of column n = 16 q + l % 16 = (ij = n / Co, co = n % Co), for
+  // n < 9 Co: the lane slot co + 16 (l / 16) of packed fragment (tap
+  // k 9 + ij, chunk c, output fragment 0).  Columns past 9 Co take tap
+  // (0, 0)'s slot: their D is never read.
   const __amdgpu_buffer_rsrc_t wrs = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<u32x4*>(a.wpack), 0, static_cast<int>(a.wpack_bytes), 0x00020000);
   const uint32_t frag_bytes = static_cast<uint32_t>(a.cofrags) * 1024u;
   uint32_t w_off[NF];
-  bool w_ok[NF];
 #pragma unroll
   for (int q = 0; q < NF; ++q) {
     const int col = 16 * q + (lane & 15);
-    w_ok[q] = col < 9 * a.Co;
-    const int ij = w_ok[q] ? col / a.Co : 0, co = w_ok[q] ? col % a.Co : 0;
+    const bool used = col < 9 * a.Co;
+    const int ij = used ? col / a.Co : 0, co = used ? col % a.Co : 0;
     w_off[q] = static_cast<uint32_t>(ij * a.chunks) * frag_bytes +
                static_cast<uint32_t>(co + 16 * (lane >> 4)) * 16u;
   }
@@ -163,17 +193,24 @@ __global__ __launch_bounds__(256, 1) void conv_head(HeadArgs a) {
   // channel 8g + 4h + j / 4 at pixel group 4 (j % 4)
   const int j = lane & 15, g = lane >> 4;
   const int ra = hrow(8 * g + (j >> 2)) + (2 * wave * HC + 4 * (j & 3)) * 2;
-  auto read_a = [&](int buf, int pf) {
-    const unsigned char* p = lds + buf * HBUF + ra + ((pf / (HC / 16)) * HC + (pf % (HC / 16)) * 16) * 2;
+  auto read_a = [&](const unsigned char* L, int pf) __attribute__((always_inline)) {
+    const unsigned char* p = L + ra + ((pf / (HC / 16)) * HC + (pf % (HC / 16)) * 16) * 2;
     const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p));
     const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p + 4 * HPITCH));
     return i16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
   };
 
   f32x4 acc[OG][NF][HPF];
-  float* D = reinterpret_cast<float*>(lds);
   const int64_t plane = static_cast<int64_t>(a.To) * a.hw;
+  const int64_t cs_c = static_cast<int64_t>(a.Tc) * a.hw, cs_x = static_cast<int64_t>(a.T) * a.hw;
+  const int64_t cl = static_cast<int64_t>(a.L) * a.hw;
+  const uint32_t ccs = static_cast<uint32_t>(cl * 2);  // bytes between new-cache channel planes
   int f_done = -1;  // the last source frame staged by an earlier group
+
+  // wait until at most n vector-memory operations of this wave are
+  // outstanding (the LDS and export counters left alone)
+#define C3C_VMCNT(n) __builtin_amdgcn_s_waitcnt(((n) & 15) | (((n) >> 4) << 14) | (7 << 4) | (15 << 8))
+  auto barrier = [] { asm volatile("s_barrier" ::: "memory"); };
 
   for (int og0 = 0; og0 < a.To; og0 += OG) {
     // Source frames of this group's output frames [og0, og0 + OG): the
@@ -185,7 +222,7 @@ __global__ __launch_bounds__(256, 1) void conv_head(HeadArgs a) {
     const int f_top = og1 - 1 + (a.Kt - 1) * a.dt - a.p_l;
     const int f_hi = f_top < a.Z - 1 ? f_top : a.Z - 1;
     const int nst = f_hi >= f_lo ? (f_hi - f_lo + 1) * a.chunks : 0;
-    const int padded = (nst + 1) & ~1;
+    const int padded = (nst + NB - 1) / NB * NB;
 
 #pragma unroll
     for (int u = 0; u < OG; ++u)
@@ -194,160 +231,202 @@ __global__ __launch_bounds__(256, 1) void conv_head(HeadArgs a) {
 #pragma unroll
         for (int pf = 0; pf < HPF; ++pf) acc[u][q][pf] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    // stages in order: (af, ac) = frame and chunk of the next one to load;
-    // (wf, wc) the same for the next weights.  The resource of a stage starts
-    // at channel 32 ac of frame af and ends after the last real channel's
-    // plane (channels past Ci read 0); empty past the last stage.
-    int af = f_lo, ac = 0, wf = f_lo, wc = 0;
-    auto next_rsrc = [&](uint32_t& cs, int& fr, int& c0) {
-      const bool real = af <= f_hi;
-      c0 = ac * HK;
-      fr = af;
+    // Stages run frame by frame, chunk by chunk, from (f_lo, 0); frames past
+    // f_hi are padding.  Two cursors: the window loads and the stage being
+    // computed.
+    // window cursor: frame af, chunk ac; ap = channel 32 ac of frame af
+    int af = f_lo, ac = 0;
+    const uint16_t* ap = a.x;
+    uint32_t acs = 0;     // bytes between the source's channel planes
+    int64_t astep = 0;    // elements between consecutive chunks
+    auto act_frame = [&]() __attribute__((always_inline)) {
       const bool in_cache = af < a.Tc;
       const int64_t cstride = in_cache ? cs_c : cs_x;
-      const uint16_t* base = in_cache ? a.cache : a.x;
-      const int64_t off = real ? static_cast<int64_t>(in_cache ? af : af - a.Tc) * a.hw +
-                                     (static_cast<int64_t>(n) * a.Ci + c0) * cstride
-                               : 0;
-      int64_t bytes = ((a.Ci - 1 - c0) * cstride + a.hw) * 2;
-      if (!real || bytes < 0) bytes = 0;
-      if (bytes > 0x7fffffff) bytes = 0x7fffffff;
-      cs = static_cast<uint32_t>(cstride * 2);
+      ap = af <= f_hi ? (in_cache ? a.cache + static_cast<int64_t>(af) * a.hw
+                                  : a.x + static_cast<int64_t>(af - a.Tc) * a.hw) +
+                            static_cast<int64_t>(n) * a.Ci * cstride
+                      : a.x;
+      acs = static_cast<uint32_t>(cstride * 2);
+      astep = HK * cstride;
+    };
+    // the window loads of the cursor's stage into buffer L; the source is
+    // bounded after the chunk's last real channel (channels past Ci read 0),
+    // empty past the last frame
+    auto issue_act = [&](unsigned char* L) __attribute__((always_inline)) {
+      const int c0 = ac * HK;
+      const uint32_t bytes = af <= f_hi ? static_cast<uint32_t>(min(HK, a.Ci - c0) - 1) * acs +
+                                              static_cast<uint32_t>(a.hw) * 2u
+                                        : 0u;
+      const __amdgpu_buffer_rsrc_t rs =
+          __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(ap), 0, static_cast<int>(bytes), 0x00020000);
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void*)(L + lrow + i * HPITCH), 16,
+                                                 s_px + static_cast<uint32_t>(ch0 + i) * acs, 0, 0, 0);
       if (++ac == a.chunks) {
         ac = 0;
         ++af;
+        act_frame();
+      } else {
+        ap += astep;
       }
-      return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(base + off), 0,
-                                               static_cast<int>(bytes), 0x00020000);
     };
-    // Where a stage's frame goes in the new cache: a frame of the new cache
-    // staged for the first time (workgroup-uniform) has its interior segments
-    // written to cache_out, when the staged values are stored to LDS, through
-    // a resource that ends after the last real channel.
-    struct CacheDst {
-      __amdgpu_buffer_rsrc_t rs;
-      uint32_t cs;
-      bool on;
-    };
-    const uint32_t ccs = static_cast<uint32_t>(static_cast<int64_t>(a.L) * a.hw * 2);
-    // the activations of the next stage
-    auto load_act = [&](u32x4 (&v)[HSPT], CacheDst& cd) {
-      uint32_t cs;
-      int fr, c0;
-      const __amdgpu_buffer_rsrc_t rs = next_rsrc(cs, fr, c0);
-#pragma unroll
-      for (int i = 0; i < HSPT; ++i)
-        v[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
-                                             rs, s_px[i] == OOB ? OOB : s_ch[i] * cs + s_px[i], 0, 0));
-      cd.on = a.write_cache && fr <= f_hi && fr > f_done && fr >= a.Z - a.L;
-      const int64_t cl = static_cast<int64_t>(a.L) * a.hw;
-      uint16_t* cb = a.cache_out + (cd.on ? (static_cast<int64_t>(n) * a.Ci + c0) * cl +
-                                                static_cast<int64_t>(fr - (a.Z - a.L)) * a.hw
-                                          : 0);
-      int64_t cbytes = ((a.Ci - 1 - c0) * cl + a.hw) * 2;
-      if (!cd.on || cbytes < 0) cbytes = 0;
-      if (cbytes > 0x7fffffff) cbytes = 0x7fffffff;
-      cd.rs = __builtin_amdgcn_make_buffer_rsrc(cb, 0, static_cast<int>(cbytes), 0x00020000);
-    };
-    // the weights of the next stage for each output frame of the group: tap
-    // k = (f + p_l - o) / d_t when that is a whole tap index, else zeros (and
-    // the frame's products are skipped: tap_ok)
-    auto load_w = [&](u32x4 (&v)[OG][NF], bool (&ok)[OG]) {
-      const bool real = wf <= f_hi;
+    // compute cursor: frame cf, chunk cc; per output frame u of the group
+    // the table offset of its tap's entries (tap k = (f + p_l - o) / d_t
+    // when that is a whole tap index; otherwise its products are skipped:
+    // bit u of wok clear, offset 0)
+    int cf = f_lo, cc = 0;
+    uint32_t wb[OG], wok = 0;
+    auto c_frame = [&]() __attribute__((always_inline)) {
+      wok = 0;
 #pragma unroll
       for (int u = 0; u < OG; ++u) {
-        const int o = og0 + u, kd = wf + a.p_l - o;
+        const int o = og0 + u, kd = cf + a.p_l - o;
         const int k = kd >= 0 ? kd / a.dt : -1;
-        ok[u] = real && o < og1 && kd >= 0 && kd % a.dt == 0 && k < a.Kt;
-        const uint32_t base = static_cast<uint32_t>((ok[u] ? k : 0) * 9 * a.chunks + wc) * frag_bytes;
-#pragma unroll
-        for (int q = 0; q < NF; ++q)
-          v[u][q] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
-                                                  wrs, ok[u] && w_ok[q] ? base + w_off[q] : OOB, 0, 0));
-      }
-      if (++wc == a.chunks) {
-        wc = 0;
-        ++wf;
+        const bool ok = cf <= f_hi && o < og1 && kd >= 0 && kd % a.dt == 0 && k < a.Kt;
+        wb[u] = ok ? static_cast<uint32_t>(k * a.chunks * NF) * 1024u : 0u;
+        wok |= (ok ? 1u : 0u) << u;
       }
     };
-    auto store_act = [&](const u32x4 (&v)[HSPT], const CacheDst& cd, int buf) {
+    auto c_next = [&]() __attribute__((always_inline)) {
+      if (++cc == a.chunks) {
+        cc = 0;
+        ++cf;
+        c_frame();
+      } else {
 #pragma unroll
-      for (int i = 0; i < HSPT; ++i) *reinterpret_cast<u32x4*>(lds + buf * HBUF + s_lds[i]) = v[i];
-      if (cd.on) {
+        for (int u = 0; u < OG; ++u) wb[u] += (wok >> u) & 1u ? NF * 1024u : 0u;
+      }
+    };
+    // A frame of the new cache staged for the first time (workgroup-uniform)
+    // has its interior segments copied from the stage buffer to cache_out,
+    // through a resource that ends after the chunk's last real channel.
+    // Returns whether it stored (8 stores a lane).
+    auto copy_cache = [&](const unsigned char* L) __attribute__((always_inline)) {
+      const bool on = a.write_cache && cf <= f_hi && cf > f_done && cf >= a.Z - a.L;
+      if (on) {
+        const int c0 = cc * HK;
+        const uint32_t cbytes = static_cast<uint32_t>(min(HK, a.Ci - c0) - 1) * ccs + static_cast<uint32_t>(a.hw) * 2u;
+        const __amdgpu_buffer_rsrc_t crs = __builtin_amdgcn_make_buffer_rsrc(
+            a.cache_out + (static_cast<int64_t>(n) * a.Ci + c0) * cl + static_cast<int64_t>(cf - (a.Z - a.L)) * a.hw,
+            0, static_cast<int>(cbytes), 0x00020000);
+        u32x4 v[8];
 #pragma unroll
-        for (int i = 0; i < HSPT; ++i)
-          __builtin_amdgcn_raw_buffer_store_b128(v[i], cd.rs, s_in[i] ? s_ch[i] * ccs + s_px[i] : OOB,
+        for (int i = 0; i < 8; ++i) v[i] = *reinterpret_cast<const u32x4*>(L + lrow + i * HPITCH + lane * 16);
+#pragma unroll
+        for (int i = 0; i < 8; ++i)
+          __builtin_amdgcn_raw_buffer_store_b128(v[i], crs, s_in ? static_cast<uint32_t>(ch0 + i) * ccs + s_px : OOB,
                                                  0, 0);
       }
+      return on;
     };
 
-    u32x4 act0[HSPT], act1[HSPT];
-    CacheDst cd0, cd1;
-    u32x4 w0v[OG][NF], w1v[OG][NF];
-    bool ok0[OG], ok1[OG];
-    load_w(w0v, ok0);
-    load_act(act0, cd0);
-    load_act(act1, cd1);
-    store_act(act0, cd0, 0);
-    __syncthreads();
-
-    // one stage: weights of s + 1 and activations of s + 2 issued, the
-    // products of s for every output frame it feeds, then s + 1's
-    // activations into the other buffer (last read in stage s - 1, before
-    // its barrier)
-    auto stage = [&](int buf, const u32x4 (&w_cur)[OG][NF], const bool (&ok_cur)[OG],
-                     u32x4 (&w_nxt)[OG][NF], bool (&ok_nxt)[OG], u32x4 (&a_free)[HSPT],
-                     CacheDst& c_free, const u32x4 (&a_next)[HSPT], const CacheDst& c_next) {
-      load_w(w_nxt, ok_nxt);
-      load_act(a_free, c_free);
+    // one stage from buffer B: the cache copy, the window loads of stage
+    // s + NB - 1 into buffer (B + NB - 1) % NB, the B operands from the
+    // table and the products of every output frame the stage feeds, then
+    // this wave's loads of stage s + 1 awaited and one barrier.  After those
+    // loads the wave issued, in each of its last NB - 2 stages, 8 stores if
+    // it copied cache and 8 window loads; sth has a bit per such stage that
+    // stored, so the wait is exact and later loads stay in flight.
+    uint32_t sth = 0;
+    constexpr uint32_t sth_mask = NB == 4 ? 3u : 1u;
+    auto stage = [&](auto B) __attribute__((always_inline)) {
+      constexpr int b0 = decltype(B)::value, bn = (b0 + AHEAD) % NB;
+      const unsigned char* cur = bufp(b0);
+      sth = ((sth << 1) | (copy_cache(cur) ? 1u : 0u)) & sth_mask;
+      issue_act(bufp(bn));
+      u32x4 bv[OG][NF];
+#pragma unroll
+      for (int u = 0; u < OG; ++u)
+#pragma unroll
+        for (int q = 0; q < NF; ++q)
+          bv[u][q] = *reinterpret_cast<const u32x4*>(wtab + wb[u] + q * 1024 + lane * 16);
       i16x8 av[HPF];
 #pragma unroll
-      for (int pf = 0; pf < HPF; ++pf) av[pf] = read_a(buf, pf);
+      for (int pf = 0; pf < HPF; ++pf) av[pf] = read_a(cur, pf);
 #pragma unroll
       for (int u = 0; u < OG; ++u) {
-        if (!ok_cur[u]) continue;  // workgroup-uniform
+        if (!((wok >> u) & 1u)) continue;  // workgroup-uniform
 #pragma unroll
         for (int pf = 0; pf < HPF; ++pf)
 #pragma unroll
           for (int q = 0; q < NF; ++q)
             acc[u][q][pf] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                __builtin_bit_cast(bf16x8, av[pf]), __builtin_bit_cast(bf16x8, w_cur[u][q]), acc[u][q][pf],
-                0, 0, 0);
+                __builtin_bit_cast(bf16x8, av[pf]), __builtin_bit_cast(bf16x8, bv[u][q]), acc[u][q][pf], 0, 0, 0);
       }
-      store_act(a_next, c_next, buf ^ 1);
-      __syncthreads();
+      c_next();
+      if (sth == 0)
+        C3C_VMCNT((AHEAD - 1) * 8);
+      else if (sth == 3)
+        C3C_VMCNT((AHEAD - 1) * 8 + 16);
+      else
+        C3C_VMCNT((AHEAD - 1) * 8 + 8);
+      barrier();
     };
-    for (int s = 0; s < padded; s += 2) {
-      stage(0, w0v, ok0, w1v, ok1, act0, cd0, act1, cd1);
-      stage(1, w1v, ok1, w0v, ok0, act1, cd1, act0, cd0);
+
+    // prologue: the weight table (first group only), then stages
+    // 0 .. NB - 2 into buffers 0 .. NB - 2
+    if (og0 == 0) {
+      const int nent = a.Kt * a.chunks * NF;
+      for (int e = wave; e < nent; e += 4) {
+        const int q = e % NF, kc = e / NF;
+        const uint32_t base = static_cast<uint32_t>((kc / a.chunks) * 9 * a.chunks + kc % a.chunks) * frag_bytes;
+        const uint32_t vo = base + w_off[q];  // (a named offset: the host pass drops the kernel
+                                              // when this builtin's argument indexes w_off)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(wrs, (lds_void*)(wtab + e * 1024), 16, vo, 0, 0, 0);
+      }
     }
+    act_frame();
+    c_frame();
+    issue_act(lds0);
+    issue_act(lds1);
+    if constexpr (NB == 4) issue_act(lds2);
+    C3C_VMCNT((AHEAD - 1) * 8);  // the table and stage 0 have landed
+    barrier();
+    for (int s = 0; s < padded; s += NB) {
+      stage(IC<0>{});
+      stage(IC<1>{});
+      stage(IC<2>{});
+      if constexpr (NB == 4) stage(IC<3>{});
+    }
+    // the loads issued past the last stage (zeros) land before LDS is reused
+    C3C_VMCNT(0);
+    barrier();
     f_done = f_hi;
 
-    // per output frame of the group: D[n][window pixel] in fp32 over the
-    // stage buffers (lane l holds pixels 4 (l / 16) .. + 3 of column
+    // per batch of FB output frames of the group: D[n][window pixel] in
+    // fp32, column fragment q of the batch's frame du in stage buffer
+    // NF du + q (lane l holds pixels 4 (l / 16) .. + 3 of column
     // 16 q + l % 16 of each fragment), then the gather: output (co, row r,
     // columns 4 c4 .. + 3) sums D[(i j) Co + co] at window row r + i, window
     // columns 7 + 4 c4 + j .. + 3; bias once, one round-to-nearest-even,
     // 8-byte NCTHW store
+    constexpr int FB = NB / NF;  // output frames per batch
+    constexpr int ITEMS = OR * (OC / 4);  // 4-column output groups per (frame, co)
 #pragma unroll
-    for (int u = 0; u < OG; ++u) {
-      const int o = og0 + u;
-      if (o >= og1) break;
+    for (int u0 = 0; u0 < OG; u0 += FB) {
+      if (og0 + u0 >= og1) break;
 #pragma unroll
-      for (int q = 0; q < NF; ++q) {
-        const int col = 16 * q + (lane & 15);
-        if (col >= 9 * a.Co) continue;
+      for (int du = 0; du < FB && u0 + du < OG; ++du) {
+        if (og0 + u0 + du >= og1) break;
 #pragma unroll
-        for (int pf = 0; pf < HPF; ++pf) {
-          const int px = (2 * wave + pf / (HC / 16)) * HC + (pf % (HC / 16)) * 16 + 4 * g;
-          *reinterpret_cast<f32x4*>(D + col * DPITCH + px) = acc[u][q][pf];
+        for (int q = 0; q < NF; ++q) {
+          if (16 * q + (lane & 15) >= 9 * a.Co) continue;
+          float* Dq = reinterpret_cast<float*>(bufp(NF * du + q)) + (lane & 15) * DPITCH;
+#pragma unroll
+          for (int pf = 0; pf < HPF; ++pf) {
+            const int px = (2 * wave + pf / (HC / 16)) * HC + (pf % (HC / 16)) * 16 + 4 * g;
+            *reinterpret_cast<f32x4*>(Dq + px) = acc[u0 + du][q][pf];
+          }
         }
       }
       __syncthreads();
-      for (int t = tid; t < a.Co * OR * (OC / 4); t += 256) {
-        const int co = t / (OR * (OC / 4)), rem = t % (OR * (OC / 4));
+      const int nfr = min(FB, og1 - og0 - u0);
+      for (int t = tid; t < nfr * a.Co * ITEMS; t += 256) {
+        const int du = t / (a.Co * ITEMS), t2 = t % (a.Co * ITEMS);
+        const int co = t2 / ITEMS, rem = t2 % ITEMS;
         const int r = rem / (OC / 4), c4 = rem % (OC / 4);
-        const int h = h0 + r, w = w0 + 4 * c4;
+        const int h = h0 + r, w = w0 + 4 * c4, o = og0 + u0 + du;
         if (h >= a.H || w >= a.W) continue;
         const float bb = a.has_bias ? __uint_as_float(static_cast<uint32_t>(a.bias[co]) << 16) : 0.f;
         float s4[4] = {bb, bb, bb, bb};
@@ -355,7 +434,9 @@ __global__ __launch_bounds__(256, 1) void conv_head(HeadArgs a) {
         for (int i = 0; i < 3; ++i)
 #pragma unroll
           for (int jj = 0; jj < 3; ++jj) {
-            const float* src = D + ((i * 3 + jj) * a.Co + co) * DPITCH + (r + i) * HC + 7 + 4 * c4 + jj;
+            const int col = (i * 3 + jj) * a.Co + co;
+            const float* src = reinterpret_cast<const float*>(bufp(NF * du + (col >> 4))) + (col & 15) * DPITCH +
+                               (r + i) * HC + 7 + 4 * c4 + jj;
 #pragma unroll
             for (int e = 0; e < 4; ++e) s4[e] += src[e];
           }
@@ -365,9 +446,10 @@ __global__ __launch_bounds__(256, 1) void conv_head(HeadArgs a) {
                         static_cast<int64_t>(h) * a.W + w;
         *reinterpret_cast<uint2*>(dst) = make_uint2(v01, v23);
       }
-      __syncthreads();  // D is rewritten by the next frame, the stage buffers by the next group
+      __syncthreads();  // D is rewritten by the next batch, the stage buffers by the next group
     }
   }
+#undef C3C_VMCNT
 }
 
 bool aligned_to(const void* p, uintptr_t m) { return (reinterpret_cast<uintptr_t>(p) & (m - 1)) == 0; }
@@ -376,7 +458,8 @@ bool aligned_to(const void* p, uintptr_t m) { return (reinterpret_cast<uintptr_t
 
 bool head_eligible(const Geo& g, const void* x, const void* cache, const void* y) {
   const c3c_conv_desc& d = g.d;
-  if (d.Co > max_co(3) || d.W % 8 != 0) return false;
+  // the weight table must fit beside three stage buffers
+  if (d.Co > max_co(3) || d.W % 8 != 0 || head_table_entries(d) > wtab_entries(3)) return false;
   // buffer offsets are 32-bit: one 32-channel slab of a source frame and the
   // packed weights must fit
   const int64_t frames = d.T > d.Tc ? d.T : d.Tc;
@@ -444,15 +527,23 @@ hipError_t launch_head(const Geo& g, const void* x, const void* cache, const voi
   if (blocks > 0x7fffffff) return hipErrorInvalidConfiguration;
   a.nblocks = static_cast<int>(blocks);
   const int nf = static_cast<int>((9 * d.Co + 15) / 16);
+  const bool nb4 = head_table_entries(d) <= wtab_entries(4);
   const dim3 grid(static_cast<unsigned>(blocks)), block(256);
   // output frames per group: 4 (the 256 accumulator registers of 4 frames x
-  // 2 fragments x 8 pixel fragments), 2 with three column fragments
-  if (nf == 1)
-    hipLaunchKernelGGL((conv_head<1, 4>), grid, block, 0, s, a);
+  // 2 fragments x 8 pixel fragments), 2 with three column fragments; four
+  // stage buffers when the weight table fits beside them, else three
+  if (nf == 1 && nb4)
+    hipLaunchKernelGGL((conv_head<1, 4, 4>), grid, block, 0, s, a);
+  else if (nf == 1)
+    hipLaunchKernelGGL((conv_head<1, 4, 3>), grid, block, 0, s, a);
+  else if (nf == 2 && nb4)
+    hipLaunchKernelGGL((conv_head<2, 4, 4>), grid, block, 0, s, a);
   else if (nf == 2)
-    hipLaunchKernelGGL((conv_head<2, 4>), grid, block, 0, s, a);
+    hipLaunchKernelGGL((conv_head<2, 4, 3>), grid, block, 0, s, a);
+  else if (nb4)
+    hipLaunchKernelGGL((conv_head<3, 2, 4>), grid, block, 0, s, a);
   else
-    hipLaunchKernelGGL((conv_head<3, 2>), grid, block, 0, s, a);
+    hipLaunchKernelGGL((conv_head<3, 2, 3>), grid, block, 0, s, a);
   return hipGetLastError();
 }
 

@@ -342,8 +342,9 @@ def test_tap1x1_kernel_matches_oracle(over):
 # The head kernel (Co <= 5, W a multiple of 8): the 9 spatial taps x Co as
 # matrix-core columns, then a 3x3 gather-sum.  Every Co it serves, ragged
 # rows (H not a multiple of the 6-row tile) and columns (W not a multiple of
-# 64), a channel-chunk tail, dilation, p_l < 0, no cache, N = 2, Kt = 2, and
-# more output frames than one pass of the kernel takes.
+# 64), a channel-chunk tail, dilation, p_l < 0, no cache, N = 2, Kt = 2,
+# more output frames than one pass of the kernel takes, and weight tables
+# that take the three-buffer form.
 HEAD_CASES = [
     dict(N=1, Ci=96, Co=3, T=4, Tc=2, H=37, W=136),
     dict(N=1, Ci=40, Co=1, T=2, Tc=2, H=20, W=72),
@@ -356,6 +357,10 @@ HEAD_CASES = [
     # fragments): the new cache written by the group that first stages it
     dict(N=1, Ci=40, Co=3, T=6, Tc=2, H=14, W=56),
     dict(N=2, Ci=36, Co=5, T=5, Tc=2, H=9, W=48),
+    # weight tables too large for four stage buffers: the three-buffer form
+    # (3 x 3 x 3 = 27 entries; 3 x 5 x 2 = 30 with a channel-chunk tail)
+    dict(N=1, Ci=96, Co=5, T=3, Tc=2, H=13, W=48),
+    dict(N=1, Ci=150, Co=3, T=4, Tc=2, H=16, W=104),
 ]
 
 

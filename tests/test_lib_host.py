@@ -451,6 +451,24 @@ def test_plan_of_the_160_channel_parity_cases():
 
 
 @no_gpu
+def test_head_kernel_takes_calls_whose_weight_table_fits():
+    """The head kernel gathers its B operands into an LDS table of
+    Kt x chunks x column-fragment entries (1 KiB each) beside its stage
+    buffers: up to 26 entries beside four, 59 beside three.  A call whose
+    table fits neither goes to the 3x3 kernel's 16-channel tile."""
+    def kern(**over):
+        return c3c.plan_query(None, spec(**over), "bf16")["kernel"]
+    assert kern(N=1, Ci=96, Co=3, T=4, Tc=2, H=24, W=64) == "head"     # 3 x 3 x 2 = 18
+    assert kern(N=1, Ci=96, Co=5, T=3, Tc=2, H=24, W=64) == "head"     # 3 x 3 x 3 = 27
+    assert kern(N=1, Ci=192, Co=5, T=3, Tc=2, H=24, W=64) == "head"    # 3 x 6 x 3 = 54
+    assert kern(N=1, Ci=224, Co=5, T=3, Tc=2, H=24, W=64) == "conv3d_bf16"  # 63
+    assert kern(N=1, Ci=288, Co=3, T=3, Tc=2, H=24, W=64) == "head"    # 3 x 9 x 2 = 54
+    assert kern(N=1, Ci=320, Co=3, T=3, Tc=2, H=24, W=64) == "conv3d_bf16"  # 60
+    assert kern(N=1, Ci=608, Co=1, T=3, Tc=2, H=24, W=64) == "head"    # 3 x 19 x 1 = 57
+    assert kern(N=1, Ci=640, Co=1, T=3, Tc=2, H=24, W=64) == "conv3d_bf16"  # 60
+
+
+@no_gpu
 def test_noalloc_refuses_an_oversized_split_before_device_work():
     ctx = c3c.Context()
     big = spec(N=1, Ci=384, Co=192, T=1, Tc=2, H=184, W=160)
