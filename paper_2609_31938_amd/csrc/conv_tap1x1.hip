@@ -139,30 +139,43 @@ __global__ __launch_bounds__(256, 2) void conv_tap1x1(TapArgs a) {
   const int padded = (nst + 1) & ~1;
 
   // activation stages are loaded in order: (ak, ac) is the tap and channel
-  // chunk of the next one.  Its source is a buffer resource from channel
-  // 32 ac of frame f_ak (pixel px0) to the end of the last real channel's
-  // row, empty past the last stage.
+  // chunk of the next one, ap its channel 32 ac of frame f_ak at pixel px0.
+  // The pointer steps by one chunk per stage and only a new tap recomputes
+  // it (a stage's scalar work is a few additions).  Its source is a buffer
+  // resource that ends after the chunk's last real channel's row (32-bit:
+  // a 32-channel slab fits), empty past the last stage.
   const int64_t cs_c = static_cast<int64_t>(a.Tc) * a.hw, cs_x = static_cast<int64_t>(a.T) * a.hw;
   int ak = k_lo, ac = 0;
-  auto next_rsrc = [&](uint32_t& cs) {
-    const bool real = ak <= k_hi;
-    const int c0 = ac * TK;
+  const uint16_t* ap = a.x;
+  uint32_t acs = 0;   // bytes between the source's channel planes
+  int64_t astep = 0;  // elements between consecutive chunks
+  auto act_tap = [&]() __attribute__((always_inline)) {
+    if (ak > k_hi) return;
     const int f = t * a.st + ak * a.dt - a.p_l;
     const bool in_cache = f < a.Tc;
     const int64_t cstride = in_cache ? cs_c : cs_x;
-    const uint16_t* base = in_cache ? a.cache : a.x;
-    const int64_t off = static_cast<int64_t>(in_cache ? f : f - a.Tc) * a.hw +
-                        static_cast<int64_t>(n) * a.Ci * cstride + px0 + c0 * cstride;
-    int64_t bytes = ((a.Ci - 1 - c0) * cstride + a.hw - px0) * 2;
-    if (!real || bytes < 0) bytes = 0;
-    if (bytes > 0x7fffffff) bytes = 0x7fffffff;
-    cs = static_cast<uint32_t>(cstride * 2);
+    ap = (in_cache ? a.cache + static_cast<int64_t>(f) * a.hw : a.x + static_cast<int64_t>(f - a.Tc) * a.hw) +
+         static_cast<int64_t>(n) * a.Ci * cstride + px0;
+    acs = static_cast<uint32_t>(cstride * 2);
+    astep = TK * cstride;
+  };
+  act_tap();
+  auto next_rsrc = [&](uint32_t& cs) __attribute__((always_inline)) {
+    const bool real = ak <= k_hi;
+    const uint32_t bytes = real ? static_cast<uint32_t>(min(TK, a.Ci - ac * TK) - 1) * acs +
+                                      static_cast<uint32_t>(a.hw - px0) * 2u
+                                : 0u;
+    const __amdgpu_buffer_rsrc_t rs =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(ap), 0, static_cast<int>(bytes), 0x00020000);
+    cs = acs;
     if (++ac == a.chunks) {
       ac = 0;
       ++ak;
+      act_tap();
+    } else {
+      ap += astep;
     }
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(real ? base + off : base), 0,
-                                             static_cast<int>(bytes), 0x00020000);
+    return rs;
   };
 
   // staging: segment q = tid + 256 i of the tile -> channel row q / 16,
@@ -182,16 +195,21 @@ __global__ __launch_bounds__(256, 2) void conv_tap1x1(TapArgs a) {
     for (int i = 0; i < TSPT; ++i)
       v[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, s_row[i] * cs + s_px[i], 0, 0));
   };
-  // stage q's activations into LDS buffer buf; a stage whose frame goes to
-  // the new cache [N][Ci][L][H*W] (frame f is its frame f - (Z - L)) is
-  // also written there from the same registers (the chunk's real rows,
-  // pixels inside the plane)
+  // the next stage's activations (stages are stored in order: tap sk,
+  // chunk sc) into LDS buffer buf; a stage whose frame goes to the new cache
+  // [N][Ci][L][H*W] (frame f is its frame f - (Z - L)) is also written there
+  // from the same registers (the chunk's real rows, pixels inside the plane)
   const int64_t cl = static_cast<int64_t>(a.L) * a.hw;
-  auto store_act = [&](const u32x4 (&v)[TSPT], int buf, int q) {
+  int sk = k_lo, sc = 0;
+  auto store_act = [&](const u32x4 (&v)[TSPT], int buf) __attribute__((always_inline)) {
 #pragma unroll
     for (int i = 0; i < TSPT; ++i) *reinterpret_cast<u32x4*>(lds + buf * TBUF + s_lds[i]) = v[i];
-    const int k = k_lo + q / a.chunks, c0 = (q % a.chunks) * TK;
-    if (cwk != 0 && q < nst && ((cwk >> k) & 1u)) {
+    const int k = sk, c0 = sc * TK;
+    if (++sc == a.chunks) {
+      sc = 0;
+      ++sk;
+    }
+    if (cwk != 0 && k <= k_hi && ((cwk >> k) & 1u)) {
       const int f = t * a.st + k * a.dt - a.p_l;
       const uint32_t ccs = static_cast<uint32_t>(cl * 2);
       const uint32_t cbytes = static_cast<uint32_t>(min(TK, a.Ci - c0) - 1) * ccs + static_cast<uint32_t>(a.hw) * 2u;
@@ -217,14 +235,19 @@ __global__ __launch_bounds__(256, 2) void conv_tap1x1(TapArgs a) {
   for (int cf = 0; cf < WCO; ++cf)
     w_off[cf] = static_cast<uint32_t>(min(ctile * (TCO / 16) + wco * WCO + cf, a.cofrags - 1)) * 1024u +
                 static_cast<uint32_t>(lane) * 16u;
-  auto load_w = [&](int s, u32x4 (&v)[WCO]) {
-    // stage s is tap k_lo + s / chunks, chunk s % chunks: packed row k_lo * chunks + s
-    const bool real = s < nst;
-    const uint32_t row = static_cast<uint32_t>((k_lo * a.chunks + s) * a.cofrags) * 1024u;
+  // weights are loaded in order: stage ws is tap k_lo + ws / chunks, chunk
+  // ws % chunks, packed row k_lo * chunks + ws (wrow its byte offset)
+  int ws = 0;
+  uint32_t wrow = static_cast<uint32_t>(k_lo * a.chunks * a.cofrags) * 1024u;
+  const uint32_t wstep = static_cast<uint32_t>(a.cofrags) * 1024u;
+  auto load_w = [&](u32x4 (&v)[WCO]) __attribute__((always_inline)) {
+    const bool real = ws < nst;
 #pragma unroll
     for (int cf = 0; cf < WCO; ++cf)
       v[cf] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
-                                            wrs, real ? row + w_off[cf] : OOB, 0, 0));
+                                            wrs, real ? wrow + w_off[cf] : OOB, 0, 0));
+    ++ws;
+    wrow += wstep;
   };
 
   // transposing operand read: within each 16-lane block (channel group
@@ -250,19 +273,19 @@ __global__ __launch_bounds__(256, 2) void conv_tap1x1(TapArgs a) {
   // stage 0 into LDS buffer 0
   u32x4 act0[TSPT], act1[TSPT];
   u32x4 w0[WCO], w1[WCO];
-  load_w(0, w0);
+  load_w(w0);
   load_act(act0);
   load_act(act1);
-  store_act(act0, 0, 0);
+  store_act(act0, 0);
   __syncthreads();
 
   // one stage: weights of s + 1 and activations of s + 2 issued (their
   // register sets were consumed in stage s - 1), the products of s, then
   // s + 1's activations into the other buffer (last read in stage s - 1,
   // before its barrier)
-  auto stage = [&](int s, int buf, const u32x4 (&w_cur)[WCO], u32x4 (&w_nxt)[WCO], u32x4 (&a_free)[TSPT],
+  auto stage = [&](int buf, const u32x4 (&w_cur)[WCO], u32x4 (&w_nxt)[WCO], u32x4 (&a_free)[TSPT],
                    const u32x4 (&a_next)[TSPT]) {
-    load_w(s + 1, w_nxt);
+    load_w(w_nxt);
     load_act(a_free);
     i16x8 av[NPF];
 #pragma unroll
@@ -273,12 +296,12 @@ __global__ __launch_bounds__(256, 2) void conv_tap1x1(TapArgs a) {
       for (int cf = 0; cf < WCO; ++cf)
         acc[cf][pf] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
             __builtin_bit_cast(bf16x8, av[pf]), __builtin_bit_cast(bf16x8, w_cur[cf]), acc[cf][pf], 0, 0, 0);
-    store_act(a_next, buf ^ 1, s + 1);
+    store_act(a_next, buf ^ 1);
     __syncthreads();
   };
   for (int s = 0; s < padded; s += 2) {
-    stage(s, 0, w0, w1, act0, act1);
-    stage(s + 1, 1, w1, w0, act1, act0);
+    stage(0, w0, w1, act0, act1);
+    stage(1, w1, w0, act1, act0);
   }
 
   // epilogue: lane l holds pixels 4 (l / 16) .. + 3 of output channel l % 16
