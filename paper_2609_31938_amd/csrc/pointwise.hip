@@ -416,6 +416,7 @@ constexpr int PW_RES_W = 10 * 1024 * kResidentChunks;  // resident weight bytes 
 
 template <bool F16, int PD>
 __global__ __launch_bounds__(PW_NT, 1) void pointwise_resident(PwArgs a, int tiles_total) {
+  static_assert(PD % 2 == 0, "the two LDS buffers alternate within one pass over the ring");
   constexpr int NPF = 4, PX = pw_px(NPF), PITCH = pw_pitch(NPF), SEG = PX / 128;
   constexpr int ABUF = pw_row(NPF, PW_K);  // one activation stage
   __shared__ __align__(16) unsigned char lds[PW_RES_W + 2 * ABUF];
@@ -445,46 +446,53 @@ __global__ __launch_bounds__(PW_NT, 1) void pointwise_resident(PwArgs a, int til
                     static_cast<int>(gridDim.x);
   const int nst = ntile * chunks;  // stages: tile outer, chunk inner
   const int64_t cs_x = static_cast<int64_t>(a.T) * a.hw, cs_c = static_cast<int64_t>(a.Tc) * a.hw;
-  struct Src {
-    __amdgpu_buffer_rsrc_t rs;
-    uint32_t cs;
-  };
-  // stage g: tile blockIdx.x + (g / chunks) gridDim.x, chunk g % chunks;
-  // past the last stage, and for an output frame whose one tap reads no
-  // frame of Z (Eq. 4: a left pad past the cache, or a right pad), an
-  // empty resource (zeros: the output is the bias alone)
-  auto src_of = [&](int g) {
-    const bool real = g < nst;
-    const int t = static_cast<int>(blockIdx.x) + (real ? g / chunks : 0) * static_cast<int>(gridDim.x);
-    const int c0 = (real ? g % chunks : 0) * PW_K;
+  // Stages are loaded in order: stage g = lt chunks + lc is chunk lc of this
+  // workgroup's tile lt (tile blockIdx.x + lt gridDim.x).  The source pointer
+  // (channel 32 lc of the tile's frame, pixel px0) steps by one chunk per
+  // stage; a new tile recomputes it (the divisions happen once per tile).
+  // Its resource ends after the chunk's last real channel's row (32-bit: a
+  // 32-channel slab fits).  Past the last stage, and for an output frame
+  // whose one tap reads no frame of Z (Eq. 4: a left pad past the cache, or
+  // a right pad), the resource is empty (zeros: the output is the bias alone).
+  int lt = 0, lc = 0;
+  const uint16_t* lp = a.x;
+  uint32_t lcs = 0, lpx = 0;  // bytes between channel planes; pixel bytes left in the plane
+  int64_t lstep = 0;          // elements between consecutive chunks
+  bool lact = false;
+  auto l_tile = [&]() __attribute__((always_inline)) {
+    const int t = static_cast<int>(blockIdx.x) + lt * static_cast<int>(gridDim.x);
     const int pt = t % a.px_tiles, nt = t / a.px_tiles;
     const int o = nt % a.To, n = nt / a.To;
     const int f = o * a.st - a.p_l;  // Kt = 1: the one tap's source frame
-    const bool active = real && f >= 0 && f < a.Z;
-    const bool in_cache = active && f < a.Tc;
+    lact = lt < ntile && f >= 0 && f < a.Z;
+    const bool in_cache = lact && f < a.Tc;
     const int64_t cstride = in_cache ? cs_c : cs_x;
-    const uint16_t* base = in_cache ? a.cache : a.x;
     const int64_t px0 = static_cast<int64_t>(pt) * PX;
-    const int64_t off = active ? static_cast<int64_t>(in_cache ? f : f - a.Tc) * a.hw +
-                                     static_cast<int64_t>(n) * a.Ci * cstride + px0 + c0 * cstride
-                               : 0;
-    int64_t bytes = ((a.Ci - 1 - c0) * cstride + a.hw - px0) * 2;
-    if (!active || bytes < 0) bytes = 0;
-    if (bytes > 0x7fffffff) bytes = 0x7fffffff;
-    Src r;
-    r.rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(base + off), 0,
-                                             static_cast<int>(bytes), 0x00020000);
-    r.cs = static_cast<uint32_t>(cstride * 2);
-    return r;
+    lp = lact ? (in_cache ? a.cache + static_cast<int64_t>(f) * a.hw : a.x + static_cast<int64_t>(f - a.Tc) * a.hw) +
+                    static_cast<int64_t>(n) * a.Ci * cstride + px0
+              : a.x;
+    lcs = static_cast<uint32_t>(cstride * 2);
+    lpx = lact ? static_cast<uint32_t>(a.hw - px0) * 2u : 0u;
+    lstep = PW_K * cstride;
   };
+  l_tile();
   const int sch = tid >> 4, spx = (tid & 15) * 8;
   const int slds = pw_row(NPF, sch) + spx * 2;
-  auto load = [&](int g, u32x4 (&x)[SEG]) {
-    const Src sr = src_of(g);
-    const uint32_t soff = static_cast<uint32_t>(sch) * sr.cs + static_cast<uint32_t>(spx) * 2u;
+  auto load = [&](u32x4 (&x)[SEG]) __attribute__((always_inline)) {
+    const uint32_t bytes = lact ? static_cast<uint32_t>(min(PW_K, a.Ci - lc * PW_K) - 1) * lcs + lpx : 0u;
+    const __amdgpu_buffer_rsrc_t rs =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(lp), 0, static_cast<int>(bytes), 0x00020000);
+    const uint32_t soff = static_cast<uint32_t>(sch) * lcs + static_cast<uint32_t>(spx) * 2u;
 #pragma unroll
     for (int h = 0; h < SEG; ++h)
-      x[h] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(sr.rs, soff + 256u * h, 0, 0));
+      x[h] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, soff + 256u * h, 0, 0));
+    if (++lc == chunks) {
+      lc = 0;
+      ++lt;
+      l_tile();
+    } else {
+      lp += lstep;
+    }
   };
   auto store = [&](const u32x4 (&x)[SEG], int buf) {
 #pragma unroll
@@ -511,18 +519,18 @@ __global__ __launch_bounds__(PW_NT, 1) void pointwise_resident(PwArgs a, int til
 
   u32x4 ring[PD][SEG];
 #pragma unroll
-  for (int u = 0; u < PD; ++u) load(u, ring[u]);
+  for (int u = 0; u < PD; ++u) load(ring[u]);
   const int padded = (nst + PD - 1) / PD * PD;
+  int ct = 0, c = 0;  // tile ordinal and chunk of the stage being computed
   for (int g0 = 0; g0 < padded; g0 += PD) {
 #pragma unroll
     for (int u = 0; u < PD; ++u) {
-      const int g = g0 + u, buf = g & 1;
+      const int buf = u & 1;  // (g0 + u) & 1: PD is even
       // buffer `buf` was last read while computing stage g - 2, which every
       // wave finished before the barrier of stage g - 1
       store(ring[u], buf);
-      load(g + PD, ring[u]);
+      load(ring[u]);  // stage g + PD
       __syncthreads();
-      const int c = g % chunks;
       i16x8 av[NPF];
       u32x4 bv[PW_WCO];
 #pragma unroll
@@ -535,8 +543,8 @@ __global__ __launch_bounds__(PW_NT, 1) void pointwise_resident(PwArgs a, int til
         for (int cf = 0; cf < PW_WCO; ++cf) acc[cf][pf] = mma<F16>(av[pf], bv[cf], acc[cf][pf]);
       // the tile's last chunk: bias once, one rounding, NCTHW store; the
       // accumulators start again from zero (workgroup-uniform branch)
-      if (c == chunks - 1 && g < nst) {
-        const int t = static_cast<int>(blockIdx.x) + (g / chunks) * static_cast<int>(gridDim.x);
+      if (c == chunks - 1 && ct < ntile) {
+        const int t = static_cast<int>(blockIdx.x) + ct * static_cast<int>(gridDim.x);
         const int pt = t % a.px_tiles, nt = t / a.px_tiles;
         const int o = nt % a.To, n = nt / a.To;
         uint16_t* ybase = a.y + (static_cast<int64_t>(n) * a.Co * a.To + o) * a.hw;
@@ -559,6 +567,10 @@ __global__ __launch_bounds__(PW_NT, 1) void pointwise_resident(PwArgs a, int til
             acc[cf][pf] = f32x4{0.f, 0.f, 0.f, 0.f};
           }
         }
+      }
+      if (++c == chunks) {
+        c = 0;
+        ++ct;
       }
     }
   }
