@@ -156,31 +156,32 @@ __global__ __launch_bounds__(PW_NT, 1) void pointwise_conv(PwArgs a) {
 
   // the channel-plane strides of the cache and of the new chunk
   const int64_t cs_c = static_cast<int64_t>(a.Tc) * a.hw, cs_x = static_cast<int64_t>(a.T) * a.hw;
-  // Stage s's resource starts at channel 32 c of its source frame (pixel
-  // px0) and ends after the last real channel's row of that frame: channels
-  // past Ci load as 0; a stage past the last has an empty resource.
-  struct StageSrc {
-    __amdgpu_buffer_rsrc_t rs;
-    uint32_t cs;
-  };
-  auto stage_src = [&](int st_) {
-    const bool real = st_ < nst;
-    const int k = k_lo + (real ? st_ / a.chunks : 0), c0 = (real ? st_ % a.chunks : 0) * PW_K;
-    const int f = real ? t * a.st + k * a.dt - a.p_l : 0;
+  // Stages are loaded in order: tap lk, chunk lc.  The source pointer
+  // (channel 32 lc of the tap's frame, pixel px0) steps by one chunk per
+  // stage and only a new tap recomputes it; the stage's resource ends after
+  // the chunk's last real channel's row (32-bit: a 32-channel slab fits), so
+  // channels past Ci load as 0; a stage past the last has an empty resource.
+  // lwrow: the stage's packed weight row, k chunks + c fragments rows in
+  // (the stages' rows are consecutive).
+  int lk = k_lo, lc = 0;
+  const uint16_t* lp = a.x;
+  uint32_t lcs = 0;     // bytes between the source's channel planes
+  int64_t lstep = 0;    // elements between consecutive chunks
+  bool lfx = false;     // the tap's frame comes from the new chunk
+  const uint32_t lwstep = static_cast<uint32_t>(a.cofrags) * 1024u;
+  uint32_t lwrow = static_cast<uint32_t>(k_lo * a.chunks) * lwstep;
+  auto l_tap = [&]() __attribute__((always_inline)) {
+    if (lk > k_hi) return;
+    const int f = t * a.st + lk * a.dt - a.p_l;
     const bool in_cache = f < a.Tc;
     const int64_t cstride = in_cache ? cs_c : cs_x;
-    const uint16_t* base = in_cache ? a.cache : a.x;
-    const int64_t off = static_cast<int64_t>(in_cache ? f : f - a.Tc) * a.hw +
-                        static_cast<int64_t>(n) * a.Ci * cstride + px0 + c0 * cstride;
-    int64_t bytes = ((a.Ci - 1 - c0) * cstride + a.hw - px0) * 2;
-    if (!real || bytes < 0) bytes = 0;
-    if (bytes > 0x7fffffff) bytes = 0x7fffffff;
-    StageSrc r;
-    r.rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(real ? base + off : base), 0,
-                                             static_cast<int>(bytes), 0x00020000);
-    r.cs = static_cast<uint32_t>(cstride * 2);
-    return r;
+    lp = (in_cache ? a.cache + static_cast<int64_t>(f) * a.hw : a.x + static_cast<int64_t>(f - a.Tc) * a.hw) +
+         static_cast<int64_t>(n) * a.Ci * cstride + px0;
+    lcs = static_cast<uint32_t>(cstride * 2);
+    lstep = PW_K * cstride;
+    lfx = !in_cache;
   };
+  l_tap();
 
   // staging: thread -> activation channel row tid / 16, pixels
   // 128 h + 8 (tid % 16) .. + 7 for h < SEG (16 lanes read 256 contiguous bytes)
@@ -219,22 +220,26 @@ __global__ __launch_bounds__(PW_NT, 1) void pointwise_conv(PwArgs a) {
   const __amdgpu_buffer_rsrc_t shr = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<float*>(PRO && a.shift ? a.shift + static_cast<int64_t>(n) * a.Ci : a.shift), 0,
       PRO && a.shift ? a.Ci * 4 : 0, 0x00020000);
-  auto load_chunk = [&](int st_, Chunk& ck) {
-    const StageSrc sr = stage_src(st_);
+  auto load_chunk = [&](Chunk& ck) __attribute__((always_inline)) {
+    const bool real = lk <= k_hi;
+    const uint32_t bytes = real ? static_cast<uint32_t>(min(PW_K, a.Ci - lc * PW_K) - 1) * lcs +
+                                      static_cast<uint32_t>(a.hw - px0) * 2u
+                                : 0u;
+    const __amdgpu_buffer_rsrc_t rs =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(lp), 0, static_cast<int>(bytes), 0x00020000);
     if constexpr (PRO) {
       // the prologue applies to the new chunk's frames only
-      const int k = k_lo + (ntap > 0 ? st_ / a.chunks : 0);
-      const bool from_x = st_ < nst && t * a.st + k * a.dt - a.p_l >= a.Tc;
-      const uint32_t co = static_cast<uint32_t>((ntap > 0 ? st_ % a.chunks : 0) * PW_K + sch) * 4u;
+      const bool from_x = real && lfx;
+      const uint32_t co = static_cast<uint32_t>(lc * PW_K + sch) * 4u;
       ck.pro = from_x && a.scale != nullptr;
       ck.psc = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(ssr, from_x ? co : OOB, 0, 0));
       ck.psh = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(shr, from_x ? co : OOB, 0, 0));
     }
-    const uint32_t soff = static_cast<uint32_t>(sch) * sr.cs + static_cast<uint32_t>(spx) * 2u;
+    const uint32_t soff = static_cast<uint32_t>(sch) * lcs + static_cast<uint32_t>(spx) * 2u;
     if constexpr (ALIGNED) {
 #pragma unroll
       for (int h = 0; h < SEG; ++h)
-        ck.x[h] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(sr.rs, soff + 256u * h, 0, 0));
+        ck.x[h] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, soff + 256u * h, 0, 0));
     } else {
 #pragma unroll
       for (int h = 0; h < SEG; ++h) {
@@ -242,8 +247,8 @@ __global__ __launch_bounds__(PW_NT, 1) void pointwise_conv(PwArgs a) {
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const uint32_t o = soff + 256u * h + 4u * e;
-          const uint32_t lo = __builtin_amdgcn_raw_buffer_load_b16(sr.rs, o, 0, 0);
-          const uint32_t hi = __builtin_amdgcn_raw_buffer_load_b16(sr.rs, o + 2u, 0, 0);
+          const uint32_t lo = __builtin_amdgcn_raw_buffer_load_b16(rs, o, 0, 0);
+          const uint32_t hi = __builtin_amdgcn_raw_buffer_load_b16(rs, o + 2u, 0, 0);
           wd[e] = (lo & 0xffffu) | (hi << 16);
         }
         ck.x[h] = u32x4{wd[0], wd[1], wd[2], wd[3]};
@@ -251,21 +256,27 @@ __global__ __launch_bounds__(PW_NT, 1) void pointwise_conv(PwArgs a) {
     }
     if constexpr (PACKED) {
       // stage (tap k, chunk c): fragment row (k * chunks + c) of the packing
-      const int k = k_lo + (ntap > 0 ? st_ / a.chunks : 0), c = ntap > 0 ? st_ % a.chunks : 0;
-      const uint32_t row = static_cast<uint32_t>((k * a.chunks + c) * a.cofrags) * 1024u;
 #pragma unroll
       for (int i = 0; i < PW_WPT; ++i)
         ck.w[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
-                                                wrs, wp_ok[i] && st_ < nst ? row + wp_off[i] : OOB, 0, 0));
+                                                wrs, wp_ok[i] && real ? lwrow + wp_off[i] : OOB, 0, 0));
     } else {
-      const int c = st_;
+      // (Kt = 1: the stage is the chunk)
 #pragma unroll
       for (int i = 0; i < PW_WPT; ++i) {
-        const int co = ctile * PW_CO + wrow[i], ci = c * PW_K + wq[i];
-        const bool ok = (wrow[i] < PW_CO) & (co < a.Co) & (ci < a.Ci);
+        const int co = ctile * PW_CO + wrow[i], ci = lc * PW_K + wq[i];
+        const bool ok = real & (wrow[i] < PW_CO) & (co < a.Co) & (ci < a.Ci);
         ck.w[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
                                                 wrs, ok ? static_cast<uint32_t>(co * a.Ci + ci) * 2u : OOB, 0, 0));
       }
+    }
+    lwrow += lwstep;
+    if (++lc == a.chunks) {
+      lc = 0;
+      ++lk;
+      l_tap();
+    } else {
+      lp += lstep;
     }
   };
   auto store_chunk = [&](const Chunk& ck, int buf) {
@@ -319,7 +330,7 @@ __global__ __launch_bounds__(PW_NT, 1) void pointwise_conv(PwArgs a) {
 
   Chunk ring[PD];
 #pragma unroll
-  for (int u = 0; u < PD; ++u) load_chunk(u, ring[u]);
+  for (int u = 0; u < PD; ++u) load_chunk(ring[u]);
   const int padded = (nst + PD - 1) / PD * PD;
   for (int c0 = 0; c0 < padded; c0 += PD) {
 #pragma unroll
@@ -328,7 +339,7 @@ __global__ __launch_bounds__(PW_NT, 1) void pointwise_conv(PwArgs a) {
       // buffer `buf` was last read while computing chunk c - 2, which every
       // wave finished before the barrier of chunk c - 1
       store_chunk(ring[u], buf);
-      load_chunk(c + PD, ring[u]);
+      load_chunk(ring[u]);  // chunk c + PD
       __syncthreads();
       i16x8 av[PW_NPF];
       u32x4 bv[PW_WCO];
