@@ -239,21 +239,32 @@ __global__ __launch_bounds__(64 * WAVES_CO * WAVES_PX) void fast_conv3d(FastArgs
         tile[(rr * TW + cc) * PIXS + ch] = v;
       }
       __syncthreads();
-#pragma unroll 1
-      for (int ij = 0; ij < KS * KS; ++ij) {
-        const int ki = ij / KS, kj = ij % KS;
+      // A spatial tap's weight fragments (its BKC / KSTEP K-steps) are loaded
+      // one tap ahead of its products, into a second register set, so that
+      // no product waits for a weight load issued just before it.
+      constexpr int NKS = BKC / KSTEP;
+      typename M::frag wa[NKS][CO_FRAGS], wb[NKS][CO_FRAGS];
+      auto load_wt = [&](int ij, typename M::frag (&w)[NKS][CO_FRAGS]) {
         const int64_t tap = k * KS * KS + ij;
 #pragma unroll
-        for (int ks = 0; ks < BKC / KSTEP; ++ks) {
+        for (int ks = 0; ks < NKS; ++ks) {
           const int64_t chunk = c0 / KSTEP + ks;
-          if (chunk >= a.chunks) break;
-          typename M::frag af[CO_FRAGS], bf[PX_FRAGS];
 #pragma unroll
           for (int cf = 0; cf < CO_FRAGS; ++cf) {
             const int cofrag = cofrag0 + cf;
-            af[cf] = cofrag < a.cofrags ? wp[((tap * a.chunks + chunk) * a.cofrags + cofrag) * 64 + lane]
-                                        : M::zero();
+            w[ks][cf] = chunk < a.chunks && cofrag < a.cofrags
+                            ? wp[((tap * a.chunks + chunk) * a.cofrags + cofrag) * 64 + lane]
+                            : M::zero();
           }
+        }
+      };
+      auto products = [&](int ij, const typename M::frag (&w)[NKS][CO_FRAGS]) {
+        const int ki = ij / KS, kj = ij % KS;
+#pragma unroll
+        for (int ks = 0; ks < NKS; ++ks) {
+          const int64_t chunk = c0 / KSTEP + ks;
+          if (chunk >= a.chunks) break;
+          typename M::frag bf[PX_FRAGS];
 #pragma unroll
           for (int pf = 0; pf < PX_FRAGS; ++pf) {
             const int q = wpx * PX_FRAGS + pf;
@@ -264,7 +275,17 @@ __global__ __launch_bounds__(64 * WAVES_CO * WAVES_PX) void fast_conv3d(FastArgs
 #pragma unroll
           for (int cf = 0; cf < CO_FRAGS; ++cf)
 #pragma unroll
-            for (int pf = 0; pf < PX_FRAGS; ++pf) acc[cf][pf] = M::mma(af[cf], bf[pf], acc[cf][pf]);
+            for (int pf = 0; pf < PX_FRAGS; ++pf) acc[cf][pf] = M::mma(w[ks][cf], bf[pf], acc[cf][pf]);
+        }
+      };
+      load_wt(0, wa);
+#pragma unroll 1
+      for (int ij = 0; ij < KS * KS; ij += 2) {
+        if (ij + 1 < KS * KS) load_wt(ij + 1, wb);
+        products(ij, wa);
+        if (ij + 1 < KS * KS) {
+          if (ij + 2 < KS * KS) load_wt(ij + 2, wa);
+          products(ij + 1, wb);
         }
       }
     }
