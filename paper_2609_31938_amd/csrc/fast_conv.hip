@@ -79,22 +79,35 @@ __global__ __launch_bounds__(256) void repack_kernel(const T* __restrict__ w, T*
 // w (32 * taps elements per output channel), read coalesced into LDS; each
 // thread then writes whole 16-byte lane slots (8 consecutive input channels
 // of one output channel at one tap) of the block's fragments, one 1 KiB
-// fragment per 64 threads.  Channels past Ci / Co are zeros.
+// fragment per 64 threads.  Channels past Ci / Co are zeros.  vec: w is
+// 16-byte aligned and Ci * taps a multiple of 8, so a full chunk's runs are
+// read as 16-byte pieces (the tail chunk, and other calls, element by
+// element).
 constexpr int kRepackMaxTaps = 48;
 __global__ __launch_bounds__(256) void repack_block16(const uint16_t* __restrict__ w,
                                                       u32x4* __restrict__ wp, int64_t Ci,
                                                       int64_t Co, int taps, int64_t chunks,
-                                                      int64_t cofrags) {
-  __shared__ uint16_t tile[16 * 32 * kRepackMaxTaps];
+                                                      int64_t cofrags, int vec) {
+  __shared__ __align__(16) uint16_t tile[16 * 32 * kRepackMaxTaps];
   const int64_t cf = blockIdx.x % cofrags, ch = blockIdx.x / cofrags;
   const int row = 32 * taps;  // elements of one output channel's run
   const int64_t ci0 = ch * 32;
   const int64_t ci_n = Ci - ci0 < 32 ? Ci - ci0 : 32;  // real input channels of the chunk
-  for (int q = threadIdx.x; q < 16 * row; q += 256) {
-    const int r = q / row, u = q - r * row;
-    const int64_t co = cf * 16 + r;
-    const bool ok = co < Co && u < ci_n * taps;
-    tile[q] = ok ? w[(co * Ci + ci0) * taps + u] : static_cast<uint16_t>(0);
+  if (vec && ci_n == 32) {
+    const int nv = row / 8;  // 16-byte pieces of a run
+    for (int q = threadIdx.x; q < 16 * nv; q += 256) {
+      const int r = q / nv, u = q - r * nv;
+      const int64_t co = cf * 16 + r;
+      *reinterpret_cast<u32x4*>(tile + r * row + 8 * u) =
+          co < Co ? *reinterpret_cast<const u32x4*>(w + (co * Ci + ci0) * taps + 8 * u) : u32x4{0u, 0u, 0u, 0u};
+    }
+  } else {
+    for (int q = threadIdx.x; q < 16 * row; q += 256) {
+      const int r = q / row, u = q - r * row;
+      const int64_t co = cf * 16 + r;
+      const bool ok = co < Co && u < ci_n * taps;
+      tile[q] = ok ? w[(co * Ci + ci0) * taps + u] : static_cast<uint16_t>(0);
+    }
   }
   __syncthreads();
   // thread -> (tap t, lane L): lane L holds output channel L % 16, input
@@ -350,7 +363,8 @@ hipError_t launch_repack(const Geo& g, const void* w, void* wpack, hipStream_t s
            p.chunks * p.cofrags <= 0x7fffffff && (reinterpret_cast<uintptr_t>(wpack) & 15u) == 0)
     hipLaunchKernelGGL(repack_block16, dim3(static_cast<unsigned>(p.chunks * p.cofrags)), dim3(256),
                        0, s, static_cast<const uint16_t*>(w), static_cast<u32x4*>(wpack), g.d.Ci,
-                       g.d.Co, static_cast<int>(p.taps), p.chunks, p.cofrags);
+                       g.d.Co, static_cast<int>(p.taps), p.chunks, p.cofrags,
+                       ((reinterpret_cast<uintptr_t>(w) & 15u) == 0 && (g.d.Ci * p.taps) % 8 == 0) ? 1 : 0);
   else
     hipLaunchKernelGGL(repack_kernel<uint16_t>, dim3(blocks), dim3(256), 0, s,
                        static_cast<const uint16_t*>(w), static_cast<uint16_t*>(wpack), total,
