@@ -421,13 +421,19 @@ __global__ __launch_bounds__(PW_NT, 1) void pointwise_conv(PwArgs a) {
 // register sets that runs on across tile boundaries: the loads of the next
 // tile's first chunks are in flight while a tile finishes and its outputs
 // are stored.  The activation stage, its transposing LDS read and the
-// epilogue are those of pointwise_conv.
+// epilogue are those of pointwise_conv, and so is the fused form (FU, bf16):
+// the residual added before the one rounding (1), and also (2) the prologue
+// applied to a new-chunk frame's staged registers before they go to LDS,
+// with the tile's batch element's per-channel scale and shift (0 past Ci, so
+// channels past Ci stay 0).
 constexpr int kResidentChunks = 11;
 constexpr int PW_RES_W = 10 * 1024 * kResidentChunks;  // resident weight bytes (max)
 
-template <bool F16, int PD>
+template <bool F16, int PD, int FU = 0>
 __global__ __launch_bounds__(PW_NT, 1) void pointwise_resident(PwArgs a, int tiles_total) {
   static_assert(PD % 2 == 0, "the two LDS buffers alternate within one pass over the ring");
+  static_assert(FU == 0 || !F16, "the fused form is bf16");
+  constexpr bool PRO = FU == 2, RES = FU >= 1;
   constexpr int NPF = 4, PX = pw_px(NPF), PITCH = pw_pitch(NPF), SEG = PX / 128;
   constexpr int ABUF = pw_row(NPF, PW_K);  // one activation stage
   __shared__ __align__(16) unsigned char lds[PW_RES_W + 2 * ABUF];
@@ -470,6 +476,8 @@ __global__ __launch_bounds__(PW_NT, 1) void pointwise_resident(PwArgs a, int til
   uint32_t lcs = 0, lpx = 0;  // bytes between channel planes; pixel bytes left in the plane
   int64_t lstep = 0;          // elements between consecutive chunks
   bool lact = false;
+  bool lpro = false;  // PRO: the tile's frame comes from the new chunk
+  int lsc = 0;        // PRO: the tile's batch element's first scale / shift index
   auto l_tile = [&]() __attribute__((always_inline)) {
     const int t = static_cast<int>(blockIdx.x) + lt * static_cast<int>(gridDim.x);
     const int pt = t % a.px_tiles, nt = t / a.px_tiles;
@@ -477,6 +485,8 @@ __global__ __launch_bounds__(PW_NT, 1) void pointwise_resident(PwArgs a, int til
     const int f = o * a.st - a.p_l;  // Kt = 1: the one tap's source frame
     lact = lt < ntile && f >= 0 && f < a.Z;
     const bool in_cache = lact && f < a.Tc;
+    lpro = PRO && lact && !in_cache && a.scale != nullptr;
+    lsc = n * a.Ci;
     const int64_t cstride = in_cache ? cs_c : cs_x;
     const int64_t px0 = static_cast<int64_t>(pt) * PX;
     lp = lact ? (in_cache ? a.cache + static_cast<int64_t>(f) * a.hw : a.x + static_cast<int64_t>(f - a.Tc) * a.hw) +
@@ -489,7 +499,27 @@ __global__ __launch_bounds__(PW_NT, 1) void pointwise_resident(PwArgs a, int til
   l_tile();
   const int sch = tid >> 4, spx = (tid & 15) * 8;
   const int slds = pw_row(NPF, sch) + spx * 2;
-  auto load = [&](u32x4 (&x)[SEG]) __attribute__((always_inline)) {
+  // PRO: scale / shift [N][Ci] as fp32 resources; this thread's channel of
+  // the stage (32 lc + sch) reads 0 past Ci
+  const uint32_t sbytes = PRO && a.scale ? static_cast<uint32_t>(a.N * a.Ci) * 4u : 0u;
+  const __amdgpu_buffer_rsrc_t ssr = __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(a.scale), 0,
+                                                                       static_cast<int>(sbytes), 0x00020000);
+  const __amdgpu_buffer_rsrc_t shr = __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(a.shift), 0,
+                                                                       static_cast<int>(sbytes), 0x00020000);
+  struct Slot {
+    u32x4 x[SEG];
+    float psc, psh;
+    bool pro;
+  };
+  auto load = [&](Slot& sl) __attribute__((always_inline)) {
+    u32x4(&x)[SEG] = sl.x;
+    if constexpr (PRO) {
+      const int c = lc * PW_K + sch;
+      const uint32_t off = lpro && c < a.Ci ? static_cast<uint32_t>(lsc + c) * 4u : OOB;
+      sl.pro = lpro;
+      sl.psc = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(ssr, off, 0, 0));
+      sl.psh = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(shr, off, 0, 0));
+    }
     const uint32_t bytes = lact ? static_cast<uint32_t>(min(PW_K, a.Ci - lc * PW_K) - 1) * lcs + lpx : 0u;
     const __amdgpu_buffer_rsrc_t rs =
         __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(lp), 0, static_cast<int>(bytes), 0x00020000);
@@ -505,10 +535,13 @@ __global__ __launch_bounds__(PW_NT, 1) void pointwise_resident(PwArgs a, int til
       lp += lstep;
     }
   };
-  auto store = [&](const u32x4 (&x)[SEG], int buf) {
+  auto store = [&](const Slot& sl, int buf) {
 #pragma unroll
-    for (int h = 0; h < SEG; ++h)
-      *reinterpret_cast<u32x4*>(lds + PW_RES_W + buf * ABUF + slds + 256 * h) = x[h];
+    for (int h = 0; h < SEG; ++h) {
+      u32x4 v = sl.x[h];
+      if (PRO && sl.pro) v = fuse_seg8(v, sl.psc, sl.psh, true);  // workgroup-uniform
+      *reinterpret_cast<u32x4*>(lds + PW_RES_W + buf * ABUF + slds + 256 * h) = v;
+    }
   };
   const int j = lane & 15, gq = lane >> 4;
   const int ra = pw_row(NPF, 8 * gq + (j >> 2)) + (wpx * 16 * NPF + 4 * (j & 3)) * 2;
@@ -528,7 +561,7 @@ __global__ __launch_bounds__(PW_NT, 1) void pointwise_resident(PwArgs a, int til
 #pragma unroll
     for (int pf = 0; pf < NPF; ++pf) acc[cf][pf] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  u32x4 ring[PD][SEG];
+  Slot ring[PD];
 #pragma unroll
   for (int u = 0; u < PD; ++u) load(ring[u]);
   const int padded = (nst + PD - 1) / PD * PD;
@@ -542,6 +575,32 @@ __global__ __launch_bounds__(PW_NT, 1) void pointwise_resident(PwArgs a, int til
       store(ring[u], buf);
       load(ring[u]);  // stage g + PD
       __syncthreads();
+      // the tile's last chunk (workgroup-uniform): its outputs are stored
+      // after the products; RES: the tile's residual values are loaded
+      // first, so that they arrive during the products
+      const bool last = c == chunks - 1 && ct < ntile;
+      int64_t toff = 0;  // element offset of output channel 0 of the tile's (n, o) plane, pixel 0
+      int64_t tp0 = 0;   // the tile's first pixel
+      if (last) {
+        const int t = static_cast<int>(blockIdx.x) + ct * static_cast<int>(gridDim.x);
+        const int pt = t % a.px_tiles, nt = t / a.px_tiles;
+        const int o = nt % a.To, n = nt / a.To;
+        toff = (static_cast<int64_t>(n) * a.Co * a.To + o) * a.hw;
+        tp0 = static_cast<int64_t>(pt) * PX + wpx * 16 * NPF + 4 * gq;
+      }
+      uint2 rv[RES ? PW_WCO : 1][RES ? NPF : 1];
+      if (RES && last && a.residual) {
+#pragma unroll
+        for (int cf = 0; cf < PW_WCO; ++cf) {
+          const int co = wco * 16 * PW_WCO + 16 * cf + j;
+          const int64_t roff = toff + static_cast<int64_t>(co < a.Co ? co : 0) * a.To * a.hw;
+#pragma unroll
+          for (int pf = 0; pf < NPF; ++pf) {
+            const int64_t p = tp0 + pf * 16;  // hw % 8 == 0: four pixels all in or all out
+            rv[cf][pf] = *reinterpret_cast<const uint2*>(a.residual + roff + (p < a.hw ? p : 0));
+          }
+        }
+      }
       i16x8 av[NPF];
       u32x4 bv[PW_WCO];
 #pragma unroll
@@ -552,26 +611,30 @@ __global__ __launch_bounds__(PW_NT, 1) void pointwise_resident(PwArgs a, int til
       for (int pf = 0; pf < NPF; ++pf)
 #pragma unroll
         for (int cf = 0; cf < PW_WCO; ++cf) acc[cf][pf] = mma<F16>(av[pf], bv[cf], acc[cf][pf]);
-      // the tile's last chunk: bias once, one rounding, NCTHW store; the
-      // accumulators start again from zero (workgroup-uniform branch)
-      if (c == chunks - 1 && ct < ntile) {
-        const int t = static_cast<int>(blockIdx.x) + ct * static_cast<int>(gridDim.x);
-        const int pt = t % a.px_tiles, nt = t / a.px_tiles;
-        const int o = nt % a.To, n = nt / a.To;
-        uint16_t* ybase = a.y + (static_cast<int64_t>(n) * a.Co * a.To + o) * a.hw;
+      // bias once, one rounding (the residual added before it), NCTHW store;
+      // the accumulators start again from zero
+      if (last) {
 #pragma unroll
         for (int cf = 0; cf < PW_WCO; ++cf) {
           const int co = wco * 16 * PW_WCO + 16 * cf + j;
           const float bb = (a.has_bias && co < a.Co) ? from_b16(a.bias[co], F16) : 0.f;
-          uint16_t* yrow = ybase + static_cast<int64_t>(co) * a.To * a.hw;
+          uint16_t* yrow = a.y + toff + static_cast<int64_t>(co) * a.To * a.hw;
 #pragma unroll
           for (int pf = 0; pf < NPF; ++pf) {
-            const int64_t p = static_cast<int64_t>(pt) * PX + wpx * 16 * NPF + pf * 16 + 4 * gq;
+            const int64_t p = tp0 + pf * 16;
             if (co < a.Co && p < a.hw) {  // hw % 8 == 0: four pixels all in or all out
+              float rr[4] = {0.f, 0.f, 0.f, 0.f};
+              if (RES && a.residual) {
+                const uint2 r2 = rv[RES ? cf : 0][RES ? pf : 0];
+                rr[0] = fuse_widen(r2.x & 0xffffu);
+                rr[1] = fuse_widen(r2.x >> 16);
+                rr[2] = fuse_widen(r2.y & 0xffffu);
+                rr[3] = fuse_widen(r2.y >> 16);
+              }
               uint16_t v[4];
 #pragma unroll
               for (int r = 0; r < 4; ++r)
-                v[r] = F16 ? to_f16(acc[cf][pf][r] + bb) : to_bf16(acc[cf][pf][r] + bb);
+                v[r] = F16 ? to_f16(acc[cf][pf][r] + bb + rr[r]) : to_bf16(acc[cf][pf][r] + bb + rr[r]);
               *reinterpret_cast<uint2*>(yrow + p) =
                   make_uint2(v[0] | (static_cast<uint32_t>(v[1]) << 16), v[2] | (static_cast<uint32_t>(v[3]) << 16));
             }
@@ -717,8 +780,10 @@ hipError_t launch_pointwise(const Geo& g, const void* x, const void* cache, cons
                             const void* bias, void* y, hipStream_t s, const Fuse& fu,
                             LaunchInfo* info) {
   PwArgs a = common_args(g, x, cache, bias, y);
-  // unfused calls whose weights fit in LDS: the persistent resident-weight kernel
-  if (!fu.any() && g.d.Co <= PW_CO && a.chunks <= kResidentChunks && g.d.N * g.To > 0) {
+  const bool f16 = g.d.dtype == C3C_DTYPE_F16;
+  // calls whose weights fit in LDS (the fused form: bf16): the persistent
+  // resident-weight kernel
+  if ((!fu.any() || !f16) && g.d.Co <= PW_CO && a.chunks <= kResidentChunks && g.d.N * g.To > 0) {
     a.w = static_cast<const uint16_t*>(w);
     a.w_bytes = static_cast<uint32_t>(g.d.Co * g.d.Ci * 2);
     a.cofrags = 0;
@@ -736,13 +801,18 @@ hipError_t launch_pointwise(const Geo& g, const void* x, const void* cache, cons
       return hipSuccess;
     }
     if (tiles > 0x7fffffff) return hipErrorInvalidConfiguration;
-    const bool f16 = g.d.dtype == C3C_DTYPE_F16;
+    a.scale = fu.scale;
+    a.shift = fu.shift;
+    a.residual = fu.residual;  // launch_fallback checked its 8-byte alignment
+    const dim3 grid(static_cast<unsigned>(blocks)), block(PW_NT);
     if (f16)
-      hipLaunchKernelGGL((pointwise_resident<true, 4>), dim3(static_cast<unsigned>(blocks)), dim3(PW_NT), 0,
-                         s, a, static_cast<int>(tiles));
+      hipLaunchKernelGGL((pointwise_resident<true, 4>), grid, block, 0, s, a, static_cast<int>(tiles));
+    else if (fu.pro())
+      hipLaunchKernelGGL((pointwise_resident<false, 4, 2>), grid, block, 0, s, a, static_cast<int>(tiles));
+    else if (fu.residual)
+      hipLaunchKernelGGL((pointwise_resident<false, 4, 1>), grid, block, 0, s, a, static_cast<int>(tiles));
     else
-      hipLaunchKernelGGL((pointwise_resident<false, 4>), dim3(static_cast<unsigned>(blocks)), dim3(PW_NT), 0,
-                         s, a, static_cast<int>(tiles));
+      hipLaunchKernelGGL((pointwise_resident<false, 4>), grid, block, 0, s, a, static_cast<int>(tiles));
     return hipGetLastError();
   }
   a.w = static_cast<const uint16_t*>(w);

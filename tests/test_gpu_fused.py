@@ -146,6 +146,11 @@ def test_fused_fast_1x1(over):
 FALLBACK = [
     (dict(N=1, Ci=24, Co=40, T=2, Tc=2, H=11, W=37), c3c.MODE_FORCE_FALLBACK),
     (dict(N=1, Ci=64, Co=48, T=2, Tc=0, H=8, W=16, Kt=1, Kh=1, Kw=1), 0),  # 1x1x1: pointwise
+    # 1x1x1 on the resident-weight kernel: a cached frame (no prologue), a
+    # right-padded frame (bias and residual alone), a channel tail, N = 2;
+    # then 320 tiles, some workgroups taking two of different batch elements
+    (dict(N=2, Ci=40, Co=72, T=3, Tc=1, H=16, W=24, Kt=1, Kh=1, Kw=1, p_base=1, p_r=1), 0),
+    (dict(N=2, Ci=64, Co=160, T=5, Tc=0, H=64, W=128, Kt=1, Kh=1, Kw=1), 0),
     (dict(N=1, Ci=12, Co=20, T=3, Tc=2, H=10, W=13, Kh=5, Kw=3), 0),       # 5x3: generic
     (dict(N=1, Ci=16, Co=24, T=4, Tc=2, H=12, W=16, s_t=2), 0),            # 3x3 at stride 2
 ]
@@ -155,6 +160,14 @@ FALLBACK = [
 def test_fused_fallback(over, mode):
     _run(spec(**over), mode=mode, expect_fast=False)
     _run(spec(**over), mode=mode, inplace=True, expect_fast=False)
+
+
+@pytest.mark.parametrize("pro,res", [(True, False), (False, True)])
+def test_fused_parts_on_the_resident_1x1x1_kernel(pro, res):
+    """The prologue alone and the residual alone (the kernel's two fused
+    instances) on a 1x1x1 call whose weights fit in LDS."""
+    sp = spec(N=2, Ci=40, Co=72, T=3, Tc=1, H=16, W=24, Kt=1, Kh=1, Kw=1, p_base=1, p_r=1)
+    _run(sp, pro=pro, res=res, expect_fast=False)
 
 
 # ---------------------------------------------------------------- streaming
