@@ -76,7 +76,14 @@ enum {
   C3C_MODE_FORCE_FALLBACK = 2u,
   /* the fast route fails before launching anything, as a test of the failure
    * path: counted in fast_error, then fallback (or C3C_E_INJECTED if strict) */
-  C3C_MODE_INJECT_FAST_FAILURE = 4u
+  C3C_MODE_INJECT_FAST_FAILURE = 4u,
+  /* a bf16 3x3 call that runs unsplit keeps the tile its output-channel count
+   * selects even when those tiles fill less than one round of the compute
+   * units (by default such a call may take smaller tiles that fill more of
+   * them); outputs are bit-identical either way, the accumulation order of
+   * every output element being the same: this pins the kernel instance,
+   * e.g. to test each tile on small inputs */
+  C3C_MODE_CHANNEL_TILES = 8u
 };
 
 /* ---------------------------------------------------------------- routes */

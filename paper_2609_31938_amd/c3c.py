@@ -34,7 +34,7 @@ import torch  # noqa: E402,F401
 
 OK, E_INVAL, E_UNSUPPORTED, E_DEVICE, E_INJECTED = 0, 1, 2, 3, 4
 DTYPES = {"bf16": 1, "f32": 2, "f16": 3}
-MODE_STRICT, MODE_FORCE_FALLBACK, MODE_INJECT_FAST_FAILURE = 1, 2, 4
+MODE_STRICT, MODE_FORCE_FALLBACK, MODE_INJECT_FAST_FAILURE, MODE_CHANNEL_TILES = 1, 2, 4, 8
 ROUTES = ["fast", "fallback"]
 REASONS = ["none", "forced", "dtype", "groups", "stride_t", "pad_right", "no_output",
            "no_tap", "kt1", "spatial", "fast_error"]

@@ -30,7 +30,8 @@ namespace c3c {
 namespace {
 
 constexpr uint32_t kModeMask =
-    C3C_MODE_STRICT | C3C_MODE_FORCE_FALLBACK | C3C_MODE_INJECT_FAST_FAILURE;
+    C3C_MODE_STRICT | C3C_MODE_FORCE_FALLBACK | C3C_MODE_INJECT_FAST_FAILURE |
+    C3C_MODE_CHANNEL_TILES;
 constexpr int64_t kMaxElems = int64_t(1) << 40;  // per tensor, far above any HBM size
 
 int64_t floordiv(int64_t a, int64_t b) {
@@ -260,6 +261,7 @@ int c3c_route_query(const c3c_ctx* ctx, const c3c_conv_desc* d, int* route, int*
 int c3c_plan_query(const c3c_ctx* ctx, const c3c_conv_desc* d, size_t ws_bytes, c3c_plan* out) {
   Geo g;
   if (*make_geo(d, &g) || !out) return C3C_E_INVAL;
+  g.channel_tiles = ctx && (ctx->mode & C3C_MODE_CHANNEL_TILES);
   std::memset(out, 0, sizeof *out);
   const int r = decide(g, ctx ? ctx->mode : 0u);
   out->reason = r;
@@ -400,6 +402,7 @@ int run_call(c3c_ctx* ctx, const c3c_conv_desc* d, const void* x, const void* ca
   Geo g;
   const char* why = make_geo(d, &g);
   if (*why) return fail(ctx, C3C_E_INVAL, why);
+  g.channel_tiles = (ctx->mode & C3C_MODE_CHANNEL_TILES) != 0;
 
   // byte extents of every tensor
   const int64_t es = g.elem;

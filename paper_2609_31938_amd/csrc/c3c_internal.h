@@ -17,6 +17,7 @@ struct Geo {
   int64_t To, Ho, Wo;
   int64_t L;    // new cache length = min(pad_t_base, |Z|)
   int elem;     // bytes per element
+  bool channel_tiles = false;  // C3C_MODE_CHANNEL_TILES: no re-tiling of unsplit calls
 };
 
 // Fast-route packed-weight layout, in matrix-core fragment order.  One

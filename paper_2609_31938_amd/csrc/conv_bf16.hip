@@ -666,7 +666,7 @@ __global__ __launch_bounds__(256) void splitk_reduce(const float* __restrict__ p
 }
 
 // Tile configurations of the bf16 kernel (template arguments of run()).
-enum Cfg { CFG_C192, CFG_C96, CFG_C16, CFG_C160_4X80, CFG_C160_10X32, CFG_C128_4X80 };
+enum Cfg { CFG_C192, CFG_C96, CFG_C16, CFG_C160_4X80, CFG_C160_10X32, CFG_C128_4X80, CFG_C64_4X64 };
 
 // Launch plan of one bf16 fast call: tile configuration, workgroups of one
 // split, split-K factor, and the fp32 partial-sum bytes the split needs.
@@ -852,27 +852,54 @@ Plan plan_bf16(const Geo& g) {
   return p;
 }
 
-// The plan of a call that runs unsplit (no workspace, or too small a one):
-// a 192-channel tiling that fills less than one round of the compute units
-// takes the 128-channel 4 x 80 tiling instead when that costs less in whole
-// rounds of workgroups times each workgroup's work (output channels x
-// pixels): the same channels on smaller tiles, more of them in the round.
-// (384 -> 384 at 60 x 104 with one output frame: 60 workgroups of
-// 192 x 256 against 90 of 128 x 320, 0.161 -> 0.135 ms.)  A call that
-// splits keeps the 192-channel plan, which its split-K model is set for.
+// The plan of a call that runs unsplit (no workspace, or too small a one)
+// whose tiles fill less than one round of the compute units: of its own
+// tiling, the 128-channel 4 x 80 tiling (from the 192-channel one, when it
+// pads no more output channels) and the 64-channel 4 x 64 tiling, the one of
+// least modelled time
+//   rounds of workgroups x the tile's output channels x pixels x c,
+// c = 1 for the 192-, 160- and 128-channel tiles and 1.7 for the 64-channel
+// tile: with two output-channel fragments per wave, each activation operand
+// read from LDS feeds two products instead of four to six, and its main loop
+// runs at about 4.0 TFLOP/s per compute unit against 6.9.  Measured, one
+// output frame from two cached ones: 384 -> 384 at 60 x 104, 0.133 ms on 90
+// workgroups of 128 x 4x80, 0.092 on 180 of 64 x 4x64; 192 -> 192 at 60 x
+// 104, 0.087 on 30 of 192 x 4x64, 0.048 on 90 of 64 x 4x64.  With two output
+// frames the first stays on 128 x 4x80 (180 workgroups, 0.139 ms, against two
+// rounds of 360, 0.162).  Every output element's products are accumulated in
+// the same order on every tile, so the outputs are bit-identical.  A call
+// that splits keeps the tiling its split-K model is set for, and
+// C3C_MODE_CHANNEL_TILES keeps the output-channel tiling.
 Plan unsplit_plan(const Geo& g, Plan p) {
   const int64_t cus = compute_units();
   p.splits = 1;
   p.part_bytes = 0;
-  if (p.cfg != CFG_C192 || p.blocks >= cus) return p;
-  Plan r;
-  set_tiles(g, 128, 4, 80, &r);
-  if (r.tiles_co * 128 <= p.tiles_co * 192 &&
-      ((r.blocks + cus - 1) / cus) * r.tile_flop_px < ((p.blocks + cus - 1) / cus) * p.tile_flop_px) {
-    r.cfg = CFG_C128_4X80;
-    r.splits = 1;
-    r.part_bytes = 0;
-    return r;
+  const bool wide = p.cfg == CFG_C192 || p.cfg == CFG_C160_4X80 || p.cfg == CFG_C160_10X32 ||
+                    p.cfg == CFG_C128_4X80;
+  if (g.channel_tiles || !wide || p.blocks >= cus) return p;
+  // cost in tenths of c
+  auto cost = [&](const Plan& q, int64_t c10) {
+    return (q.blocks + cus - 1) / cus * q.tile_flop_px * c10;
+  };
+  int64_t best = cost(p, 10);
+  if (p.cfg == CFG_C192) {
+    Plan r;
+    set_tiles(g, 128, 4, 80, &r);
+    if (r.tiles_co * 128 <= p.tiles_co * 192 && cost(r, 10) < best) {
+      r.cfg = CFG_C128_4X80;
+      r.splits = 1;
+      r.part_bytes = 0;
+      p = r;
+      best = cost(r, 10);
+    }
+  }
+  Plan q;
+  set_tiles(g, 64, 4, 64, &q);
+  if (cost(q, 17) < best) {
+    q.cfg = CFG_C64_4X64;
+    q.splits = 1;
+    q.part_bytes = 0;
+    p = q;
   }
   return p;
 }
@@ -943,6 +970,8 @@ hipError_t launch_fast_bf16(const Geo& g, const void* x, const void* cache, cons
     // layers for this tile (the 192- and 96-channel tiles keep three)
     case CFG_C160_4X80: return run<5, 2, 5, 2, 2, 2>(g, a, pl, aligned, fused, s, info);
     case CFG_C128_4X80: return run<4, 2, 5, 2, 2, 2>(g, a, pl, aligned, fused, s, info);
+    // two fragments per wave: 64 x 4x64 tiles for unsplit calls that fill few compute units
+    case CFG_C64_4X64: return run<2, 2, 4, 2, 2, 3>(g, a, pl, aligned, fused, s, info);
     default: return run<5, 5, 2, 2, 2, 3>(g, a, pl, aligned, fused, s, info);
   }
 }

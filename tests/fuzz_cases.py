@@ -1,12 +1,17 @@
 """Seeded random call shapes for the fuzz parity test, grouped by the kernel
 each group is drawn to reach.  No convolution arithmetic here: a case is a
-(dtype, spec overrides, kernel the plan must name, mode, split-K workspace?)
+(dtype, spec overrides, kernel the plan must name, context mode, split-K workspace?)
 record, and the CPU test suite checks that every case's plan names the kernel
 its group targets, so the GPU fuzz run covers every kernel by construction.
 """
 import numpy as np
 
 from paper_2609_31938_amd.inputs import spec
+
+# C3C_MODE_CHANNEL_TILES: an unsplit call that fills few compute units keeps
+# its output-channel tiling instead of the 64-channel 4x64 tiles (half of the
+# wider cases run with it, so both tilings are drawn)
+CHANNEL_TILES = 8
 
 
 def _i(rng, lo, hi):
@@ -38,15 +43,15 @@ def cases():
         o = _conv3x3(rng, 6, 16)
         o["W"] = _i(rng, 1, 60) * 2 + 1  # odd widths: never the head kernel
         out.append(("bf16", o, "conv3d_bf16", 0, False))
-    for _ in range(30):
+    for k in range(30):
         o = _conv3x3(rng, 97, 400, hw=(1, 30, 1, 120))
         if o["Co"] % 192 == 0:
             o["Co"] += 1
-        out.append(("bf16", o, "conv3d_bf16", 0, False))
-    for _ in range(10):
+        out.append(("bf16", o, "conv3d_bf16", CHANNEL_TILES if k % 2 else 0, False))
+    for k in range(10):
         o = _conv3x3(rng, 192, 192, hw=(1, 24, 1, 100))
         o["Co"] = int(rng.choice([192, 384]))
-        out.append(("bf16", o, "conv3d_bf16", 0, False))
+        out.append(("bf16", o, "conv3d_bf16", CHANNEL_TILES if k % 2 else 0, False))
     # fp32 3x3 and 1x1
     for _ in range(15):
         out.append(("f32", _conv3x3(rng, 1, 80, hw=(1, 24, 1, 70)), "fast_f32", 0, False))

@@ -111,13 +111,24 @@ def test_fused_fast_3x3(over):
     _run(spec(**over), expect_fast=True)
 
 
+# The 160- and 192-channel cases above run unsplit on 64-channel 4x64 tiles
+# (they fill few compute units); C3C_MODE_CHANNEL_TILES keeps their own tiles.
+@pytest.mark.parametrize("over,tile", [(FAST3[1], (160, 4, 80)), (FAST3[2], (192, 4, 64))])
+def test_fused_fast_3x3_on_the_channel_tiles(over, tile):
+    sp = spec(**over)
+    plans = [c3c.plan_query(c3c.Context(m), sp, "bf16") for m in (0, c3c.MODE_CHANNEL_TILES)]
+    assert [(p["tile_co"], p["tile_h"], p["tile_w"]) for p in plans] == [(64, 4, 64), tile], plans
+    _run(sp, mode=c3c.MODE_CHANNEL_TILES, expect_fast=True)
+
+
+@pytest.mark.parametrize("mode", [0, c3c.MODE_CHANNEL_TILES])
 @pytest.mark.parametrize("pro,res,inplace", [(True, False, False), (False, True, False),
                                              (True, True, True), (False, False, False)])
-def test_fused_parts_and_in_place(pro, res, inplace):
-    _run(spec(N=1, Ci=64, Co=160, T=2, Tc=2, H=24, W=80), pro=pro, res=res, inplace=inplace,
-         expect_fast=True)
-    _run(spec(N=1, Ci=24, Co=40, T=2, Tc=2, H=11, W=37), pro=pro, res=res, inplace=inplace,
-         expect_fast=True)
+def test_fused_parts_and_in_place(pro, res, inplace, mode):
+    _run(spec(N=1, Ci=64, Co=160, T=2, Tc=2, H=24, W=80), mode=mode, pro=pro, res=res,
+         inplace=inplace, expect_fast=True)
+    _run(spec(N=1, Ci=24, Co=40, T=2, Tc=2, H=11, W=37), mode=mode, pro=pro, res=res,
+         inplace=inplace, expect_fast=True)
 
 
 @pytest.mark.parametrize("over", [dict(N=1, Ci=128, Co=128, T=1, Tc=2, H=16, W=32),

@@ -7,6 +7,8 @@ The cases and the kernel each one reaches are in fuzz_cases.py (checked on
 the CPU by test_fuzz_cases.py)."""
 import pytest
 
+from paper_2609_31938_amd import c3c
+
 from fuzz_cases import cases
 from test_gpu_parity import _case
 
@@ -21,4 +23,4 @@ def test_fuzz(i):
     ctx, _, m = _case(sp, dtype, mode, seed=1000 + i, ws=ws, kernel=kernel)
     c = ctx.counters()
     assert c["calls"] == 1 and c["failed"] == c["fast_error"] == 0
-    assert c["fast"] == (0 if mode or kernel == "fallback_direct" else 1)
+    assert c["fast"] == (0 if mode & c3c.MODE_FORCE_FALLBACK or kernel == "fallback_direct" else 1)

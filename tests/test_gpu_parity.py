@@ -155,6 +155,41 @@ def test_fast_route_matches_oracle(dtype, over):
     say(f"  rel={m['rel']:.3e} cos={m['cos']:.8f}")
 
 
+# An unsplit call whose tiles fill less than one round of the compute units
+# may take 64-channel 4x64 tiles (two output-channel fragments per wave);
+# C3C_MODE_CHANNEL_TILES keeps the tile its output-channel count selects.
+# These cases (above, and a few more for the smaller tile: W not a multiple
+# of 8, temporal dilation, five taps) run on both tilings: each against the
+# oracle, the two outputs and caches bit-identical (every output element's
+# products are accumulated in the same order on every tile).
+RETILED = [
+    (dict(N=1, Ci=64, Co=192, T=4, Tc=2, H=16, W=64), (192, 4, 64)),
+    (dict(N=1, Ci=64, Co=160, T=3, Tc=2, H=22, W=170), (160, 4, 80)),
+    (dict(N=1, Ci=72, Co=130, T=2, Tc=2, H=13, W=96), (160, 4, 80)),
+    (dict(N=2, Ci=40, Co=181, T=2, Tc=1, H=9, W=83), (128, 4, 80)),
+    (dict(N=1, Ci=48, Co=320, T=2, Tc=2, H=10, W=88), (160, 4, 80)),
+    (dict(N=1, Ci=40, Co=256, T=2, Tc=2, H=9, W=90), (128, 4, 80)),
+    (dict(N=1, Ci=40, Co=128, T=2, Tc=2, H=9, W=70), (128, 4, 80)),
+    (dict(N=1, Ci=24, Co=128, T=3, Tc=4, H=8, W=64, d_t=2, p_base=4), (128, 4, 80)),
+    (dict(N=1, Ci=20, Co=100, T=2, Tc=2, H=7, W=72, Kt=5, p_base=4), (128, 4, 80)),
+]
+
+
+@pytest.mark.parametrize("over,tile", RETILED)
+def test_small_tiles_match_the_channel_tiles(over, tile):
+    sp = spec(**over)
+    plans = [c3c.plan_query(c3c.Context(m), sp, "bf16") for m in (0, c3c.MODE_CHANNEL_TILES)]
+    assert [(p["tile_co"], p["tile_h"], p["tile_w"]) for p in plans] == [(64, 4, 64), tile], plans
+    outs = []
+    for mode in (0, c3c.MODE_CHANNEL_TILES):
+        ctx, y, m = _case(sp, "bf16", mode, kernel="conv3d_bf16")
+        c = ctx.counters()
+        assert (c["calls"], c["fast"], c["fallback"]) == (1, 1, 0)
+        say(f"  mode={mode} rel={m['rel']:.3e} cos={m['cos']:.8f}")
+        outs.append(host(y).view(torch.int16))
+    assert torch.equal(outs[0], outs[1])
+
+
 # ---------------------------------------------------------------- fallback route
 
 FALLBACK_CASES = FAST_CASES + [

@@ -118,8 +118,11 @@ def test_context_modes():
     assert ctx.mode == 0
     ctx.mode = c3c.MODE_STRICT | c3c.MODE_FORCE_FALLBACK
     assert ctx.mode == 3
+    ctx.mode = c3c.MODE_CHANNEL_TILES | c3c.MODE_STRICT
+    assert ctx.mode == 9
     with pytest.raises(c3c.C3CError):
-        ctx.mode = 8
+        ctx.mode = 16
+    assert ctx.mode == 9
     h = C.c_void_p()
     assert c3c.lib.c3c_ctx_create(16, C.byref(h)) == c3c.E_INVAL
     assert c3c.lib.c3c_ctx_create(0, None) == c3c.E_INVAL
@@ -347,8 +350,8 @@ def test_plan_of_the_workloads():
     want = {
         "c32_32x32": ("fast_f32", 32, 4, 32, 1),
         # one output frame, 60 tiles of 192 x 4 x 64: unsplit (no workspace),
-        # the 128 x 4 x 80 tiling (90 workgroups, less work in the round)
-        "c384_60x104": ("conv3d_bf16", 128, 4, 80, 1),
+        # the 64 x 4 x 64 tiling (180 workgroups, less modelled time)
+        "c384_60x104": ("conv3d_bf16", 64, 4, 64, 1),
         "c192_240x416": ("conv3d_bf16", 192, 4, 64, 1),
         "c384to192_240x416": ("conv3d_bf16", 192, 4, 64, 1),
         "c96_480x832": ("conv3d_bf16", 96, 6, 64, 1),
@@ -444,10 +447,38 @@ def test_plan_of_the_160_channel_parity_cases():
             (dict(N=1, Ci=40, Co=256, T=2, Tc=2, H=9, W=90), (128, 4, 80)),
             (dict(N=1, Ci=48, Co=320, T=2, Tc=2, H=10, W=88), (160, 4, 80)),
             (dict(N=1, Ci=40, Co=150, T=4, Tc=2, H=333, W=30), (160, 10, 32))]
+    ctx = c3c.Context(c3c.MODE_CHANNEL_TILES)
     for over, tile in want:
-        pl = c3c.plan_query(None, spec(**over), "bf16")
+        pl = c3c.plan_query(ctx, spec(**over), "bf16")
         assert pl["kernel"] == "conv3d_bf16"
         assert (pl["tile_co"], pl["tile_h"], pl["tile_w"]) == tile, (over, pl)
+
+
+@no_gpu
+def test_unsplit_calls_that_fill_few_compute_units_take_smaller_tiles():
+    """An unsplit bf16 3x3 call whose tiles fill less than one round of the
+    compute units takes, of its own tiling, the 128 x 4x80 tiling (from the
+    192-channel one) and the 64 x 4x64 tiling, the one of least rounds x tile
+    work x c (c = 1.7 for the 64-channel tile, 1 for the others).  A call
+    that splits, and C3C_MODE_CHANNEL_TILES, keep the output-channel tiling;
+    a call that fills the device is never re-tiled."""
+    def tile(sp, ctx=None, ws=0):
+        pl = c3c.plan_query(ctx, sp, "bf16", ws)
+        return pl["tile_co"], pl["tile_h"], pl["tile_w"], pl["workgroups"], pl["splits"]
+    c2 = spec(N=1, Ci=384, Co=384, T=1, Tc=2, H=60, W=104)
+    assert tile(c2) == (64, 4, 64, 6 * 2 * 15, 1)
+    assert tile(c2, c3c.Context(c3c.MODE_CHANNEL_TILES)) == (192, 4, 64, 60, 1)
+    assert tile(c2, ws=c3c.workspace_bytes(c2, "bf16")) == (192, 4, 64, 4 * 60, 4)
+    # two output frames: 180 workgroups of 128 x 4x80 (cost 1 x 40960) against
+    # two rounds of 360 of 64 x 4x64 (2 x 16384 x 1.7 = 55706)
+    assert tile(dict(c2, T=2)) == (128, 4, 80, 3 * 2 * 15 * 2, 1)
+    # 192 -> 192: 30 workgroups of 192 x 4x64 (128 x 4x80 pads to 256 channels)
+    assert tile(spec(N=1, Ci=192, Co=192, T=1, Tc=2, H=60, W=104)) == (64, 4, 64, 90, 1)
+    # a full round of 192-channel tiles stays
+    big = spec(N=1, Ci=192, Co=192, T=4, Tc=2, H=240, W=416)
+    assert tile(big)[:3] == (192, 4, 64)
+    # 96 channels or fewer keep their own tiles
+    assert tile(spec(N=1, Ci=96, Co=96, T=1, Tc=2, H=20, W=64))[:3] == (96, 6, 64)
 
 
 @no_gpu
