@@ -419,6 +419,25 @@ __global__ __launch_bounds__(64 * WAVES_CO * WAVES_PX, 1) void conv3d_bf16(Args 
   for (int cf = 0; cf < WCO; ++cf)
     wv[cf] = static_cast<uint32_t>(lane) * 16u +
              static_cast<uint32_t>(min(cofrag0 + cf, a.cofrags - 1)) * 1024u;
+  // The bias of this lane's output channel in each fragment, all loaded
+  // before the epilogue's first store: loaded fragment by fragment between
+  // the stores, each load's wait also waited for every store before it.  The
+  // plain aligned form loads them here and holds them through the main loop;
+  // the fused and unaligned forms, whose main loops have no registers to
+  // spare, at the start of the epilogue (with the residual batch).  A channel
+  // past Co, or no bias: an out-of-range offset, 0.
+  float bias_v[WCO] = {};
+  auto load_bias = [&]() {
+    const __amdgpu_buffer_rsrc_t brs = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t*>(a.bias), 0, a.has_bias ? a.Co * 2 : 0, 0x00020000);
+#pragma unroll
+    for (int cf = 0; cf < WCO; ++cf) {
+      const uint32_t co = static_cast<uint32_t>((cofrag0 + cf) * 16 + (lane & 15));
+      bias_v[cf] = __uint_as_float(static_cast<uint32_t>(__builtin_amdgcn_raw_buffer_load_b16(brs, 2u * co, 0, 0))
+                                   << 16);
+    }
+  };
+  if constexpr (!SPLIT && FU == 0 && ALIGNED) load_bias();
   auto load_w = [&](uint32_t wbase, int ij, u32x4 (&dst)[WCO]) {
     const uint32_t so = wbase + static_cast<uint32_t>(ij) * wrow;
 #pragma unroll
@@ -569,6 +588,7 @@ __global__ __launch_bounds__(64 * WAVES_CO * WAVES_PX, 1) void conv3d_bf16(Args 
   // RES: every fragment's residual values, loaded as one batch before any
   // store (branch-free: a position outside the output reads the residual's
   // first element and is not used), so the block waits for memory once
+  if constexpr (FU != 0 || !ALIGNED) load_bias();
   uint2 rv[RES ? WCO : 1][RES ? NPF : 1];
   if constexpr (RES) {
     const bool has_r = a.residual != nullptr;
@@ -596,7 +616,7 @@ __global__ __launch_bounds__(64 * WAVES_CO * WAVES_PX, 1) void conv3d_bf16(Args 
 #pragma unroll
   for (int cf = 0; cf < WCO; ++cf) {
     const int co = (cofrag0 + cf) * 16 + (lane & 15);
-    const float bb = (a.has_bias && co < a.Co) ? __uint_as_float(static_cast<uint32_t>(a.bias[co]) << 16) : 0.f;
+    const float bb = bias_v[cf];
 #pragma unroll
     for (int pf = 0; pf < NPF; ++pf) {
       const int h = h0 + wpx * WR + pf / WCF, w = w0 + (pf % WCF) * 16 + 4 * (lane >> 4);

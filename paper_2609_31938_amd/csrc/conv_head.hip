@@ -141,6 +141,17 @@ __global__ __launch_bounds__(256, 1) void conv_head(HeadArgs a) {
   constexpr uint32_t OOB = 0x80000000u;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  // the bias of every output channel (Co <= 5), loaded at the start: loaded
+  // in the gather loop, each load's wait also waited for the stores before
+  // it (no bias, or a channel past Co: an out-of-range offset, 0)
+  float bias_c[5];
+  {
+    const __amdgpu_buffer_rsrc_t brs = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t*>(a.bias), 0, a.has_bias ? a.Co * 2 : 0, 0x00020000);
+#pragma unroll
+    for (int c = 0; c < 5; ++c)
+      bias_c[c] = __uint_as_float(static_cast<uint32_t>(__builtin_amdgcn_raw_buffer_load_b16(brs, 2u * c, 0, 0)) << 16);
+  }
 
   // workgroups numbered so that each XCD runs a contiguous range of
   // neighbouring spatial tiles (their windows overlap in the halo rows)
@@ -428,7 +439,7 @@ __global__ __launch_bounds__(256, 1) void conv_head(HeadArgs a) {
         const int r = rem / (OC / 4), c4 = rem % (OC / 4);
         const int h = h0 + r, w = w0 + 4 * c4, o = og0 + u0 + du;
         if (h >= a.H || w >= a.W) continue;
-        const float bb = a.has_bias ? __uint_as_float(static_cast<uint32_t>(a.bias[co]) << 16) : 0.f;
+        const float bb = co == 0 ? bias_c[0] : co == 1 ? bias_c[1] : co == 2 ? bias_c[2] : co == 3 ? bias_c[3] : bias_c[4];
         float s4[4] = {bb, bb, bb, bb};
 #pragma unroll
         for (int i = 0; i < 3; ++i)

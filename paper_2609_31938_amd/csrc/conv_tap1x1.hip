@@ -235,6 +235,20 @@ __global__ __launch_bounds__(256, 2) void conv_tap1x1(TapArgs a) {
   for (int cf = 0; cf < WCO; ++cf)
     w_off[cf] = static_cast<uint32_t>(min(ctile * (TCO / 16) + wco * WCO + cf, a.cofrags - 1)) * 1024u +
                 static_cast<uint32_t>(lane) * 16u;
+  // the bias of this lane's output channel in each fragment, loaded here:
+  // loaded in the epilogue, each fragment's load waited for every store
+  // before it (a channel past Co, or no bias: an out-of-range offset, 0)
+  float bias_v[WCO];
+  {
+    const __amdgpu_buffer_rsrc_t brs = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t*>(a.bias), 0, a.has_bias ? a.Co * 2 : 0, 0x00020000);
+#pragma unroll
+    for (int cf = 0; cf < WCO; ++cf) {
+      const uint32_t co = static_cast<uint32_t>(ctile * TCO + wco * 16 * WCO + cf * 16 + (lane & 15));
+      bias_v[cf] = __uint_as_float(static_cast<uint32_t>(__builtin_amdgcn_raw_buffer_load_b16(brs, 2u * co, 0, 0))
+                                   << 16);
+    }
+  }
   // weights are loaded in order: stage ws is tap k_lo + ws / chunks, chunk
   // ws % chunks, packed row k_lo * chunks + ws (wrow its byte offset)
   int ws = 0;
@@ -311,7 +325,7 @@ __global__ __launch_bounds__(256, 2) void conv_tap1x1(TapArgs a) {
   for (int cf = 0; cf < WCO; ++cf) {
     const int co = ctile * TCO + wco * 16 * WCO + cf * 16 + (lane & 15);
     if (co >= a.Co) continue;
-    const float bb = a.has_bias ? __uint_as_float(static_cast<uint32_t>(a.bias[co]) << 16) : 0.f;
+    const float bb = bias_v[cf];
     uint16_t* yrow = ybase + static_cast<int64_t>(co) * a.To * a.hw;
 #pragma unroll
     for (int pf = 0; pf < NPF; ++pf) {
@@ -484,6 +498,19 @@ __global__ __launch_bounds__(256, 1) void conv_tap1x1_chunk(TapArgs a) {
   for (int cf = 0; cf < WCO; ++cf)
     w_off[cf] = static_cast<uint32_t>(min(ctile * (TCO / 16) + wv * WCO + cf, a.cofrags - 1)) * 1024u +
                 static_cast<uint32_t>(lane) * 16u;
+  // the bias of this lane's output channel in each fragment, loaded here (as
+  // in the kernel above)
+  float bias_v[WCO];
+  {
+    const __amdgpu_buffer_rsrc_t brs = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t*>(a.bias), 0, a.has_bias ? a.Co * 2 : 0, 0x00020000);
+#pragma unroll
+    for (int cf = 0; cf < WCO; ++cf) {
+      const uint32_t co = static_cast<uint32_t>(ctile * TCO + wv * 16 * WCO + cf * 16 + (lane & 15));
+      bias_v[cf] = __uint_as_float(static_cast<uint32_t>(__builtin_amdgcn_raw_buffer_load_b16(brs, 2u * co, 0, 0))
+                                   << 16);
+    }
+  }
   auto load_w = [&](int c, u32x4 (&v)[KTG][WCO]) {
 #pragma unroll
     for (int k = 0; k < KTG; ++k) {
@@ -602,7 +629,7 @@ __global__ __launch_bounds__(256, 1) void conv_tap1x1_chunk(TapArgs a) {
   for (int cf = 0; cf < WCO; ++cf) {
     const int co = ctile * TCO + wv * 16 * WCO + cf * 16 + (lane & 15);
     if (co >= a.Co) continue;
-    const float bb = a.has_bias ? __uint_as_float(static_cast<uint32_t>(a.bias[co]) << 16) : 0.f;
+    const float bb = bias_v[cf];
     uint16_t* yrow = ybase + static_cast<int64_t>(co) * a.To * a.hw;
 #pragma unroll
     for (int pf = 0; pf < NPF; ++pf) {

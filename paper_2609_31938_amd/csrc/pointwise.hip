@@ -315,6 +315,18 @@ __global__ __launch_bounds__(PW_NT, 1) void pointwise_conv(PwArgs a) {
   // weight operand: lane l holds w[co = frag * 16 + l % 16][ci = 8 (l / 16) .. + 7]
   // (unpacked rows of PW_WPITCH bytes, or the packed fragment's lane slot)
   const int cof0 = ctile * PW_CO + wco * 16 * PW_WCO + (lane & 15);
+  // the bias of this lane's output channel in each fragment, loaded here:
+  // loaded in the epilogue, each fragment's load waited for every store
+  // before it (a channel past Co, or no bias: an out-of-range offset, 0)
+  float bias_v[PW_WCO];
+  {
+    const __amdgpu_buffer_rsrc_t brs = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t*>(a.bias), 0, a.has_bias ? a.Co * 2 : 0, 0x00020000);
+#pragma unroll
+    for (int cf = 0; cf < PW_WCO; ++cf)
+      bias_v[cf] = from_b16(__builtin_amdgcn_raw_buffer_load_b16(brs, 2u * static_cast<uint32_t>(cof0 + 16 * cf), 0, 0),
+                            F16);
+  }
   const int rb = PACKED ? PW_WOFF + wco * PW_WCO * 1024 + lane * 16
                         : PW_WOFF + (wco * 16 * PW_WCO + j) * PW_WPITCH + 16 * g;
   auto read_b = [&](int buf, int cf) {
@@ -361,7 +373,7 @@ __global__ __launch_bounds__(PW_NT, 1) void pointwise_conv(PwArgs a) {
   for (int cf = 0; cf < PW_WCO; ++cf) {
     const int co = cof0 + 16 * cf;
     if (co >= a.Co) continue;
-    const float bb = a.has_bias ? from_b16(a.bias[co], F16) : 0.f;
+    const float bb = bias_v[cf];
     uint16_t* yrow = ybase + static_cast<int64_t>(co) * a.To * a.hw;
     // RES: this fragment row's residual values, loaded as one batch before
     // its stores (branch-free: a pixel past the plane reads the row's first
@@ -545,6 +557,20 @@ __global__ __launch_bounds__(PW_NT, 1) void pointwise_resident(PwArgs a, int til
   };
   const int j = lane & 15, gq = lane >> 4;
   const int ra = pw_row(NPF, 8 * gq + (j >> 2)) + (wpx * 16 * NPF + 4 * (j & 3)) * 2;
+  // the bias of this lane's output channel in each fragment, the same for
+  // every tile: loaded once here (loaded in each tile's epilogue, every
+  // fragment's load waited for the tile's earlier stores; a channel past Co,
+  // or no bias: an out-of-range offset, 0)
+  float bias_v[PW_WCO];
+  {
+    const __amdgpu_buffer_rsrc_t brs = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t*>(a.bias), 0, a.has_bias ? a.Co * 2 : 0, 0x00020000);
+#pragma unroll
+    for (int cf = 0; cf < PW_WCO; ++cf)
+      bias_v[cf] = from_b16(
+          __builtin_amdgcn_raw_buffer_load_b16(brs, 2u * static_cast<uint32_t>(wco * 16 * PW_WCO + 16 * cf + j), 0, 0),
+          F16);
+  }
   auto read_a = [&](int buf, int pf) {
     const unsigned char* p = lds + PW_RES_W + buf * ABUF + ra + pf * 32;
     const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p));
@@ -617,7 +643,7 @@ __global__ __launch_bounds__(PW_NT, 1) void pointwise_resident(PwArgs a, int til
 #pragma unroll
         for (int cf = 0; cf < PW_WCO; ++cf) {
           const int co = wco * 16 * PW_WCO + 16 * cf + j;
-          const float bb = (a.has_bias && co < a.Co) ? from_b16(a.bias[co], F16) : 0.f;
+          const float bb = bias_v[cf];
           uint16_t* yrow = a.y + toff + static_cast<int64_t>(co) * a.To * a.hw;
 #pragma unroll
           for (int pf = 0; pf < NPF; ++pf) {

@@ -190,6 +190,32 @@ def test_small_tiles_match_the_channel_tiles(over, tile):
     assert torch.equal(outs[0], outs[1])
 
 
+# No bias (has_bias = 0) on every kernel that loads the bias before its
+# epilogue: the 3x3 kernel's 96-, 64- (W not a multiple of 8) and 160-channel
+# tiles, both 1x1 kernels of the temporal route (several output frames, and
+# one), the pointwise kernel on the fast route and, for a 1x1x1 call, on the
+# fallback, and the head kernel.
+NO_BIAS = [
+    (dict(N=1, Ci=48, Co=80, T=3, Tc=2, H=37, W=72), "conv3d_bf16"),
+    (dict(N=1, Ci=40, Co=200, T=2, Tc=2, H=9, W=37), "conv3d_bf16"),
+    (dict(N=1, Ci=40, Co=160, T=4, Tc=2, H=64, W=160), "conv3d_bf16"),
+    (dict(N=1, Ci=64, Co=384, T=4, Tc=2, H=32, W=64, Kh=1, Kw=1), "tap1x1"),
+    (dict(N=1, Ci=64, Co=384, T=1, Tc=2, H=64, W=128, Kh=1, Kw=1), "tap1x1"),
+    (dict(N=1, Ci=64, Co=96, T=3, Tc=2, H=8, W=40, Kh=1, Kw=1), "pointwise"),
+    (dict(N=1, Ci=64, Co=96, T=2, Tc=0, H=16, W=64, Kt=1, Kh=1, Kw=1), "pointwise"),
+    (dict(N=1, Ci=96, Co=3, T=2, Tc=2, H=12, W=48), "head"),
+]
+
+
+@pytest.mark.parametrize("over,kernel", NO_BIAS)
+def test_no_bias_matches_oracle(over, kernel):
+    sp = spec(**over, has_bias=0)
+    ctx, _, m = _case(sp, "bf16", kernel=kernel)
+    c = ctx.counters()
+    assert c["calls"] == 1 and c["failed"] == c["fast_error"] == 0
+    say(f"  rel={m['rel']:.3e} cos={m['cos']:.8f}")
+
+
 # ---------------------------------------------------------------- fallback route
 
 FALLBACK_CASES = FAST_CASES + [
