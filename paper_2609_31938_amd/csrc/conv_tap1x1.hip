@@ -433,33 +433,37 @@ __global__ __launch_bounds__(256, 1) void conv_tap1x1_chunk(TapArgs a) {
     d_px[i] = ((static_cast<uint32_t>(lane) & 15u) ^ seg_swizzle(r)) * 16u;
   }
   const int64_t cs_c = static_cast<int64_t>(a.Tc) * a.hw, cs_x = static_cast<int64_t>(a.T) * a.hw;
-  // slot r, channels 32 c ..: the chunk's real rows from pixel px0 (at most
-  // 32 channel planes: 32-bit sizes); empty (zeros) for a slot that is not
-  // live or a chunk past the last
-  auto act_rsrc = [&](int r, int c, uint32_t& cs) {
-    const int f = slot_frame(r), c0 = c * TK;
-    const bool real = ((live >> r) & 1u) && c < a.chunks;
+  // slot r's source, built once: every channel of its frame from pixel px0
+  // (32-bit sizes: the launcher checks the extent), empty (zeros) for a slot
+  // that is not live.  A stage adds its chunk's 32 channel planes to the
+  // lanes' offsets, so the channels past Ci and a chunk past the last are
+  // out-of-range offsets and read zeros.
+  __amdgpu_buffer_rsrc_t srs[NR];
+  uint32_t scs[NR];
+#pragma unroll
+  for (int r = 0; r < NR; ++r) {
+    const int f = slot_frame(r);
+    const bool real = (live >> r) & 1u;
     const bool in_cache = f < a.Tc;
     const int64_t cstride = in_cache ? cs_c : cs_x;
     const uint16_t* base = in_cache ? a.cache : a.x;
     const int64_t off = static_cast<int64_t>(in_cache ? f : f - a.Tc) * a.hw +
-                        static_cast<int64_t>(n) * a.Ci * cstride + px0 + c0 * cstride;
-    cs = static_cast<uint32_t>(cstride * 2);
+                        static_cast<int64_t>(n) * a.Ci * cstride + px0;
+    scs[r] = static_cast<uint32_t>(cstride * 2);
     const uint32_t bytes =
-        real ? static_cast<uint32_t>(min(TK, a.Ci - c0) - 1) * cs + static_cast<uint32_t>(a.hw - px0) * 2u : 0u;
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(real ? base + off : a.x), 0,
-                                             static_cast<int>(bytes), 0x00020000);
-  };
+        real ? static_cast<uint32_t>(a.Ci - 1) * scs[r] + static_cast<uint32_t>(a.hw - px0) * 2u : 0u;
+    srs[r] = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(real ? base + off : a.x), 0,
+                                               static_cast<int>(bytes), 0x00020000);
+  }
   // chunk c's tiles into the LDS buffer at L (2 NR loads per lane)
   auto stage_act = [&](int c, unsigned char* L) {
 #pragma unroll
     for (int r = 0; r < NR; ++r) {
-      uint32_t cs;
-      const __amdgpu_buffer_rsrc_t rs = act_rsrc(r, c, cs);
+      const uint32_t add = static_cast<uint32_t>(c * TK) * scs[r];
 #pragma unroll
       for (int i = 0; i < 2; ++i)
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void*)(L + r * GTILE + (4 * i + wv) * 1024), 16,
-                                                 d_row[i] * cs + d_px[i], 0, 0, 0);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(srs[r], (lds_void*)(L + r * GTILE + (4 * i + wv) * 1024), 16,
+                                                 d_row[i] * scs[r] + d_px[i] + add, 0, 0, 0);
     }
   };
   // the new cache [N][Ci][L][H*W] (frame f is its frame f - (Z - L)):
@@ -719,7 +723,11 @@ hipError_t launch_tap1x1(const Geo& g, const void* x, const void* cache, const v
   a.write_cache = 0;
   // the chunk-stage form for one output frame (Kt <= 3), else one stage per
   // tap and chunk
-  const bool chunk_form = g.To == 1 && d.Kt <= KTG;
+  // (its source offsets span every channel of a frame, three chunks past the
+  // last included, in 32 bits)
+  const int64_t frames = d.T > d.Tc ? d.T : d.Tc;
+  const bool chunk_form = g.To == 1 && d.Kt <= KTG &&
+                          (d.Ci + 3 * TK) * frames * d.H * d.W * 2 < 0x7fffffff;
   // the new cache from the staged tiles when every frame of it is staged
   // (32-bit offsets within a 32-channel slab of it; a tap mask of 32 bits)
   a.write_cache = g.L > 0 && cache_out != nullptr && aligned_to(cache_out, 16) && d.Kt <= 32 &&
