@@ -397,15 +397,14 @@ __global__ __launch_bounds__(256, 1) void conv_tap1x1_chunk(TapArgs a) {
   const int ctile = b % a.co_tiles;
   b /= a.co_tiles;
   const int pt = b % a.px_tiles;
-  b /= a.px_tiles;
-  const int t = b % a.To;
-  const int n = b / a.To;
+  // one output frame (t = 0: the launcher takes this form only for To = 1)
+  const int n = b / a.px_tiles;
   const int px0 = pt * TPX;
 
-  // slot r (tap r) reads frame F0 + r d_t; live: r < Kt and the frame in
-  // [0, Z); cwm: live, a frame of the new cache, and read by no earlier
-  // output frame (t' < t with t' s_t = f + p_l - k d_t)
-  const int F0 = t * a.st - a.p_l;
+  // slot r (tap r) reads frame r d_t - p_l; live: r < Kt and the frame in
+  // [0, Z); cwm: live and a frame of the new cache (no earlier output frame
+  // has read it: there is none)
+  const int F0 = -a.p_l;
   auto slot_frame = [&](int r) { return F0 + r * a.dt; };
   uint32_t live = 0, cwm = 0;
 #pragma unroll
@@ -413,13 +412,7 @@ __global__ __launch_bounds__(256, 1) void conv_tap1x1_chunk(TapArgs a) {
     const int f = slot_frame(r);
     if (r >= a.Kt || f < 0 || f >= a.Z) continue;
     live |= 1u << r;
-    if (!a.write_cache || ctile != 0 || f < a.Z - a.L) continue;
-    bool before = false;
-    for (int k = 0; k < a.Kt; ++k) {
-      const int kd = f + a.p_l - k * a.dt;
-      if (kd >= 0 && kd % a.st == 0 && kd / a.st < t) before = true;
-    }
-    if (!before) cwm |= 1u << r;
+    if (a.write_cache && ctile == 0 && f >= a.Z - a.L) cwm |= 1u << r;
   }
 
   // staging: this wave's two 1 KiB blocks of a tile are rows 4 (4 i + wv)
@@ -469,25 +462,27 @@ __global__ __launch_bounds__(256, 1) void conv_tap1x1_chunk(TapArgs a) {
   // the new cache [N][Ci][L][H*W] (frame f is its frame f - (Z - L)):
   // chunk c's cache slots copied from the LDS buffer at L, 16 bytes a lane,
   // rows as staged (segment permutation undone on the way out)
+  // (one resource over batch element n's new cache, every channel and frame,
+  // built once: 32-bit sizes, the launcher checks the extent; a channel past
+  // Ci is an out-of-range offset and its stores are dropped)
   const int64_t cl = static_cast<int64_t>(a.L) * a.hw;
+  const uint32_t ccs = static_cast<uint32_t>(cl * 2);
+  const __amdgpu_buffer_rsrc_t crs = __builtin_amdgcn_make_buffer_rsrc(
+      cwm != 0 ? a.cache_out + static_cast<int64_t>(n) * a.Ci * cl : a.y, 0,
+      cwm != 0 ? static_cast<int>(static_cast<uint32_t>(a.Ci) * ccs) : 0, 0x00020000);
   auto copy_cache = [&](int c, const unsigned char* L) {
-    const int c0 = c * TK;
-    const uint32_t ccs = static_cast<uint32_t>(cl * 2);
-    const uint32_t cbytes = static_cast<uint32_t>(min(TK, a.Ci - c0) - 1) * ccs + static_cast<uint32_t>(a.hw) * 2u;
+    const uint32_t cadd = static_cast<uint32_t>(c * TK) * ccs;
 #pragma unroll
     for (int r = 0; r < NR; ++r) {
       if (!((cwm >> r) & 1u)) continue;
-      const __amdgpu_buffer_rsrc_t crs = __builtin_amdgcn_make_buffer_rsrc(
-          a.cache_out + (static_cast<int64_t>(n) * a.Ci + c0) * cl +
-              static_cast<int64_t>(slot_frame(r) - (a.Z - a.L)) * a.hw,
-          0, static_cast<int>(cbytes), 0x00020000);
+      const uint32_t fo = static_cast<uint32_t>(slot_frame(r) - (a.Z - a.L)) * static_cast<uint32_t>(a.hw) * 2u + cadd;
 #pragma unroll
       for (int i = 0; i < 2; ++i) {
         const uint32_t q = static_cast<uint32_t>(tid + 256 * i), row = q >> 4, ls = q & 15u;
         const u32x4 v = *reinterpret_cast<const u32x4*>(L + r * GTILE + q * 16);
         const uint32_t px = px0 + (ls ^ seg_swizzle(row)) * 8u;
-        __builtin_amdgcn_raw_buffer_store_b128(v, crs, px < static_cast<uint32_t>(a.hw) ? row * ccs + px * 2 : OOB,
-                                               0, 0);
+        __builtin_amdgcn_raw_buffer_store_b128(v, crs,
+                                               px < static_cast<uint32_t>(a.hw) ? row * ccs + px * 2 + fo : OOB, 0, 0);
       }
     }
   };
@@ -628,7 +623,7 @@ __global__ __launch_bounds__(256, 1) void conv_tap1x1_chunk(TapArgs a) {
 
   // epilogue: lane l holds pixels 4 (l / 16) .. + 3 of output channel l % 16
   // of each fragment; bias once, one round-to-nearest-even, NCTHW store
-  uint16_t* ybase = a.y + (static_cast<int64_t>(n) * a.Co * a.To + t) * a.hw;
+  uint16_t* ybase = a.y + static_cast<int64_t>(n) * a.Co * a.To * a.hw;
 #pragma unroll
   for (int cf = 0; cf < WCO; ++cf) {
     const int co = ctile * TCO + wv * 16 * WCO + cf * 16 + (lane & 15);
@@ -724,10 +719,10 @@ hipError_t launch_tap1x1(const Geo& g, const void* x, const void* cache, const v
   // the chunk-stage form for one output frame (Kt <= 3), else one stage per
   // tap and chunk
   // (its source offsets span every channel of a frame, three chunks past the
-  // last included, in 32 bits)
-  const int64_t frames = d.T > d.Tc ? d.T : d.Tc;
+  // last included, and its new-cache offsets every channel and frame, in 32
+  // bits)
   const bool chunk_form = g.To == 1 && d.Kt <= KTG &&
-                          (d.Ci + 3 * TK) * frames * d.H * d.W * 2 < 0x7fffffff;
+                          (d.Ci + 3 * TK) * (d.T + d.Tc) * d.H * d.W * 2 < 0x7fffffff;
   // the new cache from the staged tiles when every frame of it is staged
   // (32-bit offsets within a 32-channel slab of it; a tap mask of 32 bits)
   a.write_cache = g.L > 0 && cache_out != nullptr && aligned_to(cache_out, 16) && d.Kt <= 32 &&
