@@ -126,9 +126,9 @@ def _run(sp, mode=0, res=True, inplace=False, seed=0, ctx=None, x=None, cache=No
 
 
 CASES = [
-    (dict(N=1, Ci=64, Co=160, T=2, Tc=2, H=24, W=80), "conv3d_bf16"),     # 160-channel tile
+    (dict(N=1, Ci=64, Co=160, T=2, Tc=2, H=24, W=80), "conv3d_bf16"),     # 160 channels
     (dict(N=1, Ci=48, Co=80, T=3, Tc=2, H=37, W=72), "conv3d_bf16"),      # 96-channel tile
-    (dict(N=2, Ci=40, Co=192, T=2, Tc=1, H=16, W=64), "conv3d_bf16"),     # 192-channel tile, N = 2
+    (dict(N=2, Ci=40, Co=192, T=2, Tc=1, H=16, W=64), "conv3d_bf16"),     # 192 channels, N = 2
     (dict(N=1, Ci=32, Co=3, T=2, Tc=2, H=20, W=40), "head"),              # head kernel (no residual)
     (dict(N=1, Ci=24, Co=40, T=2, Tc=2, H=11, W=37), "conv3d_bf16"),      # H*W not a multiple of 8
     (dict(N=1, Ci=320, Co=96, T=2, Tc=3, H=9, W=16), "conv3d_bf16"),      # many channels, p_l < 0
@@ -148,6 +148,19 @@ def test_block_matches_oracle(i):
     fast = c3c.route_query(None, sp, "bf16")[0] == "fast"
     # the head kernel serves calls without a residual
     _run(sp, expect_fast=fast, kernel=kernel, res=kernel != "head")
+
+
+@pytest.mark.parametrize("i,tile", [(0, (160, 4, 80)), (2, (192, 4, 64))])
+def test_block_on_the_channel_tiles(i, tile):
+    """The 160- and 192-channel cases above fill few compute units and run on
+    64-channel 4x64 tiles; C3C_MODE_CHANNEL_TILES keeps their own tiles."""
+    over, kernel = CASES[i]
+    sp = spec(**over)
+    need = c3c.block_workspace_bytes(sp)
+    for mode, want in ((0, (64, 4, 64)), (c3c.MODE_CHANNEL_TILES, tile)):
+        pl = c3c.plan_query(c3c.Context(mode), sp, "bf16", need)
+        assert (pl["tile_co"], pl["tile_h"], pl["tile_w"]) == want, pl
+    _run(sp, mode=c3c.MODE_CHANNEL_TILES, expect_fast=True, kernel=kernel)
 
 
 def test_block_split_k_uses_the_rest_of_the_workspace():
